@@ -1,0 +1,168 @@
+/*
+ * muon_hip.h — C ABI of the MI355X (gfx950) batched Muon step.
+ *
+ * The operation (HyperParallel-FSDP, arXiv 2609.21594):
+ *   Sec. 2.3, Eq. (1): accumulate momentum, normalise X0 = G/(||G||_F + eps),
+ *     run K Newton-Schulz steps X <- a_k X + b_k (X X^T) X + c_k (X X^T)^2 X,
+ *     rescale by 0.2*sqrt(max(m, n)) (RMS matching);
+ *   Sec. 6.6: transpose-first (rows > cols runs on the transpose), shape-fused
+ *     batches capped at 2^29 elements, workspace allocated once per batched
+ *     invocation, descending-size batch order;
+ *   Sec. 6.3: an [E, M, N] expert weight is E independent M x N matrices;
+ *   Sec. 6.4 / 6.2 (local programming model): each device sees its own
+ *     gradients, momentum and parameters and applies the update with
+ *     decoupled weight decay.
+ *
+ * Readings where the paper prints no formula (the kernels follow these):
+ *   momentum   buf' = beta*buf + (1-beta)*g ;
+ *              u = (1-beta)*g + beta*buf' (nesterov) or u = buf'
+ *   update     W' = (1 - lr*wd) * W - lr * scale * O,
+ *              scale = 0.2*sqrt(max(rows, cols)) (scale_mode 0) or 1 (mode 1)
+ *   eps        added to the Frobenius norm, outside the square root
+ *   square     matrices (rows == cols) are not transposed
+ *   ns_coeffs  NULL selects the constant quintic (3.4445, -4.7750, 2.0315).
+ *
+ * Conventions for every entry point:
+ *   - Device pointers are HIP device addresses on the handle's device; host
+ *     pointers (arrays of descriptors, coefficient tables) are read during
+ *     the call only and may be freed when it returns.
+ *   - Matrices are dense and row-major: element (i, j) of an entry sits at
+ *     base + (e*rows + i)*cols + j for plane e of a stacked entry.
+ *   - All work is enqueued on `stream` (a hipStream_t; NULL is the null
+ *     stream) and the call returns without waiting for it.  Every buffer the
+ *     caller passes must stay alive until that work has completed.
+ *   - Every argument is checked before the first launch: a call that returns
+ *     an error other than MUON_ERR_DEVICE changed nothing.  Values inside the
+ *     tensors are never checked; NaN and Inf propagate.
+ *   - A handle is not thread-safe; use one handle per host thread.
+ *   - Results are deterministic: the same call on the same data gives the same
+ *     bits, and a matrix's result does not depend on which other matrices
+ *     share the call.
+ *   - No C++ exception crosses this interface.
+ */
+#ifndef MUON_HIP_H
+#define MUON_HIP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MUON_HIP_ABI_VERSION 1
+
+typedef struct muon_handle* muon_handle_t;
+
+typedef enum {
+  MUON_OK = 0,
+  MUON_ERR_INVALID_ARGUMENT = 1,  /* bad pointer, size, dtype, overlap, ... */
+  MUON_ERR_UNSUPPORTED = 2,       /* valid request this build does not do */
+  MUON_ERR_OUT_OF_MEMORY = 3,     /* workspace would exceed the limit or hipMalloc failed */
+  MUON_ERR_DEVICE = 4             /* a HIP runtime call failed */
+} muon_status_t;
+
+typedef enum { MUON_F32 = 0, MUON_BF16 = 1 } muon_dtype_t;
+
+/* Arithmetic of the Newton-Schulz products: bf16 operands with fp32
+ * accumulation (intermediates X, A = X X^T, B = bA + cA^2 stored as bf16),
+ * or fp32 throughout.  Momentum, norm and update are fp32 in both. */
+typedef enum { MUON_NS_BF16 = 0, MUON_NS_F32 = 1 } muon_ns_precision_t;
+
+/* One parameter entry (Sec. 6.3: a stacked entry is `batch` matrices). */
+typedef struct {
+  void* param;             /* in/out: batch x rows x cols, param_dtype */
+  const void* grad;        /* in:     batch x rows x cols, grad_dtype */
+  float* momentum;         /* in/out: batch x rows x cols, fp32 */
+  int64_t rows, cols;      /* the matrix plane (last two dims), >= 1 */
+  int64_t batch;           /* >= 1 */
+  int64_t ld;              /* row stride in elements: 0 or cols (dense only) */
+  muon_dtype_t param_dtype;
+  muon_dtype_t grad_dtype;
+} muon_param_t;
+
+typedef struct {
+  float lr;                /* finite */
+  float beta;              /* momentum coefficient, finite */
+  float weight_decay;      /* decoupled decay, finite */
+  float eps;               /* >= 0, finite; 1e-7 recommended */
+  int32_t ns_steps;        /* K, 0 <= K <= 64 */
+  int32_t nesterov;        /* 0 or 1 */
+  const float* ns_coeffs;  /* host array K x 3 {a_k, b_k, c_k}, or NULL */
+  muon_ns_precision_t ns_precision;
+  int32_t scale_mode;      /* 0: 0.2*sqrt(max(rows, cols)); 1: none */
+  int64_t max_chunk_elems; /* batch cap in elements of X; 0 = 2^29 (Sec. 6.6) */
+} muon_hparams_t;
+
+/* One shape-fused chunk of a plan (what muon_plan reports). */
+typedef struct {
+  int64_t s, l;            /* short and long side of every matrix in the chunk */
+  int64_t s_pad, l_pad;    /* workspace extents (multiples of 128) */
+  int64_t first;           /* index of the chunk's first matrix in plan order */
+  int64_t count;           /* matrices in the chunk */
+  int32_t param_dtype, grad_dtype;
+  size_t workspace_bytes;  /* workspace this chunk needs */
+} muon_chunk_info_t;
+
+/* Handle: owns the workspace and the device descriptor tables of one device.
+ * muon_create makes `device` current while it runs and restores the caller's
+ * device before it returns. */
+muon_status_t muon_create(muon_handle_t* out, int device);
+muon_status_t muon_destroy(muon_handle_t h);
+
+/* Grows the workspace to at least `bytes` now (hipMalloc synchronises, so do
+ * this before timing).  Fails with MUON_ERR_OUT_OF_MEMORY above the limit. */
+muon_status_t muon_reserve(muon_handle_t h, size_t bytes);
+/* Caps the workspace (0 = no cap).  A call whose plan needs more fails with
+ * MUON_ERR_OUT_OF_MEMORY before any launch. */
+muon_status_t muon_set_workspace_limit(muon_handle_t h, size_t bytes);
+size_t muon_workspace_bytes(muon_handle_t h);
+
+/*
+ * One Muon step over n entries (Sec. 2.3, Eq. (1); Sec. 6.6):
+ *   momentum <- beta*momentum + (1-beta)*grad                 (in place, fp32)
+ *   u        <- (1-beta)*grad + beta*momentum   (or momentum, nesterov = 0)
+ *   O        <- NS_K(u / (||u||_F + eps)) per matrix, transpose-first
+ *   param    <- (1 - lr*wd)*param - lr*scale*O                 (in place)
+ * grad is only read.  param, grad and momentum of all entries must not
+ * overlap (two grads may).  Matrices are grouped by (short side, long side,
+ * dtypes), chunked at max_chunk_elems, and chunks run largest first.
+ */
+muon_status_t muon_step(muon_handle_t h, const muon_param_t* params, int64_t n,
+                        const muon_hparams_t* hp, void* stream);
+
+/*
+ * Standalone batched orthogonalisation (Sec. 6.6): out[i] = NS_K(in[i] /
+ * (||in[i]||_F + eps)), rows[i] x cols[i], both in `dtype`, transpose-first
+ * inside, result in the input's own layout.  in[i] == out[i] is allowed; any
+ * other overlap between an output and another buffer is rejected.
+ */
+muon_status_t ns_orthogonalize_batched(muon_handle_t h, const void* const* in,
+                                       void* const* out, const int64_t* rows,
+                                       const int64_t* cols, int64_t n, muon_dtype_t dtype,
+                                       int32_t ns_steps, const float* ns_coeffs, float eps,
+                                       muon_ns_precision_t prec, void* stream);
+
+/* Host-only checks and planning (no device needed).  muon_validate_step
+ * returns the status muon_step would return for these arguments before
+ * launching anything and writes the reason into msg (may be NULL). */
+muon_status_t muon_validate_step(const muon_param_t* params, int64_t n,
+                                 const muon_hparams_t* hp, char* msg, size_t msg_len);
+/* Fills up to `cap` chunk records in execution order; *n_chunks receives the
+ * total, *workspace_bytes the workspace the plan needs.  `order` (may be NULL,
+ * else room for the total matrix count) receives, per matrix in plan order,
+ * its flat index (entry-major, plane-minor). */
+muon_status_t muon_plan_step(const muon_param_t* params, int64_t n, const muon_hparams_t* hp,
+                             muon_chunk_info_t* chunks, int64_t cap, int64_t* n_chunks,
+                             size_t* workspace_bytes, int64_t* order);
+
+const char* muon_status_string(muon_status_t s);
+/* Message of the last failure on h (empty string if none); valid until the
+ * next call on h. */
+const char* muon_last_error(muon_handle_t h);
+int muon_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MUON_HIP_H */

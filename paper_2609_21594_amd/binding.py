@@ -1,0 +1,260 @@
+"""ctypes binding of libmuon_hip.so (argument marshalling only).
+
+Every step of the Muon path runs in the library's HIP kernels; this module
+only turns torch tensors into device pointers and sizes, passes the current
+HIP stream, and raises on a non-OK status.  It fails loudly when the library
+is missing: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libmuon_hip.so")
+
+MUON_OK = 0
+STATUS = {0: "MUON_OK", 1: "MUON_ERR_INVALID_ARGUMENT", 2: "MUON_ERR_UNSUPPORTED",
+          3: "MUON_ERR_OUT_OF_MEMORY", 4: "MUON_ERR_DEVICE"}
+F32, BF16 = 0, 1
+NS_BF16, NS_F32 = 0, 1
+DEFAULT_CHUNK_ELEMS = 1 << 29
+
+
+class MuonError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+class MuonParam(ctypes.Structure):
+    _fields_ = [("param", ctypes.c_void_p), ("grad", ctypes.c_void_p),
+                ("momentum", ctypes.c_void_p), ("rows", ctypes.c_int64),
+                ("cols", ctypes.c_int64), ("batch", ctypes.c_int64), ("ld", ctypes.c_int64),
+                ("param_dtype", ctypes.c_int), ("grad_dtype", ctypes.c_int)]
+
+
+class MuonHParams(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("beta", ctypes.c_float),
+                ("weight_decay", ctypes.c_float), ("eps", ctypes.c_float),
+                ("ns_steps", ctypes.c_int32), ("nesterov", ctypes.c_int32),
+                ("ns_coeffs", ctypes.POINTER(ctypes.c_float)), ("ns_precision", ctypes.c_int),
+                ("scale_mode", ctypes.c_int32), ("max_chunk_elems", ctypes.c_int64)]
+
+
+class MuonChunkInfo(ctypes.Structure):
+    _fields_ = [("s", ctypes.c_int64), ("l", ctypes.c_int64), ("s_pad", ctypes.c_int64),
+                ("l_pad", ctypes.c_int64), ("first", ctypes.c_int64), ("count", ctypes.c_int64),
+                ("param_dtype", ctypes.c_int32), ("grad_dtype", ctypes.c_int32),
+                ("workspace_bytes", ctypes.c_size_t)]
+
+
+EXPORTS = ["muon_create", "muon_destroy", "muon_reserve", "muon_set_workspace_limit",
+           "muon_workspace_bytes", "muon_step", "ns_orthogonalize_batched",
+           "muon_validate_step", "muon_plan_step", "muon_status_string", "muon_last_error",
+           "muon_abi_version"]
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Loads the HIP library (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with "
+                           "`python -m paper_2609_21594_amd.csrc.build` (no fallback exists)")
+    lib = ctypes.CDLL(path)
+    vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+    lib.muon_create.argtypes = [ctypes.POINTER(vp), ctypes.c_int]
+    lib.muon_destroy.argtypes = [vp]
+    lib.muon_reserve.argtypes = [vp, ctypes.c_size_t]
+    lib.muon_set_workspace_limit.argtypes = [vp, ctypes.c_size_t]
+    lib.muon_workspace_bytes.argtypes = [vp]
+    lib.muon_workspace_bytes.restype = ctypes.c_size_t
+    lib.muon_step.argtypes = [vp, ctypes.POINTER(MuonParam), i64, ctypes.POINTER(MuonHParams), vp]
+    lib.ns_orthogonalize_batched.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                             ctypes.POINTER(i64), ctypes.POINTER(i64), i64,
+                                             ctypes.c_int, i32, ctypes.POINTER(ctypes.c_float),
+                                             ctypes.c_float, ctypes.c_int, vp]
+    lib.muon_validate_step.argtypes = [ctypes.POINTER(MuonParam), i64, ctypes.POINTER(MuonHParams),
+                                       ctypes.c_char_p, ctypes.c_size_t]
+    lib.muon_plan_step.argtypes = [ctypes.POINTER(MuonParam), i64, ctypes.POINTER(MuonHParams),
+                                   ctypes.POINTER(MuonChunkInfo), i64, ctypes.POINTER(i64),
+                                   ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(i64)]
+    lib.muon_status_string.argtypes = [ctypes.c_int]
+    lib.muon_status_string.restype = ctypes.c_char_p
+    lib.muon_last_error.argtypes = [vp]
+    lib.muon_last_error.restype = ctypes.c_char_p
+    for name in ("muon_create", "muon_destroy", "muon_reserve", "muon_set_workspace_limit",
+                 "muon_step", "ns_orthogonalize_batched", "muon_validate_step", "muon_plan_step"):
+        getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def make_hparams(lr=0.02, beta=0.95, weight_decay=0.0, eps=1e-7, ns_steps=5, nesterov=True,
+                 ns_coeffs: Optional[Sequence[Sequence[float]]] = None, ns_precision="bf16",
+                 scale_mode=0, max_chunk_elems=0):
+    """Returns (struct, keepalive) — keep the second item alive during the call."""
+    coeff_arr = None
+    if ns_coeffs is not None:
+        flat = [float(v) for row in ns_coeffs for v in row]
+        coeff_arr = (ctypes.c_float * max(1, len(flat)))(*flat)
+    hp = MuonHParams(lr, beta, weight_decay, eps, int(ns_steps), int(bool(nesterov)),
+                     ctypes.cast(coeff_arr, ctypes.POINTER(ctypes.c_float)) if coeff_arr else None,
+                     NS_F32 if ns_precision == "f32" else NS_BF16, int(scale_mode),
+                     int(max_chunk_elems))
+    return hp, coeff_arr
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _plane(t):
+    if t.dim() == 2:
+        return 1, t.shape[0], t.shape[1]
+    if t.dim() == 3:
+        return t.shape[0], t.shape[1], t.shape[2]
+    raise ValueError("Muon takes matrices [M, N] or stacks [E, M, N]")
+
+
+def params_array(params, grads, moms):
+    """MuonParam[] for lists of torch tensors ([M, N] or [E, M, N])."""
+    import torch
+    if not (len(params) == len(grads) == len(moms)):
+        raise ValueError("params, grads and momenta must have equal length")
+    arr = (MuonParam * max(1, len(params)))()
+    for i, (W, g, m) in enumerate(zip(params, grads, moms)):
+        if W.shape != g.shape or W.shape != m.shape:
+            raise ValueError(f"entry {i}: shapes differ")
+        if m.dtype != torch.float32:
+            raise TypeError(f"entry {i}: momentum must be float32")
+        for t in (W, g, m):
+            if not t.is_contiguous():
+                raise ValueError(f"entry {i}: tensors must be contiguous")
+        batch, rows, cols = _plane(W)
+        arr[i] = MuonParam(W.data_ptr(), g.data_ptr(), m.data_ptr(), rows, cols, batch, cols,
+                           _dtype_code(W), _dtype_code(g))
+    return arr
+
+
+def _stream_ptr(stream) -> int:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream)
+
+
+class Muon:
+    """A library handle on one device; owns the workspace."""
+
+    def __init__(self, device: int = 0):
+        self.lib = load_library()
+        h = ctypes.c_void_p()
+        st = self.lib.muon_create(ctypes.byref(h), int(device))
+        if st != MUON_OK:
+            raise MuonError(st, f"muon_create(device={device}) failed")
+        self.h = h
+        self.device = device
+
+    def _check(self, st: int):
+        if st != MUON_OK:
+            raise MuonError(st, self.lib.muon_last_error(self.h).decode())
+
+    def close(self):
+        if getattr(self, "h", None):
+            self.lib.muon_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def reserve(self, nbytes: int):
+        self._check(self.lib.muon_reserve(self.h, int(nbytes)))
+
+    def set_workspace_limit(self, nbytes: int):
+        self._check(self.lib.muon_set_workspace_limit(self.h, int(nbytes)))
+
+    @property
+    def workspace_bytes(self) -> int:
+        return int(self.lib.muon_workspace_bytes(self.h))
+
+    def step(self, params, grads, moms, stream=None, **hp_kw):
+        """In place: momentum and params updated, grads read (muon_step)."""
+        arr = params_array(params, grads, moms)
+        hp, keep = make_hparams(**hp_kw)
+        self._check(self.lib.muon_step(self.h, arr, len(params), ctypes.byref(hp),
+                                       ctypes.c_void_p(_stream_ptr(stream))))
+        del keep
+
+    def orthogonalize(self, inputs, outputs, ns_steps=5, ns_coeffs=None, eps=1e-7,
+                      ns_precision="bf16", stream=None):
+        """outputs[i] <- NS(inputs[i]) (ns_orthogonalize_batched); 2-D tensors."""
+        n = len(inputs)
+        if len(outputs) != n:
+            raise ValueError("inputs and outputs differ in length")
+        if n == 0:
+            return
+        dt = _dtype_code(inputs[0])
+        ins = (ctypes.c_void_p * n)()
+        outs = (ctypes.c_void_p * n)()
+        rows = (ctypes.c_int64 * n)()
+        cols = (ctypes.c_int64 * n)()
+        for i, (a, b) in enumerate(zip(inputs, outputs)):
+            if a.dim() != 2 or a.shape != b.shape:
+                raise ValueError(f"matrix {i}: need equal 2-D shapes")
+            if _dtype_code(a) != dt or _dtype_code(b) != dt:
+                raise TypeError("all inputs and outputs must share one dtype")
+            if not (a.is_contiguous() and b.is_contiguous()):
+                raise ValueError(f"matrix {i}: tensors must be contiguous")
+            ins[i], outs[i] = a.data_ptr(), b.data_ptr()
+            rows[i], cols[i] = a.shape[0], a.shape[1]
+        coeff = None
+        if ns_coeffs is not None:
+            flat = [float(v) for r in ns_coeffs for v in r]
+            coeff = (ctypes.c_float * max(1, len(flat)))(*flat)
+        self._check(self.lib.ns_orthogonalize_batched(
+            self.h, ins, outs, rows, cols, n, dt, int(ns_steps),
+            ctypes.cast(coeff, ctypes.POINTER(ctypes.c_float)) if coeff else None,
+            float(eps), NS_F32 if ns_precision == "f32" else NS_BF16,
+            ctypes.c_void_p(_stream_ptr(stream))))
+
+
+def validate_step(entries: Sequence[MuonParam], hp: MuonHParams):
+    """Host-only check (no device): returns (status, message)."""
+    lib = load_library()
+    arr = (MuonParam * max(1, len(entries)))(*entries)
+    msg = ctypes.create_string_buffer(256)
+    st = lib.muon_validate_step(arr, len(entries), ctypes.byref(hp), msg, 256)
+    return st, msg.value.decode()
+
+
+def plan_step(entries: Sequence[MuonParam], hp: MuonHParams):
+    """Host-only plan: (status, [chunk dicts], workspace bytes, plan order)."""
+    lib = load_library()
+    arr = (MuonParam * max(1, len(entries)))(*entries)
+    nch = ctypes.c_int64()
+    ws = ctypes.c_size_t()
+    st = lib.muon_plan_step(arr, len(entries), ctypes.byref(hp), None, 0, ctypes.byref(nch),
+                            ctypes.byref(ws), None)
+    if st != MUON_OK:
+        return st, [], 0, []
+    total = sum(e.batch for e in entries)
+    chunks = (MuonChunkInfo * max(1, nch.value))()
+    order = (ctypes.c_int64 * max(1, total))()
+    st = lib.muon_plan_step(arr, len(entries), ctypes.byref(hp), chunks, nch.value,
+                            ctypes.byref(nch), ctypes.byref(ws), order)
+    out = [{f: getattr(chunks[i], f) for f, _ in MuonChunkInfo._fields_} for i in range(nch.value)]
+    return st, out, ws.value, list(order[:total])

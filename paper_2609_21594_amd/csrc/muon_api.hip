@@ -1,0 +1,582 @@
+// C ABI of the batched Muon step: argument checks, the shape-fused batch
+// plan (Sec. 6.6), workspace and descriptor-table management, and the launch
+// sequence per chunk.  Kernels live in muon_kernels.hip.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <new>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "../../include/muon_hip.h"
+#include "muon_internal.h"
+
+using muon::ChunkBuffers;
+using muon::ChunkGeom;
+using muon::MatDesc;
+using muon::StepScalars;
+
+struct muon_handle {
+  int device = 0;
+  void* ws = nullptr;
+  size_t ws_bytes = 0;
+  size_t ws_limit = 0;               // 0 = no cap
+  MatDesc* d_desc = nullptr;         // device descriptor table
+  size_t desc_cap = 0;               // entries
+  MatDesc* h_stage = nullptr;        // pinned staging for the table upload
+  size_t stage_cap = 0;
+  hipEvent_t stage_done = nullptr;   // last upload out of h_stage has completed
+  bool stage_pending = false;
+  std::vector<MatDesc> last_table;   // content of d_desc
+  std::string err;
+};
+
+namespace {
+
+constexpr int64_t kDefaultChunkElems = int64_t(1) << 29;  // Sec. 6.6 batch cap
+constexpr int kMaxSteps = 64;
+constexpr int64_t kMaxDim = int64_t(1) << 28;
+constexpr int64_t kMaxChunkMats = 65535;
+const float kLegacyQuintic[3] = {3.4445f, -4.7750f, 2.0315f};
+
+struct Msg {
+  char* buf;
+  size_t len;
+  void set(const char* fmt, ...) {
+    if (!buf || !len) return;
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, len, fmt, ap);
+    va_end(ap);
+  }
+};
+
+void set_err(muon_handle_t h, const char* fmt, ...) {
+  if (!h) return;
+  char tmp[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(tmp, sizeof tmp, fmt, ap);
+  va_end(ap);
+  h->err = tmp;
+}
+
+size_t dtype_size(int dt) { return dt == MUON_BF16 ? 2 : 4; }
+bool dtype_ok(int dt) { return dt == MUON_F32 || dt == MUON_BF16; }
+
+// One matrix of the request, before planning.
+struct Item {
+  int64_t flat;            // entry-major, plane-minor index
+  int64_t rows, cols;
+  int32_t pdt, gdt;
+  void* W; const void* g; float* buf; void* out;
+};
+
+struct Range { uintptr_t lo, hi; bool written; };
+
+// Written ranges may not overlap anything; read-only ranges may overlap each
+// other.  Exact in-place pairs (orthogonalize in[i] == out[i]) are passed in
+// merged as one written range.
+bool ranges_disjoint(std::vector<Range>& rs) {
+  std::sort(rs.begin(), rs.end(), [](const Range& a, const Range& b) { return a.lo < b.lo; });
+  uintptr_t max_any = 0, max_written = 0;
+  bool first = true;
+  for (const Range& r : rs) {
+    if (r.hi <= r.lo) continue;
+    if (!first) {
+      if (r.written && r.lo < max_any) return false;
+      if (!r.written && r.lo < max_written) return false;
+    }
+    first = false;
+    max_any = std::max(max_any, r.hi);
+    if (r.written) max_written = std::max(max_written, r.hi);
+  }
+  return true;
+}
+
+muon_status_t check_hparams(const muon_hparams_t* hp, Msg& msg) {
+  if (!hp) { msg.set("hparams is NULL"); return MUON_ERR_INVALID_ARGUMENT; }
+  if (!std::isfinite(hp->lr) || !std::isfinite(hp->beta) || !std::isfinite(hp->weight_decay) ||
+      !std::isfinite(hp->eps) || hp->eps < 0.f) {
+    msg.set("lr, beta, weight_decay must be finite and eps finite and >= 0");
+    return MUON_ERR_INVALID_ARGUMENT;
+  }
+  if (hp->ns_steps < 0 || hp->ns_steps > kMaxSteps) {
+    msg.set("ns_steps must be in [0, %d]", kMaxSteps);
+    return MUON_ERR_INVALID_ARGUMENT;
+  }
+  if (hp->nesterov != 0 && hp->nesterov != 1) { msg.set("nesterov must be 0 or 1"); return MUON_ERR_INVALID_ARGUMENT; }
+  if (hp->ns_precision != MUON_NS_BF16 && hp->ns_precision != MUON_NS_F32) {
+    msg.set("unknown ns_precision %d", int(hp->ns_precision));
+    return MUON_ERR_INVALID_ARGUMENT;
+  }
+  if (hp->scale_mode != 0 && hp->scale_mode != 1) { msg.set("scale_mode must be 0 or 1"); return MUON_ERR_INVALID_ARGUMENT; }
+  if (hp->max_chunk_elems < 0) { msg.set("max_chunk_elems must be >= 0"); return MUON_ERR_INVALID_ARGUMENT; }
+  if (hp->ns_coeffs)
+    for (int i = 0; i < 3 * hp->ns_steps; ++i)
+      if (!std::isfinite(hp->ns_coeffs[i])) { msg.set("ns_coeffs[%d] is not finite", i); return MUON_ERR_INVALID_ARGUMENT; }
+  return MUON_OK;
+}
+
+muon_status_t check_dims(int64_t rows, int64_t cols, int64_t batch, const char* what, int64_t i, Msg& msg) {
+  if (rows < 1 || cols < 1 || batch < 1) {
+    msg.set("%s %lld: rows, cols and batch must be >= 1", what, (long long)i);
+    return MUON_ERR_INVALID_ARGUMENT;
+  }
+  if (rows > kMaxDim || cols > kMaxDim) {
+    msg.set("%s %lld: rows and cols must be <= 2^28", what, (long long)i);
+    return MUON_ERR_UNSUPPORTED;
+  }
+  return MUON_OK;
+}
+
+muon_status_t validate_step(const muon_param_t* params, int64_t n, const muon_hparams_t* hp,
+                            std::vector<Item>* items, Msg& msg) {
+  muon_status_t st = check_hparams(hp, msg);
+  if (st != MUON_OK) return st;
+  if (n < 0) { msg.set("n must be >= 0"); return MUON_ERR_INVALID_ARGUMENT; }
+  if (n > 0 && !params) { msg.set("params is NULL"); return MUON_ERR_INVALID_ARGUMENT; }
+  std::vector<Range> ranges;
+  ranges.reserve(3 * n);
+  int64_t flat = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    const muon_param_t& p = params[i];
+    if (!p.param || !p.grad || !p.momentum) { msg.set("entry %lld: NULL pointer", (long long)i); return MUON_ERR_INVALID_ARGUMENT; }
+    if ((st = check_dims(p.rows, p.cols, p.batch, "entry", i, msg)) != MUON_OK) return st;
+    if (!dtype_ok(p.param_dtype) || !dtype_ok(p.grad_dtype)) { msg.set("entry %lld: unknown dtype", (long long)i); return MUON_ERR_INVALID_ARGUMENT; }
+    if (p.ld != 0 && p.ld != p.cols) { msg.set("entry %lld: only dense rows (ld == cols) are supported", (long long)i); return MUON_ERR_UNSUPPORTED; }
+    const int64_t plane = p.rows * p.cols;
+    if (p.batch > (int64_t(1) << 40) / plane) { msg.set("entry %lld: too many elements", (long long)i); return MUON_ERR_UNSUPPORTED; }
+    const uintptr_t W = reinterpret_cast<uintptr_t>(p.param), G = reinterpret_cast<uintptr_t>(p.grad),
+                    M = reinterpret_cast<uintptr_t>(p.momentum);
+    const uint64_t ne = uint64_t(plane) * uint64_t(p.batch);
+    if ((W % dtype_size(p.param_dtype)) || (G % dtype_size(p.grad_dtype)) || (M % 4)) {
+      msg.set("entry %lld: pointer not aligned to its element size", (long long)i);
+      return MUON_ERR_INVALID_ARGUMENT;
+    }
+    ranges.push_back({W, W + ne * dtype_size(p.param_dtype), true});
+    ranges.push_back({G, G + ne * dtype_size(p.grad_dtype), false});
+    ranges.push_back({M, M + ne * 4, true});
+    if (items) {
+      for (int64_t e = 0; e < p.batch; ++e) {
+        Item it;
+        it.flat = flat++;
+        it.rows = p.rows; it.cols = p.cols;
+        it.pdt = p.param_dtype; it.gdt = p.grad_dtype;
+        it.W = static_cast<char*>(p.param) + e * plane * dtype_size(p.param_dtype);
+        it.g = static_cast<const char*>(p.grad) + e * plane * dtype_size(p.grad_dtype);
+        it.buf = p.momentum + e * plane;
+        it.out = nullptr;
+        items->push_back(it);
+      }
+    }
+  }
+  if (!ranges_disjoint(ranges)) {
+    msg.set("param, grad and momentum buffers overlap");
+    return MUON_ERR_INVALID_ARGUMENT;
+  }
+  return MUON_OK;
+}
+
+muon_status_t validate_orth(const void* const* in, void* const* out, const int64_t* rows,
+                            const int64_t* cols, int64_t n, int dtype, int32_t ns_steps,
+                            const float* coeffs, float eps, int prec, std::vector<Item>* items,
+                            Msg& msg) {
+  if (n < 0) { msg.set("n must be >= 0"); return MUON_ERR_INVALID_ARGUMENT; }
+  if (n > 0 && (!in || !out || !rows || !cols)) { msg.set("NULL array argument"); return MUON_ERR_INVALID_ARGUMENT; }
+  if (!dtype_ok(dtype)) { msg.set("unknown dtype"); return MUON_ERR_INVALID_ARGUMENT; }
+  if (ns_steps < 0 || ns_steps > kMaxSteps) { msg.set("ns_steps must be in [0, %d]", kMaxSteps); return MUON_ERR_INVALID_ARGUMENT; }
+  if (!std::isfinite(eps) || eps < 0.f) { msg.set("eps must be finite and >= 0"); return MUON_ERR_INVALID_ARGUMENT; }
+  if (prec != MUON_NS_BF16 && prec != MUON_NS_F32) { msg.set("unknown ns precision"); return MUON_ERR_INVALID_ARGUMENT; }
+  if (coeffs)
+    for (int i = 0; i < 3 * ns_steps; ++i)
+      if (!std::isfinite(coeffs[i])) { msg.set("ns_coeffs[%d] is not finite", i); return MUON_ERR_INVALID_ARGUMENT; }
+  std::vector<Range> ranges;
+  const size_t es = dtype_size(dtype);
+  muon_status_t st;
+  for (int64_t i = 0; i < n; ++i) {
+    if (!in[i] || !out[i]) { msg.set("matrix %lld: NULL pointer", (long long)i); return MUON_ERR_INVALID_ARGUMENT; }
+    if ((st = check_dims(rows[i], cols[i], 1, "matrix", i, msg)) != MUON_OK) return st;
+    const uintptr_t a = reinterpret_cast<uintptr_t>(in[i]), b = reinterpret_cast<uintptr_t>(out[i]);
+    if (a % es || b % es) { msg.set("matrix %lld: pointer not aligned to its element size", (long long)i); return MUON_ERR_INVALID_ARGUMENT; }
+    const uintptr_t bytes = uintptr_t(rows[i]) * uintptr_t(cols[i]) * es;
+    if (a == b) {
+      ranges.push_back({a, a + bytes, true});
+    } else {
+      ranges.push_back({a, a + bytes, false});
+      ranges.push_back({b, b + bytes, true});
+    }
+    if (items) {
+      Item it;
+      it.flat = i; it.rows = rows[i]; it.cols = cols[i];
+      it.pdt = dtype; it.gdt = dtype;
+      it.W = nullptr; it.g = in[i]; it.buf = nullptr; it.out = out[i];
+      items->push_back(it);
+    }
+  }
+  if (!ranges_disjoint(ranges)) { msg.set("an output overlaps another buffer"); return MUON_ERR_INVALID_ARGUMENT; }
+  return MUON_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Plan: bucket by (short side, long side, dtypes) after transpose-first,
+// largest work first, chunks of at most `cap` elements (at least one matrix).
+// ---------------------------------------------------------------------------
+struct Chunk {
+  int64_t s, l, S, L;
+  int32_t pdt, gdt;
+  int64_t first, count;
+  size_t bytes;
+  // byte offsets inside the workspace
+  size_t off_X[2], off_XT[2], off_A, off_B, off_part, off_r;
+};
+
+struct Plan {
+  std::vector<int64_t> order;  // plan position -> index into items
+  std::vector<Chunk> chunks;
+  size_t ws_bytes = 0;
+};
+
+size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+
+Plan make_plan(const std::vector<Item>& items, int64_t cap, bool ns_f32) {
+  if (cap <= 0) cap = kDefaultChunkElems;
+  using Key = std::tuple<int64_t, int64_t, int32_t, int32_t>;
+  std::map<Key, std::vector<int64_t>> buckets;
+  std::map<Key, int64_t> first_seen;
+  for (size_t i = 0; i < items.size(); ++i) {
+    const Item& it = items[i];
+    Key k{std::min(it.rows, it.cols), std::max(it.rows, it.cols), it.pdt, it.gdt};
+    if (!first_seen.count(k)) first_seen[k] = int64_t(i);
+    buckets[k].push_back(int64_t(i));
+  }
+  std::vector<Key> keys;
+  for (auto& kv : buckets) keys.push_back(kv.first);
+  std::stable_sort(keys.begin(), keys.end(), [&](const Key& a, const Key& b) {
+    const double wa = double(std::get<0>(a)) * std::get<0>(a) * std::get<1>(a);
+    const double wb = double(std::get<0>(b)) * std::get<0>(b) * std::get<1>(b);
+    if (wa != wb) return wa > wb;
+    return first_seen[a] < first_seen[b];
+  });
+  Plan plan;
+  const size_t es = ns_f32 ? 4 : 2;
+  for (const Key& k : keys) {
+    const auto& idx = buckets[k];
+    const int64_t s = std::get<0>(k), l = std::get<1>(k);
+    const int64_t per = std::max<int64_t>(1, std::min<int64_t>(kMaxChunkMats, cap / (s * l)));
+    for (size_t b = 0; b < idx.size(); b += size_t(per)) {
+      Chunk c{};
+      c.s = s; c.l = l;
+      c.S = muon::round_up(s, muon::kPad);
+      c.L = muon::round_up(l, muon::kPad);
+      c.pdt = std::get<2>(k); c.gdt = std::get<3>(k);
+      c.first = int64_t(plan.order.size());
+      c.count = std::min<int64_t>(per, int64_t(idx.size() - b));
+      for (int64_t j = 0; j < c.count; ++j) plan.order.push_back(idx[b + size_t(j)]);
+      const size_t xb = align256(size_t(c.count) * size_t(c.S) * size_t(c.L) * es);
+      const size_t ab = align256(size_t(c.count) * size_t(c.S) * size_t(c.S) * es);
+      const size_t pb = align256(size_t(c.count) * size_t(muon::norm_blocks(s * l)) * 4);
+      size_t off = 0;
+      c.off_X[0] = off; off += xb;
+      c.off_X[1] = off; off += xb;
+      c.off_XT[0] = off; off += xb;
+      c.off_XT[1] = off; off += xb;
+      c.off_A = off; off += ab;
+      c.off_B = off; off += ab;
+      c.off_part = off; off += pb;
+      c.off_r = off; off += align256(size_t(c.count) * 4);
+      c.bytes = off;
+      plan.ws_bytes = std::max(plan.ws_bytes, off);
+      plan.chunks.push_back(c);
+    }
+  }
+  return plan;
+}
+
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = false;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) return;
+    ok = hipSetDevice(dev) == hipSuccess;
+  }
+  ~DeviceGuard() { if (prev >= 0) (void)hipSetDevice(prev); }
+};
+
+muon_status_t device_fail(muon_handle_t h, const char* what, hipError_t e) {
+  set_err(h, "%s: %s", what, hipGetErrorString(e));
+  return MUON_ERR_DEVICE;
+}
+
+muon_status_t ensure_workspace(muon_handle_t h, size_t bytes) {
+  if (bytes <= h->ws_bytes) return MUON_OK;
+  if (h->ws_limit && bytes > h->ws_limit) {
+    set_err(h, "workspace of %zu bytes exceeds the limit of %zu bytes", bytes, h->ws_limit);
+    return MUON_ERR_OUT_OF_MEMORY;
+  }
+  hipError_t e;
+  if (h->ws) {
+    // earlier work may still use the old workspace
+    if ((e = hipDeviceSynchronize()) != hipSuccess) return device_fail(h, "hipDeviceSynchronize", e);
+    if ((e = hipFree(h->ws)) != hipSuccess) return device_fail(h, "hipFree", e);
+    h->ws = nullptr;
+    h->ws_bytes = 0;
+  }
+  void* p = nullptr;
+  e = hipMalloc(&p, bytes);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    set_err(h, "hipMalloc of %zu workspace bytes failed: %s", bytes, hipGetErrorString(e));
+    return MUON_ERR_OUT_OF_MEMORY;
+  }
+  h->ws = p;
+  h->ws_bytes = bytes;
+  return MUON_OK;
+}
+
+// Puts `table` into h->d_desc on `stream`, skipping the copy when the device
+// table already holds exactly these bytes.
+muon_status_t upload_table(muon_handle_t h, const std::vector<MatDesc>& table, hipStream_t stream) {
+  if (table.size() == h->last_table.size() &&
+      std::memcmp(table.data(), h->last_table.data(), table.size() * sizeof(MatDesc)) == 0)
+    return MUON_OK;
+  hipError_t e;
+  if (table.size() > h->desc_cap) {
+    const size_t cap = std::max(table.size(), size_t(256));
+    if (h->d_desc) {
+      if ((e = hipDeviceSynchronize()) != hipSuccess) return device_fail(h, "hipDeviceSynchronize", e);
+      if ((e = hipFree(h->d_desc)) != hipSuccess) return device_fail(h, "hipFree", e);
+      h->d_desc = nullptr; h->desc_cap = 0;
+    }
+    if ((e = hipMalloc(&h->d_desc, cap * sizeof(MatDesc))) != hipSuccess) {
+      (void)hipGetLastError();
+      set_err(h, "hipMalloc of the descriptor table failed");
+      return MUON_ERR_OUT_OF_MEMORY;
+    }
+    h->desc_cap = cap;
+  }
+  if (h->stage_pending) {
+    if ((e = hipEventSynchronize(h->stage_done)) != hipSuccess) return device_fail(h, "hipEventSynchronize", e);
+    h->stage_pending = false;
+  }
+  if (table.size() > h->stage_cap) {
+    if (h->h_stage) { (void)hipHostFree(h->h_stage); h->h_stage = nullptr; h->stage_cap = 0; }
+    const size_t cap = std::max(table.size(), size_t(256));
+    if ((e = hipHostMalloc(reinterpret_cast<void**>(&h->h_stage), cap * sizeof(MatDesc), hipHostMallocDefault)) != hipSuccess) {
+      (void)hipGetLastError();
+      set_err(h, "hipHostMalloc of the descriptor staging buffer failed");
+      return MUON_ERR_OUT_OF_MEMORY;
+    }
+    h->stage_cap = cap;
+  }
+  std::memcpy(h->h_stage, table.data(), table.size() * sizeof(MatDesc));
+  if ((e = hipMemcpyAsync(h->d_desc, h->h_stage, table.size() * sizeof(MatDesc), hipMemcpyHostToDevice, stream)) != hipSuccess)
+    return device_fail(h, "hipMemcpyAsync", e);
+  if ((e = hipEventRecord(h->stage_done, stream)) != hipSuccess) return device_fail(h, "hipEventRecord", e);
+  h->stage_pending = true;
+  h->last_table = table;
+  return MUON_OK;
+}
+
+MatDesc make_desc(const Item& it, double lr, double wd, int scale_mode) {
+  MatDesc d{};
+  d.W = it.W; d.g = it.g; d.buf = it.buf; d.out = it.out;
+  d.rows = int32_t(it.rows); d.cols = int32_t(it.cols);
+  d.transposed = it.rows > it.cols ? 1 : 0;
+  const auto al16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
+  d.vec_ok = ((it.rows * it.cols) % 8 == 0) && al16(it.g) && (!it.buf || al16(it.buf)) ? 1 : 0;
+  const double scale = scale_mode == 0 ? 0.2 * std::sqrt(double(std::max(it.rows, it.cols))) : 1.0;
+  d.upd_scale = float(lr * scale);
+  d.decay = float(1.0 - lr * wd);
+  return d;
+}
+
+muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Plan& plan,
+                      double lr, double wd, int scale_mode, const StepScalars& sc, bool ns_f32,
+                      const float* coeffs, int K, hipStream_t stream) {
+  DeviceGuard dg(h->device);
+  if (!dg.ok) { set_err(h, "cannot select device %d", h->device); return MUON_ERR_DEVICE; }
+  muon_status_t st = ensure_workspace(h, plan.ws_bytes);
+  if (st != MUON_OK) return st;
+  std::vector<MatDesc> table(plan.order.size());
+  for (size_t p = 0; p < plan.order.size(); ++p) table[p] = make_desc(items[size_t(plan.order[p])], lr, wd, scale_mode);
+  if ((st = upload_table(h, table, stream)) != MUON_OK) return st;
+  char* ws = static_cast<char*>(h->ws);
+  for (const Chunk& c : plan.chunks) {
+    ChunkGeom g{};
+    g.s = int32_t(c.s); g.l = int32_t(c.l); g.S = int32_t(c.S); g.L = int32_t(c.L);
+    g.nmat = int32_t(c.count);
+    g.ns_f32 = ns_f32 ? 1 : 0;
+    g.grad_dtype = c.gdt == MUON_BF16 ? muon::DT_BF16 : muon::DT_F32;
+    g.param_dtype = c.pdt == MUON_BF16 ? muon::DT_BF16 : muon::DT_F32;
+    ChunkBuffers b{};
+    b.X[0] = ws + c.off_X[0]; b.X[1] = ws + c.off_X[1];
+    b.XT[0] = ws + c.off_XT[0]; b.XT[1] = ws + c.off_XT[1];
+    b.A = ws + c.off_A; b.B = ws + c.off_B;
+    b.partials = reinterpret_cast<float*>(ws + c.off_part);
+    b.rscale = reinterpret_cast<float*>(ws + c.off_r);
+    hipError_t e = muon::run_chunk(g, h->d_desc + c.first, b, sc, coeffs, K, stream);
+    if (e != hipSuccess) return device_fail(h, "kernel launch", e);
+  }
+  return MUON_OK;
+}
+
+std::vector<float> coefficient_table(int K, const float* coeffs) {
+  std::vector<float> t(size_t(3) * size_t(K));
+  for (int k = 0; k < K; ++k)
+    for (int j = 0; j < 3; ++j) t[size_t(3 * k + j)] = coeffs ? coeffs[3 * k + j] : kLegacyQuintic[j];
+  return t;
+}
+
+}  // namespace
+
+extern "C" {
+
+int muon_abi_version(void) { return MUON_HIP_ABI_VERSION; }
+
+const char* muon_status_string(muon_status_t s) {
+  switch (s) {
+    case MUON_OK: return "MUON_OK";
+    case MUON_ERR_INVALID_ARGUMENT: return "MUON_ERR_INVALID_ARGUMENT";
+    case MUON_ERR_UNSUPPORTED: return "MUON_ERR_UNSUPPORTED";
+    case MUON_ERR_OUT_OF_MEMORY: return "MUON_ERR_OUT_OF_MEMORY";
+    case MUON_ERR_DEVICE: return "MUON_ERR_DEVICE";
+  }
+  return "MUON_ERR_UNKNOWN";
+}
+
+const char* muon_last_error(muon_handle_t h) { return h ? h->err.c_str() : "NULL handle"; }
+
+muon_status_t muon_create(muon_handle_t* out, int device) {
+  if (!out) return MUON_ERR_INVALID_ARGUMENT;
+  *out = nullptr;
+  int count = 0;
+  if (hipGetDeviceCount(&count) != hipSuccess || count <= 0) { (void)hipGetLastError(); return MUON_ERR_DEVICE; }
+  if (device < 0 || device >= count) return MUON_ERR_INVALID_ARGUMENT;
+  muon_handle* h = new (std::nothrow) muon_handle();
+  if (!h) return MUON_ERR_OUT_OF_MEMORY;
+  h->device = device;
+  DeviceGuard dg(device);
+  if (!dg.ok || hipEventCreateWithFlags(&h->stage_done, hipEventDisableTiming) != hipSuccess) {
+    delete h;
+    return MUON_ERR_DEVICE;
+  }
+  *out = h;
+  return MUON_OK;
+}
+
+muon_status_t muon_destroy(muon_handle_t h) {
+  if (!h) return MUON_ERR_INVALID_ARGUMENT;
+  muon_status_t st = MUON_OK;
+  {
+    DeviceGuard dg(h->device);
+    if (hipDeviceSynchronize() != hipSuccess) st = MUON_ERR_DEVICE;
+    if (h->ws) (void)hipFree(h->ws);
+    if (h->d_desc) (void)hipFree(h->d_desc);
+    if (h->h_stage) (void)hipHostFree(h->h_stage);
+    if (h->stage_done) (void)hipEventDestroy(h->stage_done);
+  }
+  delete h;
+  return st;
+}
+
+muon_status_t muon_reserve(muon_handle_t h, size_t bytes) {
+  if (!h) return MUON_ERR_INVALID_ARGUMENT;
+  DeviceGuard dg(h->device);
+  if (!dg.ok) return MUON_ERR_DEVICE;
+  return ensure_workspace(h, bytes);
+}
+
+muon_status_t muon_set_workspace_limit(muon_handle_t h, size_t bytes) {
+  if (!h) return MUON_ERR_INVALID_ARGUMENT;
+  h->ws_limit = bytes;
+  return MUON_OK;
+}
+
+size_t muon_workspace_bytes(muon_handle_t h) { return h ? h->ws_bytes : 0; }
+
+muon_status_t muon_validate_step(const muon_param_t* params, int64_t n, const muon_hparams_t* hp,
+                                 char* msg, size_t msg_len) {
+  Msg m{msg, msg_len};
+  if (msg && msg_len) msg[0] = '\0';
+  return validate_step(params, n, hp, nullptr, m);
+}
+
+muon_status_t muon_plan_step(const muon_param_t* params, int64_t n, const muon_hparams_t* hp,
+                             muon_chunk_info_t* chunks, int64_t cap, int64_t* n_chunks,
+                             size_t* workspace_bytes, int64_t* order) {
+  Msg m{nullptr, 0};
+  std::vector<Item> items;
+  muon_status_t st = validate_step(params, n, hp, &items, m);
+  if (st != MUON_OK) return st;
+  if (cap > 0 && !chunks) return MUON_ERR_INVALID_ARGUMENT;
+  const Plan plan = make_plan(items, hp->max_chunk_elems, hp->ns_precision == MUON_NS_F32);
+  if (n_chunks) *n_chunks = int64_t(plan.chunks.size());
+  if (workspace_bytes) *workspace_bytes = plan.ws_bytes;
+  for (int64_t i = 0; i < cap && i < int64_t(plan.chunks.size()); ++i) {
+    const Chunk& c = plan.chunks[size_t(i)];
+    muon_chunk_info_t& o = chunks[i];
+    o.s = c.s; o.l = c.l; o.s_pad = c.S; o.l_pad = c.L;
+    o.first = c.first; o.count = c.count;
+    o.param_dtype = c.pdt; o.grad_dtype = c.gdt;
+    o.workspace_bytes = c.bytes;
+  }
+  if (order)
+    for (size_t p = 0; p < plan.order.size(); ++p) order[p] = items[size_t(plan.order[p])].flat;
+  return MUON_OK;
+}
+
+muon_status_t muon_step(muon_handle_t h, const muon_param_t* params, int64_t n,
+                        const muon_hparams_t* hp, void* stream) {
+  if (!h) return MUON_ERR_INVALID_ARGUMENT;
+  h->err.clear();
+  char buf[256] = {0};
+  Msg m{buf, sizeof buf};
+  std::vector<Item> items;
+  muon_status_t st = validate_step(params, n, hp, &items, m);
+  if (st != MUON_OK) { h->err = buf; return st; }
+  if (items.empty()) return MUON_OK;
+  const bool f32 = hp->ns_precision == MUON_NS_F32;
+  const Plan plan = make_plan(items, hp->max_chunk_elems, f32);
+  StepScalars sc{};
+  sc.beta = hp->beta;
+  sc.one_minus_beta = 1.0f - hp->beta;
+  sc.nesterov = hp->nesterov;
+  sc.momentum = 1;
+  sc.eps = hp->eps;
+  sc.final_kind = 0;
+  const std::vector<float> coeffs = coefficient_table(hp->ns_steps, hp->ns_coeffs);
+  return execute(h, items, plan, hp->lr, hp->weight_decay, hp->scale_mode, sc, f32, coeffs.data(),
+                 hp->ns_steps, static_cast<hipStream_t>(stream));
+}
+
+muon_status_t ns_orthogonalize_batched(muon_handle_t h, const void* const* in, void* const* out,
+                                       const int64_t* rows, const int64_t* cols, int64_t n,
+                                       muon_dtype_t dtype, int32_t ns_steps, const float* ns_coeffs,
+                                       float eps, muon_ns_precision_t prec, void* stream) {
+  if (!h) return MUON_ERR_INVALID_ARGUMENT;
+  h->err.clear();
+  char buf[256] = {0};
+  Msg m{buf, sizeof buf};
+  std::vector<Item> items;
+  muon_status_t st = validate_orth(in, out, rows, cols, n, dtype, ns_steps, ns_coeffs, eps, prec, &items, m);
+  if (st != MUON_OK) { h->err = buf; return st; }
+  if (items.empty()) return MUON_OK;
+  const bool f32 = prec == MUON_NS_F32;
+  const Plan plan = make_plan(items, 0, f32);
+  StepScalars sc{};
+  sc.momentum = 0;
+  sc.eps = eps;
+  sc.final_kind = 1;
+  const std::vector<float> coeffs = coefficient_table(ns_steps, ns_coeffs);
+  return execute(h, items, plan, 0.0, 0.0, 1, sc, f32, coeffs.data(), ns_steps,
+                 static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

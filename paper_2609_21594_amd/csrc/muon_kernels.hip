@@ -1,0 +1,562 @@
+// gfx950 (CDNA4) kernels of the batched Muon step.
+//
+// Per chunk of same-shape matrices (Sec. 6.6 shape fusion):
+//   k_partials   momentum update in place + per-block sums of u^2   (HBM-bound)
+//   k_finalize   r = 1 / (||u||_F + eps) per matrix (fixed-order sum)
+//   k_normalize  X0 = r*u, transpose-first, cast; writes X0 and X0^T (HBM-bound)
+//   k_gemm_nt    the three contractions of Eq. (1) on MFMA:
+//                  A  = X X^T          (Gram, upper tiles only, mirrored)
+//                  B  = b A + c A A    (A is symmetric, so A A = A A^T)
+//                  X' = a X + B X      (reads X^T as the K-contiguous operand)
+//                the last step's epilogue applies the update to W directly.
+//   k_apply      update from X0 when K = 0.
+//
+// All workspace buffers are zero-padded to multiples of 128 in both extents,
+// so the contraction kernels never test bounds; zero padding is preserved by
+// every step (padded rows/columns of X, A and B stay exactly zero).
+#include <hip/hip_runtime.h>
+
+#include "muon_internal.h"
+
+namespace muon {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------------------
+// bfloat16 storage: uint16 bit patterns.  Widening is exact; narrowing rounds
+// to nearest, ties to even (NaN stays NaN).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) {
+  return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+template <typename T> __device__ __forceinline__ float to_f32(T v);
+template <> __device__ __forceinline__ float to_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ float to_f32<uint16_t>(uint16_t v) { return bf16_to_f32(v); }
+
+template <typename T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ uint16_t from_f32<uint16_t>(float v) { return f32_to_bf16(v); }
+
+__device__ __forceinline__ float load_as_f32(const void* p, int64_t i, int dt) {
+  return dt == DT_BF16 ? bf16_to_f32(static_cast<const uint16_t*>(p)[i])
+                       : static_cast<const float*>(p)[i];
+}
+__device__ __forceinline__ void store_from_f32(void* p, int64_t i, int dt, float v) {
+  if (dt == DT_BF16) static_cast<uint16_t*>(p)[i] = f32_to_bf16(v);
+  else static_cast<float*>(p)[i] = v;
+}
+
+// Fixed-order sum over a 256-thread block: butterfly within each 64-lane
+// wavefront, then the four wave sums in wave order.  Deterministic.
+__device__ __forceinline__ float block_sum_256(float v, float* red4) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red4[wave] = v;
+  __syncthreads();
+  float s = ((red4[0] + red4[1]) + red4[2]) + red4[3];
+  return s;
+}
+
+// ---------------------------------------------------------------------------
+// Momentum update (in place) and partial sums of u^2; or, without momentum,
+// partial sums of G^2.  One workgroup reduces kNormElemsPerBlock elements of
+// one matrix; grid = (blocks per matrix, matrices).
+// ---------------------------------------------------------------------------
+template <typename GT, bool MOM>
+__global__ __launch_bounds__(256) void k_partials(const MatDesc* __restrict__ desc, int nblk,
+                                                  StepScalars sc, float* __restrict__ partials) {
+  __shared__ float red4[4];
+  const int m = blockIdx.y;
+  const MatDesc md = desc[m];
+  const int64_t numel = static_cast<int64_t>(md.rows) * md.cols;
+  const int64_t start = static_cast<int64_t>(blockIdx.x) * kNormElemsPerBlock;
+  const int64_t end = min(numel, start + static_cast<int64_t>(kNormElemsPerBlock));
+  const GT* __restrict__ g = static_cast<const GT*>(md.g);
+  float* __restrict__ buf = md.buf;
+  const float beta = sc.beta, omb = sc.one_minus_beta;
+  float acc = 0.f;
+
+  auto one = [&](float gv, float bv, float& bn_out) -> float {
+    if (MOM) {
+      const float bn = fmaf(beta, bv, omb * gv);
+      bn_out = bn;
+      return sc.nesterov ? fmaf(beta, bn, omb * gv) : bn;
+    }
+    return gv;
+  };
+
+  if (md.vec_ok) {
+    // 8 consecutive elements per thread and iteration; numel % 8 == 0.
+    for (int64_t i = start + threadIdx.x * 8; i < end; i += 256 * 8) {
+      float gv[8];
+      if (sizeof(GT) == 2) {
+        const u32x4_t raw = *reinterpret_cast<const u32x4_t*>(g + i);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          gv[2 * q] = __uint_as_float(raw[q] << 16);
+          gv[2 * q + 1] = __uint_as_float(raw[q] & 0xffff0000u);
+        }
+      } else {
+        const float4 a = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(g) + i);
+        const float4 b = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(g) + i + 4);
+        gv[0] = a.x; gv[1] = a.y; gv[2] = a.z; gv[3] = a.w;
+        gv[4] = b.x; gv[5] = b.y; gv[6] = b.z; gv[7] = b.w;
+      }
+      float bv[8] = {0, 0, 0, 0, 0, 0, 0, 0}, bn[8];
+      if (MOM) {
+        const float4 a = *reinterpret_cast<const float4*>(buf + i);
+        const float4 b = *reinterpret_cast<const float4*>(buf + i + 4);
+        bv[0] = a.x; bv[1] = a.y; bv[2] = a.z; bv[3] = a.w;
+        bv[4] = b.x; bv[5] = b.y; bv[6] = b.z; bv[7] = b.w;
+      }
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const float u = one(gv[q], bv[q], bn[q]);
+        acc = fmaf(u, u, acc);
+      }
+      if (MOM) {
+        *reinterpret_cast<float4*>(buf + i) = make_float4(bn[0], bn[1], bn[2], bn[3]);
+        *reinterpret_cast<float4*>(buf + i + 4) = make_float4(bn[4], bn[5], bn[6], bn[7]);
+      }
+    }
+  } else {
+    for (int64_t i = start + threadIdx.x; i < end; i += 256) {
+      const float gv = to_f32<GT>(g[i]);
+      float bn = 0.f;
+      const float u = one(gv, MOM ? buf[i] : 0.f, bn);
+      if (MOM) buf[i] = bn;
+      acc = fmaf(u, u, acc);
+    }
+  }
+  const float s = block_sum_256(acc, red4);
+  if (threadIdx.x == 0) partials[static_cast<int64_t>(m) * nblk + blockIdx.x] = s;
+}
+
+// r = 1 / (sqrt(sum of partials) + eps), one workgroup per matrix.
+__global__ __launch_bounds__(256) void k_finalize(const float* __restrict__ partials, int nblk,
+                                                  float eps, float* __restrict__ rscale) {
+  __shared__ float red4[4];
+  const int m = blockIdx.x;
+  float acc = 0.f;
+  for (int i = threadIdx.x; i < nblk; i += 256) acc += partials[static_cast<int64_t>(m) * nblk + i];
+  const float s = block_sum_256(acc, red4);
+  if (threadIdx.x == 0) rscale[m] = 1.0f / (sqrtf(s) + eps);
+}
+
+// ---------------------------------------------------------------------------
+// X0 = r*u with transpose-first.  A workgroup owns a 64x64 tile of the
+// padded X extent (S x L); it reads the matching tile of u row by row
+// (coalesced), writes it unchanged into whichever of X / X^T has u's layout,
+// and transposes it through LDS into the other.  Zero outside the matrix.
+// grid = (L/64, S/64, matrices).
+// ---------------------------------------------------------------------------
+template <typename GT, typename XT, bool MOM>
+__global__ __launch_bounds__(256) void k_normalize(const MatDesc* __restrict__ desc,
+                                                   const float* __restrict__ rscale,
+                                                   StepScalars sc, ChunkGeom cg, XT* __restrict__ X,
+                                                   XT* __restrict__ XTb) {
+  constexpr int LDT = sizeof(XT) == 2 ? 66 : 65;  // LDS row stride (odd word stride)
+  __shared__ XT tile[64 * LDT];
+  const int m = blockIdx.z;
+  const MatDesc md = desc[m];
+  const bool tr = md.transposed != 0;
+  const int i0 = blockIdx.y * 64, j0 = blockIdx.x * 64;  // tile origin in X coordinates
+  const int ur0 = tr ? j0 : i0, uc0 = tr ? i0 : j0;       // same tile in u coordinates
+  const int64_t matX = static_cast<int64_t>(cg.S) * cg.L;
+  XT* Xm = X + m * matX;
+  XT* XTm = XTb + m * matX;
+  XT* D = tr ? XTm : Xm;            // u's own layout
+  const int ldD = tr ? cg.S : cg.L;
+  XT* Tb = tr ? Xm : XTm;           // the transpose
+  const int ldT = tr ? cg.L : cg.S;
+  const float r = rscale[m];
+  const GT* __restrict__ g = static_cast<const GT*>(md.g);
+  const float beta = sc.beta, omb = sc.one_minus_beta;
+  const int col = threadIdx.x & 63;
+#pragma unroll 4
+  for (int row = threadIdx.x >> 6; row < 64; row += 4) {
+    const int ur = ur0 + row, uc = uc0 + col;
+    float v = 0.f;
+    if (ur < md.rows && uc < md.cols) {
+      const int64_t idx = static_cast<int64_t>(ur) * md.cols + uc;
+      const float gv = to_f32<GT>(g[idx]);
+      float u;
+      if (MOM) {
+        const float bn = md.buf[idx];  // already updated by k_partials
+        u = sc.nesterov ? fmaf(beta, bn, omb * gv) : bn;
+      } else {
+        u = gv;
+      }
+      v = u * r;
+    }
+    const XT xv = from_f32<XT>(v);
+    D[static_cast<int64_t>(ur) * ldD + uc] = xv;
+    tile[row * LDT + col] = xv;
+  }
+  __syncthreads();
+#pragma unroll 4
+  for (int trow = threadIdx.x >> 6; trow < 64; trow += 4) {
+    Tb[static_cast<int64_t>(uc0 + trow) * ldT + ur0 + col] = tile[col * LDT + trow];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// C = P Q^T on MFMA, P: M x K and Q: N x K row-major (K contiguous), all
+// extents multiples of 128.  256 threads = 4 wavefronts in a 2 x 2 grid,
+// each owning a 64 x 64 sub-tile = 2 x 2 blocks of the 32x32 MFMA.  K is
+// staged through LDS 128 bytes per row at a time (64 bf16 or 32 fp32),
+// double-buffered, with the next slab prefetched into registers while the
+// current one is multiplied.
+//
+// bf16: v_mfma_f32_32x32x16_bf16, a lane supplies 8 consecutive k of its row.
+// fp32: v_mfma_f32_32x32x2_f32, a lane holds 4 consecutive k and issues four
+//       MFMAs (lanes 0-31 give k = j, lanes 32-63 give k = 4 + j).
+// In both, a lane's operand for a 32-k (bf16) / 8-k (fp32) group is the 16
+// bytes at byte offset 16*(lane/32) of the group, so the LDS geometry is the
+// same for both element types.
+//
+// Output layout of a 32x32 block: lane l, register r holds
+//   row 8*(r/4) + 4*(l/32) + (r%4), column l%32.
+// ---------------------------------------------------------------------------
+enum Epi : int { EPI_GRAM = 0, EPI_POLY = 1, EPI_UPDATE = 2, EPI_FINAL = 3 };
+
+struct GemmArgs {
+  const char* P;   int64_t p_mat;  int32_t ldp;   // bytes
+  const char* Q;   int64_t q_mat;  int32_t ldq;
+  int32_t k_slabs;                               // K * elem / 128
+  int32_t tiles_m, tiles_n, syrk, tiles_per_mat;
+  const char* E;   int64_t e_mat;  int32_t lde;   // epilogue input (A or X), bytes
+  char* C;         int64_t c_mat;  int32_t ldc;   // output, direct orientation
+  char* CT;        int64_t ct_mat; int32_t ldct;  // output, transposed orientation
+  float alpha, beta;
+  const MatDesc* desc;
+  int32_t final_kind, param_dtype;
+  int32_t s, l;
+};
+
+constexpr int kRowBytes = 144;                   // 128 data + 16 pad per LDS row
+constexpr int kOpBytes = kTile * kRowBytes;      // one operand slab
+constexpr int kStageBytes = 2 * kOpBytes;
+constexpr int kFStride = 137;                    // fp32 epilogue tile stride (odd)
+static_assert(kTile * kFStride * 4 <= 2 * kStageBytes, "epilogue tile fits in LDS");
+
+template <typename T> struct Mma;
+template <> struct Mma<uint16_t> {
+  __device__ __forceinline__ static void run(const u32x4_t& a, const u32x4_t& b, f32x16_t& c) {
+    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+  }
+};
+template <> struct Mma<float> {
+  __device__ __forceinline__ static void run(const u32x4_t& a, const u32x4_t& b, f32x16_t& c) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[j]), __uint_as_float(b[j]), c,
+                                               0, 0, 0);
+  }
+};
+
+template <typename T, int EPI>
+__global__ __launch_bounds__(256, 2) void k_gemm_nt(GemmArgs ga) {
+  __shared__ __attribute__((aligned(16))) char smem[2 * kStageBytes];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  // ---- tile assignment -----------------------------------------------------
+  const int mat = blockIdx.x / ga.tiles_per_mat;
+  int t = blockIdx.x - mat * ga.tiles_per_mat;
+  int bm, bn;
+  if (ga.syrk) {  // upper-triangle tiles bm <= bn, row by row
+    bm = 0;
+    while (t >= ga.tiles_m - bm) { t -= ga.tiles_m - bm; ++bm; }
+    bn = bm + t;
+  } else {
+    bm = t / ga.tiles_n;
+    bn = t - bm * ga.tiles_n;
+  }
+  const char* Pb = ga.P + mat * ga.p_mat + static_cast<int64_t>(bm) * kTile * ga.ldp;
+  const char* Qb = ga.Q + mat * ga.q_mat + static_cast<int64_t>(bn) * kTile * ga.ldq;
+
+  // ---- main loop -----------------------------------------------------------
+  // Global -> register staging: row (tid/8 + 32v), 16-byte column (tid%8).
+  const int lrow = tid >> 3, lcol = (tid & 7) * 16;
+  u32x4_t rp[4], rq[4];
+  auto gload = [&](int ks) {
+    const int64_t koff = static_cast<int64_t>(ks) * 128 + lcol;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      rp[v] = *reinterpret_cast<const u32x4_t*>(Pb + static_cast<int64_t>(lrow + 32 * v) * ga.ldp + koff);
+      rq[v] = *reinterpret_cast<const u32x4_t*>(Qb + static_cast<int64_t>(lrow + 32 * v) * ga.ldq + koff);
+    }
+  };
+  auto sstore = [&](int stage) {
+    char* sp = smem + stage * kStageBytes;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      *reinterpret_cast<u32x4_t*>(sp + (lrow + 32 * v) * kRowBytes + lcol) = rp[v];
+      *reinterpret_cast<u32x4_t*>(sp + kOpBytes + (lrow + 32 * v) * kRowBytes + lcol) = rq[v];
+    }
+  };
+
+  f32x16_t acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int arow = wm * 64 + (lane & 31), brow = wn * 64 + (lane & 31);
+  const int khalf = (lane >> 5) * 16;
+
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int ks = 0; ks < ga.k_slabs; ++ks) {
+    const int stage = ks & 1;
+    if (ks + 1 < ga.k_slabs) gload(ks + 1);
+    const char* sp = smem + stage * kStageBytes;
+#pragma unroll
+    for (int grp = 0; grp < 4; ++grp) {
+      u32x4_t a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        a[i] = *reinterpret_cast<const u32x4_t*>(sp + (arow + 32 * i) * kRowBytes + grp * 32 + khalf);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        b[j] = *reinterpret_cast<const u32x4_t*>(sp + kOpBytes + (brow + 32 * j) * kRowBytes + grp * 32 + khalf);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) Mma<T>::run(a[i], b[j], acc[i][j]);
+    }
+    if (ks + 1 < ga.k_slabs) sstore(stage ^ 1);
+    __syncthreads();
+  }
+
+  // ---- epilogue: accumulators -> LDS fp32 tile ------------------------------
+  float* ft = reinterpret_cast<float*>(smem);
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        const int col = wn * 64 + j * 32 + (lane & 31);
+        ft[row * kFStride + col] = acc[i][j][r];
+      }
+  __syncthreads();
+
+  const bool diag = ga.syrk && bm == bn;
+  const int gi0 = bm * kTile, gj0 = bn * kTile;  // tile origin (rows of P, rows of Q)
+  const MatDesc* md = (EPI == EPI_FINAL) ? ga.desc + mat : nullptr;
+  const bool tr = (EPI == EPI_FINAL) ? md->transposed != 0 : false;
+
+  // Phase A: direct orientation, consecutive lanes on consecutive columns.
+  for (int idx = tid; idx < kTile * kTile; idx += 256) {
+    const int r = idx >> 7, c = idx & 127;
+    const int gi = gi0 + r, gj = gj0 + c;
+    float v;
+    if (EPI == EPI_GRAM || EPI == EPI_POLY) {
+      v = diag && r > c ? ft[c * kFStride + r] : ft[r * kFStride + c];
+      if (EPI == EPI_POLY) {
+        const float e = to_f32<T>(*reinterpret_cast<const T*>(ga.E + mat * ga.e_mat + static_cast<int64_t>(gi) * ga.lde + gj * static_cast<int>(sizeof(T))));
+        v = fmaf(ga.alpha, e, ga.beta * v);
+      }
+      const T o = from_f32<T>(v);
+      *reinterpret_cast<T*>(ga.C + mat * ga.c_mat + static_cast<int64_t>(gi) * ga.ldc + gj * static_cast<int>(sizeof(T))) = o;
+      if (!diag) ft[r * kFStride + c] = to_f32<T>(o);  // for the mirror store
+    } else {
+      const float e = to_f32<T>(*reinterpret_cast<const T*>(ga.E + mat * ga.e_mat + static_cast<int64_t>(gi) * ga.lde + gj * static_cast<int>(sizeof(T))));
+      v = fmaf(ga.alpha, e, ft[r * kFStride + c]);
+      if (EPI == EPI_UPDATE) {
+        const T o = from_f32<T>(v);
+        *reinterpret_cast<T*>(ga.C + mat * ga.c_mat + static_cast<int64_t>(gi) * ga.ldc + gj * static_cast<int>(sizeof(T))) = o;
+        ft[r * kFStride + c] = to_f32<T>(o);
+      } else {  // EPI_FINAL
+        if (!tr) {
+          if (gi < ga.s && gj < ga.l) {
+            const int64_t pidx = static_cast<int64_t>(gi) * md->cols + gj;
+            if (ga.final_kind == 0) {
+              const float w = load_as_f32(md->W, pidx, ga.param_dtype);
+              store_from_f32(md->W, pidx, ga.param_dtype, fmaf(md->decay, w, -md->upd_scale * v));
+            } else {
+              store_from_f32(md->out, pidx, ga.param_dtype, v);
+            }
+          }
+        } else {
+          ft[r * kFStride + c] = v;
+        }
+      }
+    }
+  }
+  const bool phase_b = (EPI == EPI_GRAM || EPI == EPI_POLY) ? !diag : (EPI == EPI_UPDATE ? true : tr);
+  if (!phase_b) return;  // uniform across the workgroup
+  __syncthreads();
+  // Phase B: transposed orientation, consecutive lanes on consecutive rows r.
+  for (int idx = tid; idx < kTile * kTile; idx += 256) {
+    const int c = idx >> 7, r = idx & 127;
+    const float v = ft[r * kFStride + c];
+    const int gi = gi0 + r, gj = gj0 + c;
+    if (EPI == EPI_FINAL) {
+      if (gi < ga.s && gj < ga.l) {  // parameter is l x s: element (gj, gi)
+        const int64_t pidx = static_cast<int64_t>(gj) * md->cols + gi;
+        if (ga.final_kind == 0) {
+          const float w = load_as_f32(md->W, pidx, ga.param_dtype);
+          store_from_f32(md->W, pidx, ga.param_dtype, fmaf(md->decay, w, -md->upd_scale * v));
+        } else {
+          store_from_f32(md->out, pidx, ga.param_dtype, v);
+        }
+      }
+    } else {
+      *reinterpret_cast<T*>(ga.CT + mat * ga.ct_mat + static_cast<int64_t>(gj) * ga.ldct + gi * static_cast<int>(sizeof(T))) = from_f32<T>(v);
+    }
+  }
+}
+
+// Update from X0 when K = 0: O is X0 in the caller's layout (the direct
+// buffer), one thread per element of the u-domain; grid = (ceil(rows*cols /
+// 256), matrices).
+template <typename XT>
+__global__ __launch_bounds__(256) void k_apply_x0(const MatDesc* __restrict__ desc, ChunkGeom cg,
+                                                  const XT* __restrict__ X, const XT* __restrict__ XTb,
+                                                  int final_kind) {
+  const int m = blockIdx.y;
+  const MatDesc md = desc[m];
+  const int64_t numel = static_cast<int64_t>(md.rows) * md.cols;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= numel) return;
+  const int64_t ur = i / md.cols, uc = i - ur * md.cols;
+  const int64_t matX = static_cast<int64_t>(cg.S) * cg.L;
+  const XT* D = (md.transposed ? XTb : X) + m * matX;
+  const int ldD = md.transposed ? cg.S : cg.L;
+  const float o = to_f32<XT>(D[ur * ldD + uc]);
+  if (final_kind == 0) {
+    const float w = load_as_f32(md.W, i, cg.param_dtype);
+    store_from_f32(md.W, i, cg.param_dtype, fmaf(md.decay, w, -md.upd_scale * o));
+  } else {
+    store_from_f32(md.out, i, cg.param_dtype, o);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Host-side launch sequence for one chunk.
+// ---------------------------------------------------------------------------
+template <typename T>
+hipError_t launch_gemm(int epi, GemmArgs ga, int nmat, hipStream_t st) {
+  const dim3 grid(static_cast<unsigned>(ga.tiles_per_mat) * nmat), block(256);
+  switch (epi) {
+    case EPI_GRAM: hipLaunchKernelGGL((k_gemm_nt<T, EPI_GRAM>), grid, block, 0, st, ga); break;
+    case EPI_POLY: hipLaunchKernelGGL((k_gemm_nt<T, EPI_POLY>), grid, block, 0, st, ga); break;
+    case EPI_UPDATE: hipLaunchKernelGGL((k_gemm_nt<T, EPI_UPDATE>), grid, block, 0, st, ga); break;
+    default: hipLaunchKernelGGL((k_gemm_nt<T, EPI_FINAL>), grid, block, 0, st, ga); break;
+  }
+  return hipGetLastError();
+}
+
+template <typename GT, typename XT>
+hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBuffers& wb,
+                       const StepScalars& sc, const float* coeffs, int K, hipStream_t st) {
+  const int nmat = cg.nmat;
+  const int64_t numel = static_cast<int64_t>(cg.s) * cg.l;
+  const int nblk = static_cast<int>(norm_blocks(numel));
+  if (sc.momentum)
+    hipLaunchKernelGGL((k_partials<GT, true>), dim3(nblk, nmat), dim3(256), 0, st, d_desc, nblk, sc, wb.partials);
+  else
+    hipLaunchKernelGGL((k_partials<GT, false>), dim3(nblk, nmat), dim3(256), 0, st, d_desc, nblk, sc, wb.partials);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_finalize, dim3(nmat), dim3(256), 0, st, wb.partials, nblk, sc.eps, wb.rscale);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const dim3 ngrid(cg.L / 64, cg.S / 64, nmat);
+  if (sc.momentum)
+    hipLaunchKernelGGL((k_normalize<GT, XT, true>), ngrid, dim3(256), 0, st, d_desc, wb.rscale, sc, cg,
+                       static_cast<XT*>(wb.X[0]), static_cast<XT*>(wb.XT[0]));
+  else
+    hipLaunchKernelGGL((k_normalize<GT, XT, false>), ngrid, dim3(256), 0, st, d_desc, wb.rscale, sc, cg,
+                       static_cast<XT*>(wb.X[0]), static_cast<XT*>(wb.XT[0]));
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+
+  if (K == 0) {
+    const int64_t blocks = (numel + 255) / 256;
+    hipLaunchKernelGGL((k_apply_x0<XT>), dim3(static_cast<unsigned>(blocks), nmat), dim3(256), 0, st,
+                       d_desc, cg, static_cast<const XT*>(wb.X[0]), static_cast<const XT*>(wb.XT[0]),
+                       sc.final_kind);
+    return hipGetLastError();
+  }
+
+  const int es = static_cast<int>(sizeof(XT));
+  const int64_t matX = static_cast<int64_t>(cg.S) * cg.L * es;
+  const int64_t matA = static_cast<int64_t>(cg.S) * cg.S * es;
+  const int ts = cg.S / kTile, tl = cg.L / kTile;
+  int cur = 0;
+  for (int k = 0; k < K; ++k) {
+    const float a = coeffs[3 * k], b = coeffs[3 * k + 1], c = coeffs[3 * k + 2];
+    const char* X = static_cast<const char*>(wb.X[cur]);
+    const char* XTc = static_cast<const char*>(wb.XT[cur]);
+    // A = X X^T: M = N = S, K = L.
+    GemmArgs g{};
+    g.P = X; g.p_mat = matX; g.ldp = cg.L * es;
+    g.Q = X; g.q_mat = matX; g.ldq = cg.L * es;
+    g.k_slabs = cg.L * es / 128;
+    g.tiles_m = ts; g.tiles_n = ts; g.syrk = 1; g.tiles_per_mat = ts * (ts + 1) / 2;
+    g.C = static_cast<char*>(wb.A); g.c_mat = matA; g.ldc = cg.S * es;
+    g.CT = g.C; g.ct_mat = matA; g.ldct = g.ldc;
+    if ((e = launch_gemm<XT>(EPI_GRAM, g, nmat, st)) != hipSuccess) return e;
+    // B = b A + c A A^T: M = N = K = S.
+    GemmArgs p = g;
+    p.P = static_cast<const char*>(wb.A); p.p_mat = matA; p.ldp = cg.S * es;
+    p.Q = p.P; p.q_mat = matA; p.ldq = p.ldp;
+    p.k_slabs = cg.S * es / 128;
+    p.E = p.P; p.e_mat = matA; p.lde = p.ldp;
+    p.C = static_cast<char*>(wb.B); p.CT = p.C;
+    p.alpha = b; p.beta = c;
+    if ((e = launch_gemm<XT>(EPI_POLY, p, nmat, st)) != hipSuccess) return e;
+    // X' = a X + B X = a X + B (X^T)^T: M = S, N = L, K = S.
+    GemmArgs u{};
+    u.P = static_cast<const char*>(wb.B); u.p_mat = matA; u.ldp = cg.S * es;
+    u.Q = XTc; u.q_mat = matX; u.ldq = cg.S * es;
+    u.k_slabs = cg.S * es / 128;
+    u.tiles_m = ts; u.tiles_n = tl; u.syrk = 0; u.tiles_per_mat = ts * tl;
+    u.E = X; u.e_mat = matX; u.lde = cg.L * es;
+    u.alpha = a;
+    u.s = cg.s; u.l = cg.l;
+    if (k + 1 < K) {
+      u.C = static_cast<char*>(wb.X[cur ^ 1]); u.c_mat = matX; u.ldc = cg.L * es;
+      u.CT = static_cast<char*>(wb.XT[cur ^ 1]); u.ct_mat = matX; u.ldct = cg.S * es;
+      if ((e = launch_gemm<XT>(EPI_UPDATE, u, nmat, st)) != hipSuccess) return e;
+      cur ^= 1;
+    } else {
+      u.desc = d_desc; u.final_kind = sc.final_kind; u.param_dtype = cg.param_dtype;
+      if ((e = launch_gemm<XT>(EPI_FINAL, u, nmat, st)) != hipSuccess) return e;
+    }
+  }
+  return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t run_chunk(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBuffers& wb,
+                     const StepScalars& sc, const float* coeffs, int K, hipStream_t st) {
+  const bool gbf = cg.grad_dtype == DT_BF16;
+  if (cg.ns_f32) {
+    return gbf ? run_chunk_t<uint16_t, float>(cg, d_desc, wb, sc, coeffs, K, st)
+               : run_chunk_t<float, float>(cg, d_desc, wb, sc, coeffs, K, st);
+  }
+  return gbf ? run_chunk_t<uint16_t, uint16_t>(cg, d_desc, wb, sc, coeffs, K, st)
+             : run_chunk_t<float, uint16_t>(cg, d_desc, wb, sc, coeffs, K, st);
+}
+
+}  // namespace muon

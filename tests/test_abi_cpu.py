@@ -1,0 +1,199 @@
+"""The C-ABI library on the CPU: it loads, exports what the header declares,
+validates arguments and plans batches without touching a device.
+
+The planner follows Sec. 6.6: matrices grouped by core shape after
+transpose-first (rows > cols runs on the transpose), batches capped at 2^29
+elements, larger work first; an [E, M, N] entry is E matrices (Sec. 6.3).
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_21594_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "muon_hip.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(B.LIB_PATH):
+        pytest.fail("libmuon_hip.so is not built (run __graft_entry__.build())")
+    return B.load_library()
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*([a-z_0-9]+)\s*\(", text, flags=re.M)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = header_functions()
+    assert "muon_step" in names and "ns_orthogonalize_batched" in names
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in muon_hip.h but not exported"
+    assert set(B.EXPORTS) <= set(names)
+
+
+def test_abi_version_and_status_strings(lib):
+    assert lib.muon_abi_version() == 1
+    for code, name in B.STATUS.items():
+        assert lib.muon_status_string(code).decode() == name
+
+
+def test_struct_layouts_match_header():
+    # sizes the C compiler gives these structs on x86-64
+    assert ctypes.sizeof(B.MuonParam) == 64
+    assert ctypes.sizeof(B.MuonHParams) == 48
+    assert ctypes.sizeof(B.MuonChunkInfo) == 64
+
+
+# fake, never dereferenced device addresses for host-only checks
+BASE = 1 << 40
+
+
+def entry(addr, rows, cols, batch=1, pdt=B.BF16, gdt=B.BF16, ld=0, gap=None):
+    n = rows * cols * batch
+    es_p = 2 if pdt == B.BF16 else 4
+    es_g = 2 if gdt == B.BF16 else 4
+    W = addr
+    G = W + n * es_p
+    M = G + n * es_g
+    end = M + n * 4
+    return B.MuonParam(W, G, M, rows, cols, batch, ld, pdt, gdt), end
+
+
+def entries(shapes, **kw):
+    out, addr = [], BASE
+    for s in shapes:
+        e, addr = entry(addr, *s, **kw)
+        out.append(e)
+        addr = (addr + 4095) // 4096 * 4096
+    return out
+
+
+def hp(**kw):
+    h, keep = B.make_hparams(**kw)
+    hp._keep = keep
+    return h
+
+
+def test_validation_accepts_good_request(lib):
+    st, msg = B.validate_step(entries([(64, 32), (3, 5, 7)]), hp())
+    assert st == B.MUON_OK, msg
+
+
+@pytest.mark.parametrize("mutate,expect", [
+    (lambda e: setattr(e, "param", 0), 1),
+    (lambda e: setattr(e, "grad", 0), 1),
+    (lambda e: setattr(e, "momentum", 0), 1),
+    (lambda e: setattr(e, "rows", 0), 1),
+    (lambda e: setattr(e, "cols", -3), 1),
+    (lambda e: setattr(e, "batch", 0), 1),
+    (lambda e: setattr(e, "param_dtype", 7), 1),
+    (lambda e: setattr(e, "grad_dtype", -1), 1),
+    (lambda e: setattr(e, "ld", 99), 2),
+    (lambda e: setattr(e, "momentum", e.momentum + 2), 1),   # misaligned fp32
+    (lambda e: setattr(e, "grad", e.param + 16), 1),          # grad overlaps param
+    (lambda e: setattr(e, "momentum", e.grad), 1),            # momentum overlaps grad
+])
+def test_validation_rejects_bad_entry(lib, mutate, expect):
+    es = entries([(64, 32), (16, 16)])
+    mutate(es[1])
+    st, msg = B.validate_step(es, hp())
+    assert st == expect, msg
+    assert msg
+
+
+def test_validation_rejects_cross_entry_overlap(lib):
+    es = entries([(64, 32), (16, 16)])
+    es[1].param = es[0].momentum + 64  # inside entry 0's momentum
+    st, _ = B.validate_step(es, hp())
+    assert st == 1
+
+
+def test_validation_allows_shared_gradients(lib):
+    es = entries([(64, 32), (64, 32)])
+    es[1].grad = es[0].grad  # two read-only buffers may alias
+    st, msg = B.validate_step(es, hp())
+    assert st == B.MUON_OK, msg
+
+
+@pytest.mark.parametrize("kw", [dict(ns_steps=-1), dict(ns_steps=65), dict(eps=-1.0),
+                                dict(lr=float("nan")), dict(beta=float("inf")),
+                                dict(ns_coeffs=[(1.0, float("nan"), 0.0)], ns_steps=1),
+                                dict(max_chunk_elems=-5)])
+def test_validation_rejects_bad_hparams(lib, kw):
+    st, msg = B.validate_step(entries([(8, 8)]), hp(**kw))
+    assert st == 1, msg
+
+
+def test_zero_entries_is_valid(lib):
+    arr = (B.MuonParam * 1)()
+    h, keep = B.make_hparams()
+    assert lib.muon_validate_step(arr, 0, ctypes.byref(h), None, 0) == 0
+    assert lib.muon_validate_step(None, 0, ctypes.byref(h), None, 0) == 0
+    assert lib.muon_validate_step(None, 1, ctypes.byref(h), None, 0) == 1
+    assert lib.muon_validate_step(arr, 0, None, None, 0) == 1
+
+
+def test_null_handle_is_rejected(lib):
+    h, keep = B.make_hparams()
+    arr = (B.MuonParam * 1)(*entries([(8, 8)]))
+    assert lib.muon_step(None, arr, 1, ctypes.byref(h), None) == 1
+    assert lib.ns_orthogonalize_batched(None, None, None, None, None, 0, 1, 5, None, 1e-7, 0, None) == 1
+    assert lib.muon_destroy(None) == 1
+    assert lib.muon_reserve(None, 10) == 1
+    assert lib.muon_last_error(None).decode() == "NULL handle"
+
+
+# ---------------------------------------------------------------------------
+# Planner (Sec. 6.6)
+# ---------------------------------------------------------------------------
+def test_plan_buckets_by_core_shape_after_transpose(lib):
+    es = entries([(1024, 4096), (4096, 1024), (512, 512), (128, 2048), (1024, 4096)])
+    st, chunks, ws, order = B.plan_step(es, hp())
+    assert st == 0
+    shapes = [(c["s"], c["l"], c["count"]) for c in chunks]
+    # 1024x4096 and its transpose share one bucket; larger s^2 l first
+    assert shapes == [(1024, 4096, 3), (512, 512, 1), (128, 2048, 1)]
+    assert order == [0, 1, 4, 2, 3]
+
+
+def test_plan_chunks_at_cap_and_experts_expand(lib):
+    es = entries([(4096, 11008), (11008, 4096, 3), (4096, 4096, 2)])
+    st, chunks, ws, order = B.plan_step(es, hp())
+    assert st == 0
+    # 4096 x 11008 = 45.1M elements: 11 fit under 2^29; four such matrices here
+    assert [(c["s"], c["l"], c["count"]) for c in chunks] == [(4096, 11008, 4), (4096, 4096, 2)]
+    st, chunks, ws2, order = B.plan_step(es, hp(max_chunk_elems=2 * 4096 * 11008))
+    assert [(c["count"]) for c in chunks] == [2, 2, 2]
+    assert order == [0, 1, 2, 3, 4, 5]
+    assert ws2 < ws
+
+
+def test_plan_single_matrix_above_cap_still_runs(lib):
+    st, chunks, ws, order = B.plan_step(entries([(300, 500)]), hp(max_chunk_elems=1000))
+    assert st == 0 and [c["count"] for c in chunks] == [1]
+
+
+def test_plan_padding_and_workspace_bytes(lib):
+    st, chunks, ws, _ = B.plan_step(entries([(17, 33), (33, 17)]), hp())
+    assert st == 0
+    c, = chunks
+    assert (c["s"], c["l"], c["s_pad"], c["l_pad"], c["count"]) == (17, 33, 128, 128, 2)
+    # 4 X buffers + A + B (bf16) + norm partials + 1/(norm+eps)
+    xb = 2 * 128 * 128 * 2
+    assert c["workspace_bytes"] == 6 * xb + 256 + 256 and ws == c["workspace_bytes"]
+    st, chunks32, ws32, _ = B.plan_step(entries([(17, 33), (33, 17)]), hp(ns_precision="f32"))
+    assert ws32 == 6 * 2 * xb + 512
+
+
+def test_plan_separates_dtypes(lib):
+    a = entries([(64, 64)], pdt=B.F32, gdt=B.F32)
+    b, _ = entry(BASE + (1 << 30), 64, 64)
+    st, chunks, ws, order = B.plan_step(a + [b], hp())
+    assert st == 0 and len(chunks) == 2

@@ -1,0 +1,332 @@
+"""Parity of the HIP path with the fp64 oracle, called through the C ABI.
+
+Sizes span several 128-wide tiles and ragged tails; every case compares each
+matrix with the oracle at the gates of the method: relative Frobenius error
+<= 2e-2 on the bf16 Newton-Schulz path, <= 1e-4 on the fp32 path (plus the
+storage-rounding floor of the output dtype), momentum <= 1e-6.
+"""
+import numpy as np
+import pytest
+
+from oracle import muon_ref as ref
+from paper_2609_21594_amd import synth
+from tests.gpu_util import (MOMENTUM_TOL, TOL, decode, o_gate, rel, require_gpu, to_bits,
+                            to_dev, to_host, tol_for, w_gate)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def muon():
+    require_gpu()
+    from paper_2609_21594_amd.binding import Muon
+    m = Muon(0)
+    yield m
+    m.close()
+
+
+def rng(*key):
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([4242, *key])))
+
+
+def gen(shape, sigma, dtype, *key):
+    return synth.draw(shape, sigma, dtype, rng(*key))
+
+
+SHAPES = [(1, 1), (1, 7), (7, 1), (17, 33), (33, 17), (64, 64), (128, 256), (256, 128),
+          (129, 257), (300, 200), (130, 1000), (384, 384)]
+
+
+def run_orth(muon, shapes, dtype, prec, ns_steps=5, coeffs=None, eps=1e-7, sigma=1.0, key=0):
+    import torch
+    G = [gen(s, sigma, dtype, key, i) for i, s in enumerate(shapes)]
+    ins = [to_dev(g, dtype) for g in G]
+    outs = [torch.empty_like(t) for t in ins]
+    muon.orthogonalize(ins, outs, ns_steps=ns_steps, ns_coeffs=coeffs, eps=eps, ns_precision=prec)
+    torch.cuda.synchronize()
+    return G, outs
+
+
+@pytest.mark.parametrize("dtype,prec", [("bf16", "bf16"), ("f32", "f32"), ("bf16", "f32"),
+                                        ("f32", "bf16")])
+def test_orthogonalize_matches_oracle(muon, dtype, prec):
+    G, outs = run_orth(muon, SHAPES, dtype, prec, key=1)
+    for s, g, o in zip(SHAPES, G, outs):
+        want = ref.orthogonalize(decode(g, dtype), 5)
+        err, rho = o_gate(to_host(o), want, dtype)
+        assert err <= tol_for(prec, s) + rho, (s, err, rho)
+
+
+@pytest.mark.parametrize("nesterov", [True, False])
+@pytest.mark.parametrize("pdt,gdt,prec", [("bf16", "bf16", "bf16"), ("f32", "f32", "f32"),
+                                          ("f32", "bf16", "bf16"), ("bf16", "f32", "f32")])
+def test_muon_step_matches_oracle(muon, pdt, gdt, prec, nesterov):
+    import torch
+    shapes = [(17, 33), (33, 17), (128, 256), (300, 200), (64, 64), (1, 50)]
+    hp = ref.MuonHParams(lr=0.02, beta=0.9, weight_decay=0.1, nesterov=nesterov)
+    Ws = [gen(s, 0.02, pdt, 2, i, 0) for i, s in enumerate(shapes)]
+    gs = [gen(s, 1e-3, gdt, 2, i, 1) for i, s in enumerate(shapes)]
+    bs = [gen(s, 1e-3, "f32", 2, i, 2) for i, s in enumerate(shapes)]
+    dW = [to_dev(w, pdt) for w in Ws]
+    dg = [to_dev(g, gdt) for g in gs]
+    db = [to_dev(b, "f32") for b in bs]
+    muon.step(dW, dg, db, lr=hp.lr, beta=hp.beta, weight_decay=hp.weight_decay,
+              nesterov=nesterov, ns_precision=prec)
+    torch.cuda.synchronize()
+    for s, W, g, b, w_dev, b_dev in zip(shapes, Ws, gs, bs, dW, db):
+        W0 = decode(W, pdt)
+        r = ref.muon_step_matrix(W0, decode(g, gdt), np.asarray(b, np.float64), hp)
+        err, rho = w_gate(to_host(w_dev), r.W_new, W0, pdt)
+        assert err <= tol_for(prec, s) + rho, (s, err, rho)
+        assert rel(to_host(b_dev), r.buf_new) <= MOMENTUM_TOL, s
+
+
+def test_fp32_step_recovers_orthogonalised_update(muon):
+    # fp32 parameters: O = (decay*W - W') / (lr*scale) is checked at 1e-4.
+    import torch
+    shape = (256, 128)
+    hp = ref.MuonHParams(lr=0.02, beta=0.95, weight_decay=0.0)
+    W, g, b = (gen(shape, 1.0, "f32", 3, k) for k in range(3))
+    dW, dg, db = to_dev(W, "f32"), to_dev(g, "f32"), to_dev(b, "f32")
+    muon.step([dW], [dg], [db], lr=0.02, beta=0.95, ns_precision="f32")
+    torch.cuda.synchronize()
+    r = ref.muon_step_matrix(W.astype(np.float64), g, b, hp)
+    scale = 0.2 * np.sqrt(256)
+    O_gpu = (W.astype(np.float64) - to_host(dW)) / (0.02 * scale)
+    assert rel(O_gpu, r.O) <= 1e-4
+
+
+def test_custom_per_step_coefficients(muon):
+    # a convergent quintic for 12 steps: the output approaches U V^T
+    coeffs = [(15 / 8, -10 / 8, 3 / 8)] * 6 + [(3.4445, -4.7750, 2.0315)] * 2 + [(1.5, -0.5, 0.0)] * 4
+    shapes = [(96, 160), (200, 130)]
+    G, outs = run_orth(muon, shapes, "f32", "f32", ns_steps=len(coeffs), coeffs=coeffs, key=4)
+    for g, o in zip(G, outs):
+        want = ref.orthogonalize(g.astype(np.float64), len(coeffs), coeffs)
+        assert rel(to_host(o), want) <= 1e-4
+
+
+def test_zero_steps_returns_normalised_input(muon):
+    G, outs = run_orth(muon, [(40, 70), (70, 40)], "f32", "f32", ns_steps=0, key=5)
+    for g, o in zip(G, outs):
+        want = ref.orthogonalize(g.astype(np.float64), 0)
+        assert rel(to_host(o), want) <= 1e-6
+
+
+def test_zero_input_and_pure_decay(muon):
+    import torch
+    W = gen((100, 60), 1.0, "f32", 6, 0)
+    dW = to_dev(W, "f32")
+    dg = torch.zeros_like(dW)
+    db = torch.zeros_like(dW)
+    muon.step([dW], [dg], [db], lr=0.1, weight_decay=0.5, ns_precision="f32")
+    torch.cuda.synchronize()
+    # the decay factor 1 - lr*wd is an fp32 constant; one rounding of its product
+    decay = np.float64(np.float32(1.0 - np.float64(np.float32(0.1)) * np.float64(np.float32(0.5))))
+    np.testing.assert_array_equal(to_host(dW), ref.round_to_f32(decay * W.astype(np.float64)))
+    z = torch.zeros((33, 9), dtype=torch.bfloat16, device="cuda")
+    o = torch.full_like(z, 7.0)
+    muon.orthogonalize([z], [o])
+    torch.cuda.synchronize()
+    assert (to_host(o) == 0).all()
+
+
+def test_nan_propagates_to_its_matrix_only(muon):
+    import torch
+    g1 = gen((64, 96), 1.0, "f32", 7, 0)
+    g2 = gen((64, 96), 1.0, "f32", 7, 1)
+    g1[3, 5] = np.nan
+    ins = [to_dev(g1, "f32"), to_dev(g2, "f32")]
+    outs = [torch.empty_like(t) for t in ins]
+    muon.orthogonalize(ins, outs, ns_precision="f32")
+    torch.cuda.synchronize()
+    assert np.isnan(to_host(outs[0])).all()
+    assert rel(to_host(outs[1]), ref.orthogonalize(g2.astype(np.float64), 5)) <= 1e-4
+
+
+def test_tiny_and_scaled_inputs(muon):
+    # 1e-4-scaled and 1e-30-scaled matrices normalise like unit ones (P8)
+    import torch
+    shapes = [(48, 80)] * 3
+    base = gen((48, 80), 1.0, "f32", 8, 0)
+    ins = [to_dev(base * np.float32(s), "f32") for s in (1.0, 1e-4, 1e-12)]
+    outs = [torch.empty_like(t) for t in ins]
+    muon.orthogonalize(ins, outs, ns_precision="f32", eps=0.0)
+    torch.cuda.synchronize()
+    want = ref.orthogonalize(base.astype(np.float64), 5, eps=0.0)
+    for o in outs:
+        assert rel(to_host(o), want) <= 1e-4
+
+
+def test_orthogonal_input_closed_form(muon):
+    import torch
+    Q, _ = np.linalg.qr(rng(9).standard_normal((256, 256)))
+    f = Q.astype(np.float32)
+    out = torch.empty((256, 256), dtype=torch.float32, device="cuda")
+    muon.orthogonalize([to_dev(f, "f32")], [out], ns_precision="f32")
+    torch.cuda.synchronize()
+    s = 1.0 / (16.0 + 1e-7)
+    for a, b, c in [ref.LEGACY_QUINTIC] * 5:
+        s = a * s + b * s ** 3 + c * s ** 5
+    assert rel(to_host(out), s * f.astype(np.float64)) <= 1e-4
+
+
+# ---------------------------------------------------------------------------
+# Invariants of the batching (Sec. 6.6) and determinism
+# ---------------------------------------------------------------------------
+def _step_bits(muon, shapes, dtypes=("bf16", "bf16"), prec="bf16", key=10, **kw):
+    import torch
+    pdt, gdt = dtypes
+    dW = [to_dev(gen(s, 0.02, pdt, key, i, 0), pdt) for i, s in enumerate(shapes)]
+    dg = [to_dev(gen(s, 1e-3, gdt, key, i, 1), gdt) for i, s in enumerate(shapes)]
+    db = [to_dev(gen(s, 1e-3, "f32", key, i, 2), "f32") for i, s in enumerate(shapes)]
+    muon.step(dW, dg, db, ns_precision=prec, **kw)
+    torch.cuda.synchronize()
+    return [to_bits(t) for t in dW], [to_bits(t) for t in db]
+
+
+def test_deterministic_repeat(muon):
+    shapes = [(256, 384), (384, 256), (200, 200)]
+    a = _step_bits(muon, shapes)
+    b = _step_bits(muon, shapes)
+    for x, y in zip(a[0] + a[1], b[0] + b[1]):
+        np.testing.assert_array_equal(x, y)
+
+
+def test_batched_equals_single(muon):
+    # a matrix's bits do not depend on which other matrices share the call
+    import torch
+    shapes = [(256, 384), (384, 256), (200, 200), (256, 384)]
+    together = _step_bits(muon, shapes)
+    for i, s in enumerate(shapes):
+        dW = to_dev(gen(s, 0.02, "bf16", 10, i, 0), "bf16")
+        dg = to_dev(gen(s, 1e-3, "bf16", 10, i, 1), "bf16")
+        db = to_dev(gen(s, 1e-3, "f32", 10, i, 2), "f32")
+        muon.step([dW], [dg], [db])
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(to_bits(dW), together[0][i])
+        np.testing.assert_array_equal(to_bits(db), together[1][i])
+
+
+def test_chunk_cap_does_not_change_results(muon):
+    shapes = [(128, 256)] * 5 + [(64, 64)] * 3
+    full = _step_bits(muon, shapes, key=11)
+    tiny = _step_bits(muon, shapes, key=11, max_chunk_elems=1)
+    for x, y in zip(full[0] + full[1], tiny[0] + tiny[1]):
+        np.testing.assert_array_equal(x, y)
+
+
+def test_expert_stack_is_independent_matrices(muon):
+    import torch
+    E, M, N = 3, 96, 160
+    W = gen((E, M, N), 0.02, "bf16", 12, 0)
+    g = gen((E, M, N), 1e-3, "bf16", 12, 1)
+    b = gen((E, M, N), 1e-3, "f32", 12, 2)
+    dW, dg, db = to_dev(W, "bf16"), to_dev(g, "bf16"), to_dev(b, "f32")
+    muon.step([dW], [dg], [db])
+    torch.cuda.synchronize()
+    Wh = to_bits(dW)
+    hp = ref.MuonHParams()
+    for e in range(E):
+        pw, pg, pb = to_dev(W[e], "bf16"), to_dev(g[e], "bf16"), to_dev(b[e], "f32")
+        muon.step([pw], [pg], [pb])
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(to_bits(pw), Wh[e])
+        r = ref.muon_step_matrix(decode(W[e], "bf16"), decode(g[e], "bf16"), b[e].astype(np.float64), hp)
+        err, rho = w_gate(to_host(pw), r.W_new, decode(W[e], "bf16"), "bf16")
+        assert err <= TOL["bf16"] + rho
+
+
+def test_three_steps_equal_one_plus_resume(muon):
+    import torch
+    shapes = [(160, 96), (96, 96)]
+    W = [gen(s, 0.02, "bf16", 13, i, 0) for i, s in enumerate(shapes)]
+    b = [gen(s, 1e-3, "f32", 13, i, 2) for i, s in enumerate(shapes)]
+    grads = [[to_dev(gen(s, 1e-3, "bf16", 13, i, 10 + t), "bf16") for i, s in enumerate(shapes)]
+             for t in range(3)]
+    dW = [to_dev(w, "bf16") for w in W]
+    db = [to_dev(x, "f32") for x in b]
+    for t in range(3):
+        muon.step(dW, grads[t], db, weight_decay=0.1)
+    torch.cuda.synchronize()
+    dW2 = [to_dev(w, "bf16") for w in W]
+    db2 = [to_dev(x, "f32") for x in b]
+    muon.step(dW2, grads[0], db2, weight_decay=0.1)
+    torch.cuda.synchronize()
+    saved = [(t.cpu().clone(), m.cpu().clone()) for t, m in zip(dW2, db2)]
+    del dW2, db2
+    dW3 = [w.cuda() for w, _ in saved]
+    db3 = [m.cuda() for _, m in saved]
+    for t in (1, 2):
+        muon.step(dW3, grads[t], db3, weight_decay=0.1)
+    torch.cuda.synchronize()
+    for x, y in zip(dW + db, dW3 + db3):
+        np.testing.assert_array_equal(to_bits(x), to_bits(y))
+
+
+def test_unaligned_views_take_the_scalar_path(muon):
+    import torch
+    rows, cols = 37, 45
+    n = rows * cols
+    Wf = gen((n + 3,), 0.02, "bf16", 14, 0)
+    gf = gen((n + 5,), 1e-3, "bf16", 14, 1)
+    bf = gen((n + 1,), 1e-3, "f32", 14, 2)
+    dWf, dgf, dbf = to_dev(Wf, "bf16"), to_dev(gf, "bf16"), to_dev(bf, "f32")
+    dW = dWf[3:3 + n].view(rows, cols)
+    dg = dgf[5:5 + n].view(rows, cols)
+    db = dbf[1:1 + n].view(rows, cols)
+    muon.step([dW], [dg], [db])
+    torch.cuda.synchronize()
+    W0 = decode(Wf[3:3 + n], "bf16").reshape(rows, cols)
+    r = ref.muon_step_matrix(W0, decode(gf[5:5 + n], "bf16").reshape(rows, cols),
+                             bf[1:1 + n].astype(np.float64).reshape(rows, cols), ref.MuonHParams())
+    err, rho = w_gate(to_host(dW), r.W_new, W0, "bf16")
+    assert err <= TOL["bf16"] + rho
+    assert (to_host(dWf[:3]) == decode(Wf[:3], "bf16")).all()  # neighbours untouched
+
+
+def test_in_place_orthogonalize(muon):
+    import torch
+    g = gen((150, 90), 1.0, "bf16", 15, 0)
+    t = to_dev(g, "bf16")
+    muon.orthogonalize([t], [t])
+    torch.cuda.synchronize()
+    err, rho = o_gate(to_host(t), ref.orthogonalize(decode(g, "bf16"), 5), "bf16")
+    assert err <= TOL["bf16"] + rho
+
+
+def test_non_default_stream(muon):
+    import torch
+    shapes = [(256, 384)]
+    base = _step_bits(muon, shapes, key=16)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        dW = [to_dev(gen(shapes[0], 0.02, "bf16", 16, 0, 0), "bf16")]
+        dg = [to_dev(gen(shapes[0], 1e-3, "bf16", 16, 0, 1), "bf16")]
+        db = [to_dev(gen(shapes[0], 1e-3, "f32", 16, 0, 2), "f32")]
+        muon.step(dW, dg, db, stream=s)
+    s.synchronize()
+    np.testing.assert_array_equal(to_bits(dW[0]), base[0][0])
+
+
+def test_errors_leave_buffers_untouched(muon):
+    import torch
+    from paper_2609_21594_amd.binding import Muon, MuonError
+    W = gen((64, 64), 0.02, "bf16", 17, 0)
+    dW = to_dev(W, "bf16")
+    dg = to_dev(gen((64, 64), 1e-3, "bf16", 17, 1), "bf16")
+    db = to_dev(gen((64, 64), 1e-3, "f32", 17, 2), "f32")
+    with pytest.raises(MuonError) as e:
+        muon.step([dW], [dg], [db], ns_steps=-1)
+    assert e.value.status == 1
+    with pytest.raises(MuonError) as e:
+        muon.step([dW], [dW], [db])  # grad aliases param
+    assert e.value.status == 1
+    small = Muon(0)
+    small.set_workspace_limit(1024)
+    with pytest.raises(MuonError) as e:
+        small.step([dW], [dg], [db])
+    assert e.value.status == 3
+    small.close()
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(to_bits(dW), to_bits(to_dev(W, "bf16")))
