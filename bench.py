@@ -1,0 +1,230 @@
+"""Benchmark of the batched Muon step on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload 3] [--no-cpu-baseline]
+
+One step = one muon_step call over every matrix of the workload: momentum
+update, Frobenius normalisation, transpose-first cast, 5 Newton-Schulz steps
+(Gram, polynomial, update products) and the parameter update, all in the HIP
+library.  Inputs are the seeded synthetic workload, resident in HBM before
+the timed region.  Prints one JSON line.
+
+Default workload: a 7B-like per-device share, 8 layers of hidden 4096 and
+FFN 11008 (56 matrices: 32 x 4096x4096, 16 x 11008x4096, 8 x 4096x11008),
+bf16 parameters and gradients, fp32 momentum, bf16 Newton-Schulz products.
+
+roofline: the dominant kernel by time, its algorithmic flops (dense count of
+the product it computes) per launch over its mean launch duration, both from
+HIP events the library records around each launch on its own stream.
+cpu_baseline: the fp64 CPU oracle on a bounded sample of the same workload
+(one matrix of each shape bucket), extrapolated to the workload's mix.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "Muon-step matrices/s and NS TFLOP/s (% bf16 MFMA peak), 1×MI355X"
+PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA: 256 CU x 4 SIMD x 1024 flop/clk x 2.4 GHz
+PEAK_F32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_21594_amd", "csrc", "muon_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_update_gemm_workload3.json")
+
+
+def kernel_source_sha() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="also run one plain device copy of this size (HBM counter calibration)")
+    return ap.parse_args()
+
+
+def upload(inputs, wl):
+    import numpy as np
+    import torch
+
+    def dev(a, dt):
+        if dt == "bf16":
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+
+    W = [dev(m.W, wl.param_dtype) for m in inputs]
+    G = [dev(m.g, wl.grad_dtype) for m in inputs]
+    B = [dev(m.buf, "f32") for m in inputs]
+    return W, G, B
+
+
+def cpu_baseline(wl, inputs):
+    """Times the oracle on one matrix per (short, long) shape bucket and
+    extrapolates to the workload's mix of shapes."""
+    import numpy as np
+    from oracle import muon_ref as ref
+    try:
+        from threadpoolctl import threadpool_limits
+    except ImportError:  # pragma: no cover
+        threadpool_limits = None
+    cores = min(16, len(os.sched_getaffinity(0)))
+    buckets = {}
+    for i, m in enumerate(wl.matrices):
+        key = (min(m.rows, m.cols), max(m.rows, m.cols))
+        buckets.setdefault(key, []).append(i)
+    hp = ref.MuonHParams(lr=wl.lr, beta=wl.beta, weight_decay=wl.weight_decay,
+                         ns_steps=wl.ns_steps, nesterov=wl.nesterov)
+    dec = (lambda a, dt: ref.decode_bf16(a) if dt == "bf16" else np.asarray(a, np.float64))
+    total, sampled = 0.0, []
+    import contextlib
+    limit = threadpool_limits(limits=cores) if threadpool_limits else contextlib.nullcontext()
+    with limit:
+        for key, idx in buckets.items():
+            i = idx[0]
+            m = inputs[i]
+            t0 = time.perf_counter()
+            ref.muon_step_matrix(dec(m.W, wl.param_dtype), dec(m.g, wl.grad_dtype),
+                                 np.asarray(m.buf, np.float64), hp)
+            dt = time.perf_counter() - t0
+            total += dt * len(idx)
+            sampled.append(f"{wl.matrices[i].name} {wl.matrices[i].rows}x{wl.matrices[i].cols}: {dt:.2f}s")
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"value": len(wl.matrices) / total, "unit": "matrices/s", "cores": cores,
+            "kind": "oracle",
+            "sample": (f"fp64 NumPy oracle, one full Muon step on one matrix per shape bucket "
+                       f"({'; '.join(sampled)}), extrapolated by bucket counts to all "
+                       f"{len(wl.matrices)} matrices; {cores} BLAS threads on {cpu}")}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}): "
+              "this build has no multi-GPU path; run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2609_21594_amd import synth
+    from paper_2609_21594_amd.binding import Muon
+
+    wl = synth.WORKLOADS[args.workload]
+    if wl.orthogonalize_only:
+        raise SystemExit("bench.py times the Muon step; pick a workload with optimizer state")
+    t_gen = time.perf_counter()
+    inputs = synth.make_workload(wl)
+    W, G, B = upload(inputs, wl)
+    torch.cuda.synchronize()
+    gen_s = time.perf_counter() - t_gen
+
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    muon = Muon(0)
+    hp = dict(lr=wl.lr, beta=wl.beta, weight_decay=wl.weight_decay, ns_steps=wl.ns_steps,
+              nesterov=wl.nesterov, ns_precision=wl.ns_precision)
+    for _ in range(args.warmup):
+        muon.step(W, G, B, **hp)
+    torch.cuda.synchronize()
+    muon.profile(True)
+    muon.profile_read(reset=True)
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        muon.step(W, G, B, **hp)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    stats = muon.profile_read(reset=True)
+    muon.profile(False)
+
+    ms = elapsed * 1e3 / args.steps
+    n_mat = wl.n_matrices
+    ns_flops = synth.workload_ns_flops(wl)
+    peak = PEAK_BF16_TFLOPS if wl.ns_precision == "bf16" else PEAK_F32_TFLOPS
+
+    kernels = {}
+    for name, st in stats.items():
+        if not st["launches"]:
+            continue
+        d = {"launches_per_step": st["launches"] / args.steps,
+             "ms_per_step": st["total_ms"] / args.steps,
+             "mean_launch_us": st["total_ms"] * 1e3 / st["launches"]}
+        if st["flops"]:
+            d["tflops"] = st["flops"] / (st["total_ms"] * 1e-3) / 1e12
+            d["exec_tflops"] = st["exec_flops"] / (st["total_ms"] * 1e-3) / 1e12
+        else:
+            d["gbs"] = st["bytes"] / (st["total_ms"] * 1e-3) / 1e9
+        kernels[name] = d
+    dom = max(stats, key=lambda k: stats[k]["total_ms"])
+    ds = stats[dom]
+    if ds["flops"]:
+        achieved = ds["flops"] / ds["launches"] / (ds["total_ms"] / ds["launches"] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                "frac": achieved / peak}
+    else:
+        achieved = ds["bytes"] / (ds["total_ms"] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": achieved / PEAK_HBM_GBS}
+    roof["kernel"] = dom
+    roof["mean_launch_us"] = ds["total_ms"] * 1e3 / ds["launches"]
+    roof["algorithmic_per_launch"] = (ds["flops"] or ds["bytes"]) / ds["launches"]
+    roof["traffic"] = None
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            tr = json.load(f)
+        if tr.get("kernel_source_sha") == kernel_source_sha() and tr.get("kernel") == dom:
+            roof["traffic"] = tr.get("hbm_bytes_per_launch")
+
+    out = {
+        "metric": METRIC, "value": n_mat / (ms * 1e-3), "unit": "matrices/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": wl.ns_precision, "data": "synthetic",
+        "config": {"workload": wl.name, "matrices": n_mat,
+                   "shapes": "32x4096x4096, 16x11008x4096, 8x4096x11008" if wl.index == 3 else
+                   ", ".join(f"{m.rows}x{m.cols}" for m in wl.matrices[:8]),
+                   "ns_steps": wl.ns_steps, "ns_precision": wl.ns_precision,
+                   "param_dtype": wl.param_dtype, "grad_dtype": wl.grad_dtype,
+                   "momentum_dtype": "f32", "parallelism": "none (one GPU)"},
+        "ns_tflops": ns_flops / (ms * 1e-3) / 1e12,
+        "ns_pct_peak": 100.0 * ns_flops / (ms * 1e-3) / 1e12 / peak,
+        "roofline": roof,
+        "kernels": kernels,
+        "input_generation_s": gen_s,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, inputs)
+    muon.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

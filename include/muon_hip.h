@@ -156,6 +156,32 @@ muon_status_t muon_plan_step(const muon_param_t* params, int64_t n, const muon_h
                              muon_chunk_info_t* chunks, int64_t cap, int64_t* n_chunks,
                              size_t* workspace_bytes, int64_t* order);
 
+/* Per-kernel timing.  When enabled, every kernel the handle launches is
+ * bracketed by two HIP events on its launch stream; muon_profile_read waits
+ * for them and returns, per kernel family, the launch count, the summed
+ * event durations and the algorithmic work of those launches:
+ *   flops       dense flop count of the product the kernel computes
+ *               (2 s^2 l for X X^T and B X, 2 s^3 for A A; 0 for
+ *               elementwise kernels),
+ *   exec_flops  flops the kernel issues on the real extents (upper tiles
+ *               only for the symmetric products),
+ *   bytes       minimal HBM traffic: each operand read once, each output
+ *               written once.
+ * Families (in this order): momentum_norm, norm_finalize,
+ * normalize_transpose, gram_syrk, poly_syrk, update_gemm, update_apply_gemm,
+ * apply_x0.  `reset` != 0 clears the counters after reading. */
+typedef struct {
+  const char* name;
+  int64_t launches;
+  double total_ms;
+  double flops;
+  double exec_flops;
+  double bytes;
+} muon_kernel_stats_t;
+muon_status_t muon_profile_enable(muon_handle_t h, int enable);
+muon_status_t muon_profile_read(muon_handle_t h, muon_kernel_stats_t* out, int cap, int* n,
+                                int reset);
+
 const char* muon_status_string(muon_status_t s);
 /* Message of the last failure on h (empty string if none); valid until the
  * next call on h. */

@@ -50,10 +50,16 @@ class MuonChunkInfo(ctypes.Structure):
                 ("workspace_bytes", ctypes.c_size_t)]
 
 
+class MuonKernelStats(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char_p), ("launches", ctypes.c_int64),
+                ("total_ms", ctypes.c_double), ("flops", ctypes.c_double),
+                ("exec_flops", ctypes.c_double), ("bytes", ctypes.c_double)]
+
+
 EXPORTS = ["muon_create", "muon_destroy", "muon_reserve", "muon_set_workspace_limit",
            "muon_workspace_bytes", "muon_step", "ns_orthogonalize_batched",
            "muon_validate_step", "muon_plan_step", "muon_status_string", "muon_last_error",
-           "muon_abi_version"]
+           "muon_abi_version", "muon_profile_enable", "muon_profile_read"]
 
 _lib: Optional[ctypes.CDLL] = None
 
@@ -84,12 +90,16 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.muon_plan_step.argtypes = [ctypes.POINTER(MuonParam), i64, ctypes.POINTER(MuonHParams),
                                    ctypes.POINTER(MuonChunkInfo), i64, ctypes.POINTER(i64),
                                    ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(i64)]
+    lib.muon_profile_enable.argtypes = [vp, ctypes.c_int]
+    lib.muon_profile_read.argtypes = [vp, ctypes.POINTER(MuonKernelStats), ctypes.c_int,
+                                      ctypes.POINTER(ctypes.c_int), ctypes.c_int]
     lib.muon_status_string.argtypes = [ctypes.c_int]
     lib.muon_status_string.restype = ctypes.c_char_p
     lib.muon_last_error.argtypes = [vp]
     lib.muon_last_error.restype = ctypes.c_char_p
     for name in ("muon_create", "muon_destroy", "muon_reserve", "muon_set_workspace_limit",
-                 "muon_step", "ns_orthogonalize_batched", "muon_validate_step", "muon_plan_step"):
+                 "muon_step", "ns_orthogonalize_batched", "muon_validate_step", "muon_plan_step",
+                 "muon_profile_enable", "muon_profile_read"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -186,6 +196,18 @@ class Muon:
 
     def set_workspace_limit(self, nbytes: int):
         self._check(self.lib.muon_set_workspace_limit(self.h, int(nbytes)))
+
+    def profile(self, enable: bool = True):
+        """Bracket every launch with HIP events on its stream."""
+        self._check(self.lib.muon_profile_enable(self.h, int(bool(enable))))
+
+    def profile_read(self, reset: bool = True):
+        """{family: dict(launches, total_ms, flops, exec_flops, bytes)}; waits for the events."""
+        arr = (MuonKernelStats * 16)()
+        n = ctypes.c_int()
+        self._check(self.lib.muon_profile_read(self.h, arr, 16, ctypes.byref(n), int(bool(reset))))
+        return {arr[i].name.decode(): {f: getattr(arr[i], f) for f, _ in MuonKernelStats._fields_[1:]}
+                for i in range(n.value)}
 
     @property
     def workspace_bytes(self) -> int:

@@ -22,8 +22,57 @@ using muon::ChunkGeom;
 using muon::MatDesc;
 using muon::StepScalars;
 
+// Event-pair timing of every launch (enabled on demand).
+struct EventTimer : muon::LaunchTimer {
+  struct Pending { int kind; hipEvent_t a, b; double flops, exec, bytes; };
+  struct Acc { int64_t launches = 0; double ms = 0, flops = 0, exec = 0, bytes = 0; };
+  std::vector<hipEvent_t> pool;
+  std::vector<Pending> pending;
+  Acc acc[muon::KK_COUNT];
+  hipEvent_t cur_a = nullptr;
+  bool failed = false;
+
+  hipEvent_t take() {
+    if (!pool.empty()) { hipEvent_t e = pool.back(); pool.pop_back(); return e; }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) { failed = true; return nullptr; }
+    return e;
+  }
+  void begin(int, hipStream_t st) override {
+    cur_a = take();
+    if (cur_a && hipEventRecord(cur_a, st) != hipSuccess) failed = true;
+  }
+  void end(int kind, hipStream_t st, double flops, double exec, double bytes) override {
+    hipEvent_t b = take();
+    if (!cur_a || !b || hipEventRecord(b, st) != hipSuccess) { failed = true; return; }
+    pending.push_back({kind, cur_a, b, flops, exec, bytes});
+    cur_a = nullptr;
+  }
+  bool collect() {
+    for (const Pending& p : pending) {
+      float ms = 0.f;
+      if (hipEventSynchronize(p.b) != hipSuccess || hipEventElapsedTime(&ms, p.a, p.b) != hipSuccess)
+        failed = true;
+      Acc& a = acc[p.kind];
+      a.launches += 1; a.ms += ms; a.flops += p.flops; a.exec += p.exec; a.bytes += p.bytes;
+      pool.push_back(p.a);
+      pool.push_back(p.b);
+    }
+    pending.clear();
+    return !failed;
+  }
+  void reset() { for (Acc& a : acc) a = Acc(); failed = false; }
+  void destroy() {
+    collect();
+    for (hipEvent_t e : pool) (void)hipEventDestroy(e);
+    pool.clear();
+  }
+};
+
 struct muon_handle {
   int device = 0;
+  bool profiling = false;
+  EventTimer timer;
   void* ws = nullptr;
   size_t ws_bytes = 0;
   size_t ws_limit = 0;               // 0 = no cap
@@ -421,7 +470,8 @@ muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Pla
     b.A = ws + c.off_A; b.B = ws + c.off_B;
     b.partials = reinterpret_cast<float*>(ws + c.off_part);
     b.rscale = reinterpret_cast<float*>(ws + c.off_r);
-    hipError_t e = muon::run_chunk(g, h->d_desc + c.first, b, sc, coeffs, K, stream);
+    hipError_t e = muon::run_chunk(g, h->d_desc + c.first, b, sc, coeffs, K, stream,
+                                   h->profiling ? &h->timer : nullptr);
     if (e != hipSuccess) return device_fail(h, "kernel launch", e);
   }
   return MUON_OK;
@@ -481,6 +531,7 @@ muon_status_t muon_destroy(muon_handle_t h) {
     if (h->d_desc) (void)hipFree(h->d_desc);
     if (h->h_stage) (void)hipHostFree(h->h_stage);
     if (h->stage_done) (void)hipEventDestroy(h->stage_done);
+    h->timer.destroy();
   }
   delete h;
   return st;
@@ -500,6 +551,35 @@ muon_status_t muon_set_workspace_limit(muon_handle_t h, size_t bytes) {
 }
 
 size_t muon_workspace_bytes(muon_handle_t h) { return h ? h->ws_bytes : 0; }
+
+muon_status_t muon_profile_enable(muon_handle_t h, int enable) {
+  if (!h) return MUON_ERR_INVALID_ARGUMENT;
+  h->profiling = enable != 0;
+  return MUON_OK;
+}
+
+muon_status_t muon_profile_read(muon_handle_t h, muon_kernel_stats_t* out, int cap, int* n,
+                                int reset) {
+  static const char* const kNames[muon::KK_COUNT] = {
+      "momentum_norm", "norm_finalize", "normalize_transpose", "gram_syrk",
+      "poly_syrk", "update_gemm", "update_apply_gemm", "apply_x0"};
+  if (!h || (cap > 0 && !out)) return MUON_ERR_INVALID_ARGUMENT;
+  DeviceGuard dg(h->device);
+  const bool ok = h->timer.collect();
+  if (n) *n = muon::KK_COUNT;
+  for (int k = 0; k < cap && k < muon::KK_COUNT; ++k) {
+    const EventTimer::Acc& a = h->timer.acc[k];
+    out[k].name = kNames[k];
+    out[k].launches = a.launches;
+    out[k].total_ms = a.ms;
+    out[k].flops = a.flops;
+    out[k].exec_flops = a.exec;
+    out[k].bytes = a.bytes;
+  }
+  if (reset) h->timer.reset();
+  if (!ok) { set_err(h, "event timing failed"); return MUON_ERR_DEVICE; }
+  return MUON_OK;
+}
 
 muon_status_t muon_validate_step(const muon_param_t* params, int64_t n, const muon_hparams_t* hp,
                                  char* msg, size_t msg_len) {

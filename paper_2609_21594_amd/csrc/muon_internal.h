@@ -62,6 +62,19 @@ struct StepScalars {
   int32_t final_kind;   // 0: update W, 1: write out
 };
 
+// Kernel families, for the optional per-launch timing.
+enum KernelKind : int {
+  KK_PARTIALS = 0, KK_FINALIZE, KK_NORMALIZE, KK_GRAM, KK_POLY, KK_UPDATE, KK_FINAL,
+  KK_APPLY_X0, KK_COUNT
+};
+
+// Receives a bracket around every launch when timing is enabled.
+struct LaunchTimer {
+  virtual void begin(int kind, hipStream_t st) = 0;
+  virtual void end(int kind, hipStream_t st, double flops, double exec_flops, double bytes) = 0;
+  virtual ~LaunchTimer() = default;
+};
+
 inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 inline int64_t norm_blocks(int64_t numel) {
   return (numel + kNormElemsPerBlock - 1) / kNormElemsPerBlock;
@@ -72,6 +85,6 @@ inline int64_t norm_blocks(int64_t numel) {
 // Newton-Schulz steps (Gram, polynomial, update), and the final apply.
 hipError_t run_chunk(const ChunkGeom& g, const MatDesc* d_desc, const ChunkBuffers& wb,
                      const StepScalars& sc, const float* coeffs /* host, K x 3 */, int K,
-                     hipStream_t stream);
+                     hipStream_t stream, LaunchTimer* timer /* may be null */);
 
 }  // namespace muon

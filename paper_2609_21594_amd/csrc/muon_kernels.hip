@@ -466,41 +466,77 @@ hipError_t launch_gemm(int epi, GemmArgs ga, int nmat, hipStream_t st) {
   return hipGetLastError();
 }
 
+// Brackets one launch with the optional timer.
+struct Timed {
+  LaunchTimer* t;
+  int kind;
+  hipStream_t st;
+  Timed(LaunchTimer* timer, int k, hipStream_t s) : t(timer), kind(k), st(s) {
+    if (t) t->begin(kind, st);
+  }
+  void done(double flops, double exec_flops, double bytes) {
+    if (t) t->end(kind, st, flops, exec_flops, bytes);
+  }
+};
+
 template <typename GT, typename XT>
 hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBuffers& wb,
-                       const StepScalars& sc, const float* coeffs, int K, hipStream_t st) {
+                       const StepScalars& sc, const float* coeffs, int K, hipStream_t st,
+                       LaunchTimer* timer) {
   const int nmat = cg.nmat;
+  const double nm = nmat;
   const int64_t numel = static_cast<int64_t>(cg.s) * cg.l;
+  const double ne = double(numel);
+  const double s = cg.s, l = cg.l;
   const int nblk = static_cast<int>(norm_blocks(numel));
-  if (sc.momentum)
-    hipLaunchKernelGGL((k_partials<GT, true>), dim3(nblk, nmat), dim3(256), 0, st, d_desc, nblk, sc, wb.partials);
-  else
-    hipLaunchKernelGGL((k_partials<GT, false>), dim3(nblk, nmat), dim3(256), 0, st, d_desc, nblk, sc, wb.partials);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_finalize, dim3(nmat), dim3(256), 0, st, wb.partials, nblk, sc.eps, wb.rscale);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  const dim3 ngrid(cg.L / 64, cg.S / 64, nmat);
-  if (sc.momentum)
-    hipLaunchKernelGGL((k_normalize<GT, XT, true>), ngrid, dim3(256), 0, st, d_desc, wb.rscale, sc, cg,
-                       static_cast<XT*>(wb.X[0]), static_cast<XT*>(wb.XT[0]));
-  else
-    hipLaunchKernelGGL((k_normalize<GT, XT, false>), ngrid, dim3(256), 0, st, d_desc, wb.rscale, sc, cg,
-                       static_cast<XT*>(wb.X[0]), static_cast<XT*>(wb.XT[0]));
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const double gsz = sizeof(GT), xsz = sizeof(XT);
+  const double psz = cg.param_dtype == DT_BF16 ? 2.0 : 4.0;
+  hipError_t e;
+  {
+    Timed tm(timer, KK_PARTIALS, st);
+    if (sc.momentum)
+      hipLaunchKernelGGL((k_partials<GT, true>), dim3(nblk, nmat), dim3(256), 0, st, d_desc, nblk, sc, wb.partials);
+    else
+      hipLaunchKernelGGL((k_partials<GT, false>), dim3(nblk, nmat), dim3(256), 0, st, d_desc, nblk, sc, wb.partials);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    tm.done(0, 0, nm * ne * (gsz + (sc.momentum ? 8.0 : 0.0)) + nm * nblk * 4.0);
+  }
+  {
+    Timed tm(timer, KK_FINALIZE, st);
+    hipLaunchKernelGGL(k_finalize, dim3(nmat), dim3(256), 0, st, wb.partials, nblk, sc.eps, wb.rscale);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    tm.done(0, 0, nm * nblk * 4.0 + nm * 4.0);
+  }
+  {
+    Timed tm(timer, KK_NORMALIZE, st);
+    const dim3 ngrid(cg.L / 64, cg.S / 64, nmat);
+    if (sc.momentum)
+      hipLaunchKernelGGL((k_normalize<GT, XT, true>), ngrid, dim3(256), 0, st, d_desc, wb.rscale, sc, cg,
+                         static_cast<XT*>(wb.X[0]), static_cast<XT*>(wb.XT[0]));
+    else
+      hipLaunchKernelGGL((k_normalize<GT, XT, false>), ngrid, dim3(256), 0, st, d_desc, wb.rscale, sc, cg,
+                         static_cast<XT*>(wb.X[0]), static_cast<XT*>(wb.XT[0]));
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    tm.done(0, 0, nm * ne * (gsz + (sc.momentum ? 4.0 : 0.0) + 2.0 * xsz));
+  }
 
   if (K == 0) {
+    Timed tm(timer, KK_APPLY_X0, st);
     const int64_t blocks = (numel + 255) / 256;
     hipLaunchKernelGGL((k_apply_x0<XT>), dim3(static_cast<unsigned>(blocks), nmat), dim3(256), 0, st,
                        d_desc, cg, static_cast<const XT*>(wb.X[0]), static_cast<const XT*>(wb.XT[0]),
                        sc.final_kind);
-    return hipGetLastError();
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    tm.done(0, 0, nm * ne * (xsz + (sc.final_kind == 0 ? 2.0 * psz : psz)));
+    return hipSuccess;
   }
 
   const int es = static_cast<int>(sizeof(XT));
   const int64_t matX = static_cast<int64_t>(cg.S) * cg.L * es;
   const int64_t matA = static_cast<int64_t>(cg.S) * cg.S * es;
   const int ts = cg.S / kTile, tl = cg.L / kTile;
+  // flops the symmetric products issue: upper tiles only, on the real extent
+  const double syrk_frac = double(ts * (ts + 1) / 2) / double(ts * ts);
   int cur = 0;
   for (int k = 0; k < K; ++k) {
     const float a = coeffs[3 * k], b = coeffs[3 * k + 1], c = coeffs[3 * k + 2];
@@ -514,7 +550,11 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
     g.tiles_m = ts; g.tiles_n = ts; g.syrk = 1; g.tiles_per_mat = ts * (ts + 1) / 2;
     g.C = static_cast<char*>(wb.A); g.c_mat = matA; g.ldc = cg.S * es;
     g.CT = g.C; g.ct_mat = matA; g.ldct = g.ldc;
-    if ((e = launch_gemm<XT>(EPI_GRAM, g, nmat, st)) != hipSuccess) return e;
+    {
+      Timed tm(timer, KK_GRAM, st);
+      if ((e = launch_gemm<XT>(EPI_GRAM, g, nmat, st)) != hipSuccess) return e;
+      tm.done(nm * 2 * s * s * l, nm * 2 * s * s * l * syrk_frac, nm * (s * l + s * s) * xsz);
+    }
     // B = b A + c A A^T: M = N = K = S.
     GemmArgs p = g;
     p.P = static_cast<const char*>(wb.A); p.p_mat = matA; p.ldp = cg.S * es;
@@ -523,7 +563,11 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
     p.E = p.P; p.e_mat = matA; p.lde = p.ldp;
     p.C = static_cast<char*>(wb.B); p.CT = p.C;
     p.alpha = b; p.beta = c;
-    if ((e = launch_gemm<XT>(EPI_POLY, p, nmat, st)) != hipSuccess) return e;
+    {
+      Timed tm(timer, KK_POLY, st);
+      if ((e = launch_gemm<XT>(EPI_POLY, p, nmat, st)) != hipSuccess) return e;
+      tm.done(nm * 2 * s * s * s, nm * 2 * s * s * s * syrk_frac, nm * 2 * s * s * xsz);
+    }
     // X' = a X + B X = a X + B (X^T)^T: M = S, N = L, K = S.
     GemmArgs u{};
     u.P = static_cast<const char*>(wb.B); u.p_mat = matA; u.ldp = cg.S * es;
@@ -533,14 +577,21 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
     u.E = X; u.e_mat = matX; u.lde = cg.L * es;
     u.alpha = a;
     u.s = cg.s; u.l = cg.l;
+    const double uf = nm * 2 * s * s * l;
     if (k + 1 < K) {
       u.C = static_cast<char*>(wb.X[cur ^ 1]); u.c_mat = matX; u.ldc = cg.L * es;
       u.CT = static_cast<char*>(wb.XT[cur ^ 1]); u.ct_mat = matX; u.ldct = cg.S * es;
+      Timed tm(timer, KK_UPDATE, st);
       if ((e = launch_gemm<XT>(EPI_UPDATE, u, nmat, st)) != hipSuccess) return e;
+      // reads B, X^T, X; writes X', X'^T
+      tm.done(uf, uf, nm * (s * s + 4 * s * l) * xsz);
       cur ^= 1;
     } else {
       u.desc = d_desc; u.final_kind = sc.final_kind; u.param_dtype = cg.param_dtype;
+      Timed tm(timer, KK_FINAL, st);
       if ((e = launch_gemm<XT>(EPI_FINAL, u, nmat, st)) != hipSuccess) return e;
+      // reads B, X^T, X (and W); writes W or out
+      tm.done(uf, uf, nm * ((s * s + 2 * s * l) * xsz + s * l * (sc.final_kind == 0 ? 2 * psz : psz)));
     }
   }
   return hipSuccess;
@@ -549,14 +600,15 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
 }  // namespace
 
 hipError_t run_chunk(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBuffers& wb,
-                     const StepScalars& sc, const float* coeffs, int K, hipStream_t st) {
+                     const StepScalars& sc, const float* coeffs, int K, hipStream_t st,
+                     LaunchTimer* timer) {
   const bool gbf = cg.grad_dtype == DT_BF16;
   if (cg.ns_f32) {
-    return gbf ? run_chunk_t<uint16_t, float>(cg, d_desc, wb, sc, coeffs, K, st)
-               : run_chunk_t<float, float>(cg, d_desc, wb, sc, coeffs, K, st);
+    return gbf ? run_chunk_t<uint16_t, float>(cg, d_desc, wb, sc, coeffs, K, st, timer)
+               : run_chunk_t<float, float>(cg, d_desc, wb, sc, coeffs, K, st, timer);
   }
-  return gbf ? run_chunk_t<uint16_t, uint16_t>(cg, d_desc, wb, sc, coeffs, K, st)
-             : run_chunk_t<float, uint16_t>(cg, d_desc, wb, sc, coeffs, K, st);
+  return gbf ? run_chunk_t<uint16_t, uint16_t>(cg, d_desc, wb, sc, coeffs, K, st, timer)
+             : run_chunk_t<float, uint16_t>(cg, d_desc, wb, sc, coeffs, K, st, timer);
 }
 
 }  // namespace muon
