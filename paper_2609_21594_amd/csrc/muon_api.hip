@@ -440,6 +440,7 @@ MatDesc make_desc(const Item& it, double lr, double wd, int scale_mode) {
   d.transposed = it.rows > it.cols ? 1 : 0;
   const auto al16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
   d.vec_ok = ((it.rows * it.cols) % 8 == 0) && al16(it.g) && (!it.buf || al16(it.buf)) ? 1 : 0;
+  d.vec4_ok = (it.cols % 4 == 0) && al16(it.W ? it.W : it.out) ? 1 : 0;
   const double scale = scale_mode == 0 ? 0.2 * std::sqrt(double(std::max(it.rows, it.cols))) : 1.0;
   d.upd_scale = float(lr * scale);
   d.decay = float(1.0 - lr * wd);

@@ -29,7 +29,8 @@ struct MatDesc {
   int32_t vec_ok;       // 16-byte aligned pointers and rows*cols % 8 == 0
   float upd_scale;      // lr * RMS-matching scale
   float decay;          // 1 - lr * weight_decay
-  int32_t reserved0, reserved1;
+  int32_t vec4_ok;      // W (or out) 16-byte aligned and cols % 4 == 0
+  int32_t reserved1;
 };
 static_assert(sizeof(MatDesc) == 64, "MatDesc layout");
 

@@ -16,6 +16,8 @@
 // every step (padded rows/columns of X, A and B stay exactly zero).
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "muon_internal.h"
 
 namespace muon {
@@ -229,7 +231,9 @@ __global__ __launch_bounds__(256) void k_normalize(const MatDesc* __restrict__ d
 // Output layout of a 32x32 block: lane l, register r holds
 //   row 8*(r/4) + 4*(l/32) + (r%4), column l%32.
 // ---------------------------------------------------------------------------
-enum Epi : int { EPI_GRAM = 0, EPI_POLY = 1, EPI_UPDATE = 2, EPI_FINAL = 3 };
+enum Epi : int { EPI_GRAM = 0, EPI_POLY = 1, EPI_UPDATE = 2, EPI_FINAL = 3,
+                 // final-step variants of the 256-tile kernel: update W / write out, bf16 / fp32
+                 EPI_FINAL_W_BF16 = 4, EPI_FINAL_W_F32 = 5, EPI_FINAL_O_BF16 = 6, EPI_FINAL_O_F32 = 7 };
 
 struct GemmArgs {
   const char* P;   int64_t p_mat;  int32_t ldp;   // bytes
@@ -237,6 +241,7 @@ struct GemmArgs {
   int32_t k_slabs;                               // K * elem / 128
   int32_t tiles_m, tiles_n, syrk, tiles_per_mat;
   const char* E;   int64_t e_mat;  int32_t lde;   // epilogue input (A or X), bytes
+  const char* ET;  int64_t et_mat; int32_t ldet;  // the same values, transposed layout
   char* C;         int64_t c_mat;  int32_t ldc;   // output, direct orientation
   char* CT;        int64_t ct_mat; int32_t ldct;  // output, transposed orientation
   float alpha, beta;
@@ -426,6 +431,293 @@ __global__ __launch_bounds__(256, 2) void k_gemm_nt(GemmArgs ga) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 C = P Q^T with a 256 x 256 output tile per workgroup (M and N
+// multiples of 256).  512 threads = 8 wavefronts in a 2 x 4 grid, each owning
+// a 128 x 64 sub-tile = 4 x 2 blocks of v_mfma_f32_32x32x16_bf16, so every
+// operand fragment read from LDS feeds two or four MFMAs.
+//
+// K is staged 64 elements (128 bytes per row) at a time with direct
+// global-to-LDS loads (global_load_lds_dwordx4: lane i of a wavefront writes
+// bytes [16 i, 16 i + 16) after the wave-uniform LDS base), double-buffered.
+// A wavefront instruction fills 8 consecutive tile rows; lane i fetches the
+// 16-byte k-chunk (i % 8) ^ (row % 8) of its row, so LDS row r holds chunk c
+// at position c ^ (r % 8).  Fragment reads (32 rows, one chunk) then hit 8
+// distinct 16-byte positions per 8 lanes: no bank conflicts.
+//
+// Workgroup b runs on XCD b % 8; the tile order gives every XCD a contiguous
+// range of tiles, grouped 4 tile-rows high so concurrent tiles of one XCD
+// share operand panels in its L2.
+//
+// The epilogue works on the accumulator registers directly: lane l holds
+// rows 8*(r/4) + 4*(l/32) + (r%4) of column l%32 in register r of a block;
+// direct stores are 2 bytes per lane (32 lanes on consecutive columns), the
+// transposed orientation stores the 4 consecutive rows a lane holds as one
+// 8-byte vector.
+// ---------------------------------------------------------------------------
+// Lanes 4p..4p+3 each hold x[0..3] = M[t][0..3] (t = lane % 4); afterwards
+// lane t holds M[0..3][t].  Two butterfly stages over lane bits 0 and 1.
+__device__ __forceinline__ void quad_transpose(float x[4]) {
+  const int t = threadIdx.x & 3;
+  float y[4], n[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) y[k] = __shfl_xor(x[k], 1, 64);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) n[r] = ((r ^ t) & 1) ? y[r ^ 1] : x[r];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) y[k] = __shfl_xor(n[k], 2, 64);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) x[r] = ((r ^ t) & 2) ? y[r ^ 2] : n[r];
+}
+
+__device__ __forceinline__ uint2 pack_bf16x4(const float v[4]) {
+  uint2 p;
+  p.x = static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
+  p.y = static_cast<uint32_t>(f32_to_bf16(v[2])) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
+  return p;
+}
+
+// Ragged-edge tail of apply4 (kept out of line: it is rare, and keeping the
+// epilogue small lets the compiler hold every accumulator in registers).
+template <int FK, int PDT>
+__device__ __noinline__ void apply_tail(const MatDesc* md, int64_t idx, float o0, float o1, float o2,
+                                        float o3, int n) {
+  using PT = typename std::conditional<PDT == DT_BF16, uint16_t, float>::type;
+  PT* dst = static_cast<PT*>(FK == 0 ? md->W : md->out);
+  const float o[4] = {o0, o1, o2, o3};
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    if (q < n) {
+      const float r = FK == 0 ? fmaf(md->decay, to_f32<PT>(dst[idx + q]), -md->upd_scale * o[q]) : o[q];
+      dst[idx + q] = from_f32<PT>(r);
+    }
+  }
+}
+
+// W[idx .. idx+3] = decay*W - upd*o (FK = 0) or out[idx ..] = o (FK = 1), 4
+// consecutive elements of dtype PDT: one vector access when `vec`, else
+// element by element up to `n`.
+template <int FK, int PDT>
+__device__ __forceinline__ void apply4(const MatDesc* md, int64_t idx, const float o[4], bool vec,
+                                       int n) {
+  using PT = typename std::conditional<PDT == DT_BF16, uint16_t, float>::type;
+  PT* dst = static_cast<PT*>(FK == 0 ? md->W : md->out);
+  const float decay = md->decay, upd = md->upd_scale;
+  if (vec) {
+    float w[4] = {0.f, 0.f, 0.f, 0.f}, r[4];
+    if (PDT == DT_BF16) {
+      uint2* p = reinterpret_cast<uint2*>(dst + idx);
+      if (FK == 0) {
+        const uint2 raw = *p;
+        w[0] = __uint_as_float(raw.x << 16); w[1] = __uint_as_float(raw.x & 0xffff0000u);
+        w[2] = __uint_as_float(raw.y << 16); w[3] = __uint_as_float(raw.y & 0xffff0000u);
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) r[q] = FK == 0 ? fmaf(decay, w[q], -upd * o[q]) : o[q];
+      *p = pack_bf16x4(r);
+    } else {
+      float4* p = reinterpret_cast<float4*>(dst + idx);
+      if (FK == 0) {
+        const float4 raw = *p;
+        w[0] = raw.x; w[1] = raw.y; w[2] = raw.z; w[3] = raw.w;
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) r[q] = FK == 0 ? fmaf(decay, w[q], -upd * o[q]) : o[q];
+      *p = make_float4(r[0], r[1], r[2], r[3]);
+    }
+    return;
+  }
+  apply_tail<FK, PDT>(md, idx, o[0], o[1], o[2], o[3], n);
+}
+
+constexpr int kBig = 256;
+constexpr int kBigOp = kBig * 128;        // bytes of one operand slab
+constexpr int kBigStage = 2 * kBigOp;     // P and Q slabs
+#ifndef MUON_BIG_WAVES_M
+#define MUON_BIG_WAVES_M 2
+#define MUON_BIG_WAVES_N 4
+#endif
+constexpr int kBigWavesM = MUON_BIG_WAVES_M, kBigWavesN = MUON_BIG_WAVES_N;
+
+__device__ __forceinline__ void tile_coords(const GemmArgs& ga, int tile_dim, int& mat, int& bm,
+                                            int& bn) {
+  const int total = ga.tiles_per_mat * static_cast<int>(gridDim.x / ga.tiles_per_mat);
+  const int b = blockIdx.x;
+  const int per = total >> 3, rem = total & 7, x = b & 7, idx = b >> 3;
+  const int logical = x * per + min(x, rem) + idx;
+  mat = logical / ga.tiles_per_mat;
+  int t = logical - mat * ga.tiles_per_mat;
+  if (ga.syrk) {
+    bm = 0;
+    while (t >= ga.tiles_m - bm) { t -= ga.tiles_m - bm; ++bm; }
+    bn = bm + t;
+  } else {
+    constexpr int GM = 4;
+    const int band = t / (GM * ga.tiles_n);
+    const int within = t - band * GM * ga.tiles_n;
+    const int rows = min(GM, ga.tiles_m - band * GM);
+    bm = band * GM + within % rows;
+    bn = within / rows;
+  }
+  (void)tile_dim;
+}
+
+template <int EPI, int WM, int WN>
+__global__ __launch_bounds__(64 * WM * WN) void k_gemm256(GemmArgs ga) {
+  constexpr int NW = WM * WN;                 // wavefronts
+  constexpr int BI = kBig / WM / 32;          // 32x32 blocks per wave, rows
+  constexpr int BJ = kBig / WN / 32;          // and columns
+  constexpr int ROWS_PER_WAVE = kBig / NW;    // operand rows each wave loads
+  constexpr bool FINAL = EPI >= EPI_FINAL_W_BF16;
+  constexpr int FK = (EPI == EPI_FINAL_O_BF16 || EPI == EPI_FINAL_O_F32) ? 1 : 0;
+  constexpr int PDT = (EPI == EPI_FINAL_W_F32 || EPI == EPI_FINAL_O_F32) ? DT_F32 : DT_BF16;
+  __shared__ __attribute__((aligned(1024))) char smem[2 * kBigStage];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WN, wn = wave % WN;
+  int mat, bm, bn;
+  tile_coords(ga, kBig, mat, bm, bn);
+  const char* Pb = ga.P + mat * ga.p_mat + static_cast<int64_t>(bm) * kBig * ga.ldp;
+  const char* Qb = ga.Q + mat * ga.q_mat + static_cast<int64_t>(bn) * kBig * ga.ldq;
+
+  // This lane's share of the slab loads: rows wave*ROWS_PER_WAVE + 8*i + lane/8.
+  const int lrow = wave * ROWS_PER_WAVE + (lane >> 3);
+  const int lchunk = ((lane & 7) ^ (lrow & 7)) * 16;
+  const char* pa = Pb + static_cast<int64_t>(lrow) * ga.ldp + lchunk;
+  const char* qa = Qb + static_cast<int64_t>(lrow) * ga.ldq + lchunk;
+  const int64_t p8 = static_cast<int64_t>(8) * ga.ldp, q8 = static_cast<int64_t>(8) * ga.ldq;
+  auto issue = [&](int ks, int stage) {
+    char* base = smem + stage * kBigStage + wave * ROWS_PER_WAVE * 128;
+    const int64_t ko = static_cast<int64_t>(ks) * 128;
+#pragma unroll
+    for (int i = 0; i < ROWS_PER_WAVE / 8; ++i) {
+      __builtin_amdgcn_global_load_lds(
+          (const __attribute__((address_space(1))) void*)(pa + i * p8 + ko),
+          (__attribute__((address_space(3))) void*)(base + i * 1024), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(
+          (const __attribute__((address_space(1))) void*)(qa + i * q8 + ko),
+          (__attribute__((address_space(3))) void*)(base + kBigOp + i * 1024), 16, 0, 0);
+    }
+  };
+
+  f32x16_t acc[BI][BJ];
+#pragma unroll
+  for (int i = 0; i < BI; ++i)
+#pragma unroll
+    for (int j = 0; j < BJ; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  // fragment addressing: row (..+ lane%32), chunk (2*grp + lane/32) at position chunk ^ (lane%8)
+  const int frow = lane & 31, fsel = lane >> 5, fsw = lane & 7;
+  const int a_off = (wm * (kBig / WM) + frow) * 128;
+  const int b_off = kBigOp + (wn * (kBig / WN) + frow) * 128;
+
+  issue(0, 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  for (int ks = 0; ks < ga.k_slabs; ++ks) {
+    const int stage = ks & 1;
+    if (ks + 1 < ga.k_slabs) issue(ks + 1, stage ^ 1);
+    const char* sp = smem + stage * kBigStage;
+#pragma unroll
+    for (int grp = 0; grp < 4; ++grp) {
+      const int pos = ((2 * grp + fsel) ^ fsw) * 16;
+      u32x4_t a[BI], b[BJ];
+#pragma unroll
+      for (int i = 0; i < BI; ++i)
+        a[i] = *reinterpret_cast<const u32x4_t*>(sp + a_off + i * 32 * 128 + pos);
+#pragma unroll
+      for (int j = 0; j < BJ; ++j)
+        b[j] = *reinterpret_cast<const u32x4_t*>(sp + b_off + j * 32 * 128 + pos);
+#pragma unroll
+      for (int i = 0; i < BI; ++i)
+#pragma unroll
+        for (int j = 0; j < BJ; ++j) Mma<uint16_t>::run(a[i], b[j], acc[i][j]);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+  }
+
+  // ---- epilogue from registers ----------------------------------------------
+  // Lane l holds, per block and register group g, rows row0..row0+3 of one
+  // column.  The transposed orientation takes those 4 values as one 8-byte
+  // vector; a 4-lane transpose gives the direct orientation the same shape
+  // (lane t of a quad: row row0+t, columns c0..c0+3).
+  const bool diag = ga.syrk && bm == bn;
+  const MatDesc* md = FINAL ? ga.desc + mat : nullptr;
+  const bool tr = FINAL ? md->transposed != 0 : false;
+  const bool v4 = FINAL ? md->vec4_ok != 0 : false;
+  const int q4 = lane & 3;
+  const int row_base = bm * kBig + wm * (kBig / WM) + 4 * fsel;
+  const int col_base = bn * kBig + wn * (kBig / WN) + frow;
+  char* const C = ga.C + mat * ga.c_mat;
+  char* const CT = ga.CT + mat * ga.ct_mat;
+  const char* const ET = ga.ET + mat * ga.et_mat;
+#pragma unroll
+  for (int i = 0; i < BI; ++i)
+#pragma unroll
+    for (int j = 0; j < BJ; ++j)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int row0 = row_base + i * 32 + 8 * g;  // rows row0 .. row0 + 3
+        const int col = col_base + j * 32;
+        float v[4];
+        if (EPI == EPI_GRAM) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) v[q] = acc[i][j][4 * g + q];
+        } else {
+          // the a*X (or b*A) term: 4 consecutive rows of column `col`, read
+          // from the transposed copy (same bits) as one 8-byte vector
+          const uint2 raw = *reinterpret_cast<const uint2*>(ET + static_cast<int64_t>(col) * ga.ldet + row0 * 2);
+          const float e[4] = {__uint_as_float(raw.x << 16), __uint_as_float(raw.x & 0xffff0000u),
+                              __uint_as_float(raw.y << 16), __uint_as_float(raw.y & 0xffff0000u)};
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            v[q] = EPI == EPI_POLY ? fmaf(ga.alpha, e[q], ga.beta * acc[i][j][4 * g + q])
+                                   : fmaf(ga.alpha, e[q], acc[i][j][4 * g + q]);
+        }
+        if (EPI == EPI_GRAM || EPI == EPI_POLY || EPI == EPI_UPDATE) {
+          float o[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) o[q] = bf16_to_f32(f32_to_bf16(v[q]));
+          if (!diag) {
+            *reinterpret_cast<uint2*>(CT + static_cast<int64_t>(col) * ga.ldct + row0 * 2) = pack_bf16x4(o);
+            quad_transpose(o);
+            *reinterpret_cast<uint2*>(C + static_cast<int64_t>(row0 + q4) * ga.ldc + (col - q4) * 2) = pack_bf16x4(o);
+          } else {
+            // symmetric diagonal tile: the upper triangle (row <= col) is the
+            // value of both (row, col) and (col, row)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int row = row0 + q;
+              if (row <= col) {
+                const uint16_t h = f32_to_bf16(o[q]);
+                *reinterpret_cast<uint16_t*>(C + static_cast<int64_t>(row) * ga.ldc + col * 2) = h;
+                *reinterpret_cast<uint16_t*>(C + static_cast<int64_t>(col) * ga.ldc + row * 2) = h;
+              }
+            }
+          }
+        } else {  // final step: O = v (fp32) -> parameter update or output
+          if (tr) {  // parameter is l x s: elements (col, row0 .. row0 + 3)
+            if (col < ga.l) {
+              const int n = min(4, ga.s - row0);
+              if (n > 0)
+                apply4<FK, PDT>(md, static_cast<int64_t>(col) * md->cols + row0, v, v4 && n == 4, n);
+            }
+          } else {   // parameter is s x l: elements (row0 + q4, c0 .. c0 + 3)
+            quad_transpose(v);
+            const int row = row0 + q4, c0 = col - q4;
+            if (row < ga.s) {
+              const int n = min(4, ga.l - c0);
+              if (n > 0)
+                apply4<FK, PDT>(md, static_cast<int64_t>(row) * md->cols + c0, v, v4 && n == 4, n);
+            }
+          }
+        }
+      }
+}
+
 // Update from X0 when K = 0: O is X0 in the caller's layout (the direct
 // buffer), one thread per element of the u-domain; grid = (ceil(rows*cols /
 // 256), matrices).
@@ -454,8 +746,35 @@ __global__ __launch_bounds__(256) void k_apply_x0(const MatDesc* __restrict__ de
 // ---------------------------------------------------------------------------
 // Host-side launch sequence for one chunk.
 // ---------------------------------------------------------------------------
+// 256-wide tiles for bf16 products whose extents allow them, else 128.
+template <typename T>
+bool use_big(const GemmArgs& ga128) {
+  return sizeof(T) == 2 && (ga128.tiles_m % 2 == 0) && (ga128.tiles_n % 2 == 0);
+}
+
 template <typename T>
 hipError_t launch_gemm(int epi, GemmArgs ga, int nmat, hipStream_t st) {
+  if (use_big<T>(ga)) {
+    ga.tiles_m /= 2;
+    ga.tiles_n /= 2;
+    ga.tiles_per_mat = ga.syrk ? ga.tiles_m * (ga.tiles_m + 1) / 2 : ga.tiles_m * ga.tiles_n;
+    constexpr int WM = kBigWavesM, WN = kBigWavesN;
+    const dim3 grid(static_cast<unsigned>(ga.tiles_per_mat) * nmat), block(64 * WM * WN);
+    switch (epi) {
+      case EPI_GRAM: hipLaunchKernelGGL((k_gemm256<EPI_GRAM, WM, WN>), grid, block, 0, st, ga); break;
+      case EPI_POLY: hipLaunchKernelGGL((k_gemm256<EPI_POLY, WM, WN>), grid, block, 0, st, ga); break;
+      case EPI_UPDATE: hipLaunchKernelGGL((k_gemm256<EPI_UPDATE, WM, WN>), grid, block, 0, st, ga); break;
+      default: {
+        const bool o = ga.final_kind != 0, f32 = ga.param_dtype == DT_F32;
+        if (!o && !f32) hipLaunchKernelGGL((k_gemm256<EPI_FINAL_W_BF16, WM, WN>), grid, block, 0, st, ga);
+        else if (!o) hipLaunchKernelGGL((k_gemm256<EPI_FINAL_W_F32, WM, WN>), grid, block, 0, st, ga);
+        else if (!f32) hipLaunchKernelGGL((k_gemm256<EPI_FINAL_O_BF16, WM, WN>), grid, block, 0, st, ga);
+        else hipLaunchKernelGGL((k_gemm256<EPI_FINAL_O_F32, WM, WN>), grid, block, 0, st, ga);
+        break;
+      }
+    }
+    return hipGetLastError();
+  }
   const dim3 grid(static_cast<unsigned>(ga.tiles_per_mat) * nmat), block(256);
   switch (epi) {
     case EPI_GRAM: hipLaunchKernelGGL((k_gemm_nt<T, EPI_GRAM>), grid, block, 0, st, ga); break;
@@ -561,6 +880,7 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
     p.Q = p.P; p.q_mat = matA; p.ldq = p.ldp;
     p.k_slabs = cg.S * es / 128;
     p.E = p.P; p.e_mat = matA; p.lde = p.ldp;
+    p.ET = p.P; p.et_mat = matA; p.ldet = p.ldp;  // A is symmetric
     p.C = static_cast<char*>(wb.B); p.CT = p.C;
     p.alpha = b; p.beta = c;
     {
@@ -575,6 +895,7 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
     u.k_slabs = cg.S * es / 128;
     u.tiles_m = ts; u.tiles_n = tl; u.syrk = 0; u.tiles_per_mat = ts * tl;
     u.E = X; u.e_mat = matX; u.lde = cg.L * es;
+    u.ET = XTc; u.et_mat = matX; u.ldet = cg.S * es;
     u.alpha = a;
     u.s = cg.s; u.l = cg.l;
     const double uf = nm * 2 * s * s * l;
