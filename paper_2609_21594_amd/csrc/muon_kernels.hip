@@ -17,6 +17,7 @@
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
+#include <utility>
 
 #include "muon_internal.h"
 
@@ -455,6 +456,17 @@ __global__ __launch_bounds__(256, 2) void k_gemm_nt(GemmArgs ga) {
 // transposed orientation stores the 4 consecutive rows a lane holds as one
 // 8-byte vector.
 // ---------------------------------------------------------------------------
+// Compile-time loop: f(std::integral_constant<int, 0>) ... f(<N-1>), so array
+// indices inside f are constants whatever the unroller decides.
+template <typename F, int... Is>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
+  (f(std::integral_constant<int, Is>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
 // Lanes 4p..4p+3 each hold x[0..3] = M[t][0..3] (t = lane % 4); afterwards
 // lane t holds M[0..3][t].  Two butterfly stages over lane bits 0 and 1.
 __device__ __forceinline__ void quad_transpose(float x[4]) {
@@ -530,74 +542,132 @@ __device__ __forceinline__ void apply4(const MatDesc* md, int64_t idx, const flo
   apply_tail<FK, PDT>(md, idx, o[0], o[1], o[2], o[3], n);
 }
 
-constexpr int kBig = 256;
-constexpr int kBigOp = kBig * 128;        // bytes of one operand slab
-constexpr int kBigStage = 2 * kBigOp;     // P and Q slabs
-#ifndef MUON_BIG_WAVES_M
-#define MUON_BIG_WAVES_M 2
-#define MUON_BIG_WAVES_N 4
-#endif
-constexpr int kBigWavesM = MUON_BIG_WAVES_M, kBigWavesN = MUON_BIG_WAVES_N;
+// Tile configuration of the direct-to-LDS MFMA kernel: output tile BM x BN,
+// a WM x WN grid of wavefronts (each BM/WM x BN/WN), SLAB bytes of every
+// tile row staged per LDS stage, NS stages, WPE wavefronts per SIMD.
+template <int BM_, int BN_, int WM_, int WN_, int SLAB_, int NS_, int WPE_>
+struct TileCfg {
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, SLAB = SLAB_, NS = NS_, WPE = WPE_;
+  static constexpr int NW = WM * WN;
+  static constexpr int LDS = NS * (BM + BN) * SLAB;
+  static_assert(LDS <= 160 * 1024, "LDS budget");
+};
+// 256 x 256, 8 wavefronts, one workgroup per CU (symmetric products).
+using CfgSquare = TileCfg<256, 256, 2, 4, 128, 2, 2>;
+// 256 x 128, 4 wavefronts, two workgroups per CU.
+using CfgRect = TileCfg<256, 128, 2, 2, 64, 2, 2>;
 
-__device__ __forceinline__ void tile_coords(const GemmArgs& ga, int tile_dim, int& mat, int& bm,
-                                            int& bn) {
-  const int total = ga.tiles_per_mat * static_cast<int>(gridDim.x / ga.tiles_per_mat);
+__device__ __forceinline__ void tile_coords(const GemmArgs& ga, int& mat, int& bm, int& bn) {
+  const int total = static_cast<int>(gridDim.x);
   const int b = blockIdx.x;
   const int per = total >> 3, rem = total & 7, x = b & 7, idx = b >> 3;
   const int logical = x * per + min(x, rem) + idx;
   mat = logical / ga.tiles_per_mat;
   int t = logical - mat * ga.tiles_per_mat;
   if (ga.syrk) {
-    bm = 0;
-    while (t >= ga.tiles_m - bm) { t -= ga.tiles_m - bm; ++bm; }
-    bn = bm + t;
+    // upper-triangle tiles (bm <= bn) in bands of GS tile-rows, column by
+    // column inside a band, so concurrent tiles share row and column panels
+#ifndef MUON_GS
+#define MUON_GS 8
+#endif
+    constexpr int GS = MUON_GS;
+    const int T = ga.tiles_m;
+    int b0 = 0;
+    for (;;) {
+      const int rows = min(GS, T - b0);
+      const int size = rows * (rows + 1) / 2 + (T - b0 - rows) * rows;
+      if (t < size) break;
+      t -= size;
+      b0 += GS;
+    }
+    const int rows = min(GS, T - b0);
+    int c = 0;
+    while (t >= min(rows, c + 1)) { t -= min(rows, c + 1); ++c; }
+    bn = b0 + c;
+    bm = b0 + t;
   } else {
-    constexpr int GM = 4;
+#ifndef MUON_GM
+#define MUON_GM 8
+#endif
+    constexpr int GM = MUON_GM;
     const int band = t / (GM * ga.tiles_n);
     const int within = t - band * GM * ga.tiles_n;
     const int rows = min(GM, ga.tiles_m - band * GM);
     bm = band * GM + within % rows;
     bn = within / rows;
   }
-  (void)tile_dim;
 }
 
-template <int EPI, int WM, int WN>
-__global__ __launch_bounds__(64 * WM * WN) void k_gemm256(GemmArgs ga) {
-  constexpr int NW = WM * WN;                 // wavefronts
-  constexpr int BI = kBig / WM / 32;          // 32x32 blocks per wave, rows
-  constexpr int BJ = kBig / WN / 32;          // and columns
-  constexpr int ROWS_PER_WAVE = kBig / NW;    // operand rows each wave loads
+// Waits until at most `n` slabs of this wave's direct-to-LDS loads are still
+// in flight (LPS load instructions per slab).
+template <int LPS>
+__device__ __forceinline__ void wait_slabs_in_flight(int n) {
+  if (n >= 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * LPS) : "memory");
+  else if (n == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPS) : "memory");
+  else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+template <int EPI, class Cfg>
+__global__ __launch_bounds__(64 * Cfg::NW) __attribute__((amdgpu_waves_per_eu(Cfg::WPE, Cfg::WPE)))
+void k_gemm_tile(GemmArgs ga) {
+  constexpr int BM = Cfg::BM, BN = Cfg::BN, WM = Cfg::WM, WN = Cfg::WN, NW = Cfg::NW;
+  constexpr int SLAB = Cfg::SLAB, NS = Cfg::NS;
+  constexpr int BI = BM / WM / 32;            // 32x32 blocks per wave, rows
+  constexpr int BJ = BN / WN / 32;            // and columns
+  constexpr int CPR = SLAB / 16;              // 16-byte chunks per staged row
+  constexpr int SH = CPR == 8 ? 1 : 2;        // swizzle key: (row >> SH) & (CPR - 1)
+  constexpr int RPI = 1024 / SLAB;            // rows one wave load instruction fills
+  constexpr int PR = BM / NW, QR = BN / NW;   // operand rows each wave loads
+  constexpr int NLP = PR / RPI, NLQ = QR / RPI;
+  static_assert(NLP * RPI == PR && NLQ * RPI == QR, "load split");
+  constexpr int LPS = NLP + NLQ;              // load instructions per wave and slab
+  constexpr int GPS = SLAB / 32;              // 16-k MFMA groups per slab
+  constexpr int D = NS - 1;                   // prefetch distance in slabs
+  static_assert(D >= 1 && D <= 3, "wait_slabs_in_flight handles up to 2 slabs in flight");
+  constexpr int OPQ = BM * SLAB;              // Q slab offset in a stage
+  constexpr int STAGE = (BM + BN) * SLAB;
   constexpr bool FINAL = EPI >= EPI_FINAL_W_BF16;
   constexpr int FK = (EPI == EPI_FINAL_O_BF16 || EPI == EPI_FINAL_O_F32) ? 1 : 0;
   constexpr int PDT = (EPI == EPI_FINAL_W_F32 || EPI == EPI_FINAL_O_F32) ? DT_F32 : DT_BF16;
-  __shared__ __attribute__((aligned(1024))) char smem[2 * kBigStage];
+  __shared__ __attribute__((aligned(1024))) char smem[Cfg::LDS];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
   int mat, bm, bn;
-  tile_coords(ga, kBig, mat, bm, bn);
-  const char* Pb = ga.P + mat * ga.p_mat + static_cast<int64_t>(bm) * kBig * ga.ldp;
-  const char* Qb = ga.Q + mat * ga.q_mat + static_cast<int64_t>(bn) * kBig * ga.ldq;
+  tile_coords(ga, mat, bm, bn);
+  const char* Pb = ga.P + mat * ga.p_mat + static_cast<int64_t>(bm) * BM * ga.ldp;
+  const char* Qb = ga.Q + mat * ga.q_mat + static_cast<int64_t>(bn) * BN * ga.ldq;
 
-  // This lane's share of the slab loads: rows wave*ROWS_PER_WAVE + 8*i + lane/8.
-  const int lrow = wave * ROWS_PER_WAVE + (lane >> 3);
-  const int lchunk = ((lane & 7) ^ (lrow & 7)) * 16;
-  const char* pa = Pb + static_cast<int64_t>(lrow) * ga.ldp + lchunk;
-  const char* qa = Qb + static_cast<int64_t>(lrow) * ga.ldq + lchunk;
-  const int64_t p8 = static_cast<int64_t>(8) * ga.ldp, q8 = static_cast<int64_t>(8) * ga.ldq;
-  auto issue = [&](int ks, int stage) {
-    char* base = smem + stage * kBigStage + wave * ROWS_PER_WAVE * 128;
-    const int64_t ko = static_cast<int64_t>(ks) * 128;
+  // Direct global -> LDS loads.  A wave instruction fills RPI consecutive
+  // tile rows (1 KB); lane l writes row r0 + l / CPR at position l % CPR and
+  // therefore fetches k-chunk (l % CPR) ^ key(row): LDS row r holds chunk c at
+  // position c ^ key(r), key(r) = (r >> SH) & (CPR - 1), which spreads the 32
+  // rows of a fragment read over all banks.
+  const char* pa[NLP];
+  const char* qa[NLQ];
 #pragma unroll
-    for (int i = 0; i < ROWS_PER_WAVE / 8; ++i) {
+  for (int i = 0; i < NLP; ++i) {
+    const int r = wave * PR + RPI * i + lane / CPR;
+    pa[i] = Pb + static_cast<int64_t>(r) * ga.ldp + ((lane % CPR) ^ ((r >> SH) & (CPR - 1))) * 16;
+  }
+#pragma unroll
+  for (int i = 0; i < NLQ; ++i) {
+    const int r = wave * QR + RPI * i + lane / CPR;
+    qa[i] = Qb + static_cast<int64_t>(r) * ga.ldq + ((lane % CPR) ^ ((r >> SH) & (CPR - 1))) * 16;
+  }
+  auto issue = [&](int ks) {
+    char* base = smem + (ks % NS) * STAGE;
+    const int64_t ko = static_cast<int64_t>(ks) * SLAB;
+#pragma unroll
+    for (int i = 0; i < NLP; ++i)
       __builtin_amdgcn_global_load_lds(
-          (const __attribute__((address_space(1))) void*)(pa + i * p8 + ko),
-          (__attribute__((address_space(3))) void*)(base + i * 1024), 16, 0, 0);
+          (const __attribute__((address_space(1))) void*)(pa[i] + ko),
+          (__attribute__((address_space(3))) void*)(base + (wave * PR + RPI * i) * SLAB), 16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < NLQ; ++i)
       __builtin_amdgcn_global_load_lds(
-          (const __attribute__((address_space(1))) void*)(qa + i * q8 + ko),
-          (__attribute__((address_space(3))) void*)(base + kBigOp + i * 1024), 16, 0, 0);
-    }
+          (const __attribute__((address_space(1))) void*)(qa[i] + ko),
+          (__attribute__((address_space(3))) void*)(base + OPQ + (wave * QR + RPI * i) * SLAB), 16, 0, 0);
   };
 
   f32x16_t acc[BI][BJ];
@@ -608,34 +678,42 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm256(GemmArgs ga) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // fragment addressing: row (..+ lane%32), chunk (2*grp + lane/32) at position chunk ^ (lane%8)
-  const int frow = lane & 31, fsel = lane >> 5, fsw = lane & 7;
-  const int a_off = (wm * (kBig / WM) + frow) * 128;
-  const int b_off = kBigOp + (wn * (kBig / WN) + frow) * 128;
+  // fragment addressing: row (..+ lane%32), chunk (2*grp + lane/32) at position chunk ^ key(row)
+  const int frow = lane & 31, fsel = lane >> 5, fsw = (frow >> SH) & (CPR - 1);
+  const int a_off = (wm * (BM / WM) + frow) * SLAB;
+  const int b_off = OPQ + (wn * (BN / WN) + frow) * SLAB;
 
-  issue(0, 0);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  for (int ks = 0; ks < ga.k_slabs; ++ks) {
-    const int stage = ks & 1;
-    if (ks + 1 < ga.k_slabs) issue(ks + 1, stage ^ 1);
-    const char* sp = smem + stage * kBigStage;
+  const int nk = ga.k_slabs;
 #pragma unroll
-    for (int grp = 0; grp < 4; ++grp) {
+  for (int s = 0; s < D; ++s)
+    if (s < nk) issue(s);
+  if constexpr (D == 1)
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  else
+    wait_slabs_in_flight<LPS>(min(D, nk) - 1);
+  __syncthreads();
+  for (int ks = 0; ks < nk; ++ks) {
+    if (ks + D < nk) issue(ks + D);
+    const char* sp = smem + (ks % NS) * STAGE;
+#pragma unroll
+    for (int grp = 0; grp < GPS; ++grp) {
       const int pos = ((2 * grp + fsel) ^ fsw) * 16;
       u32x4_t a[BI], b[BJ];
 #pragma unroll
       for (int i = 0; i < BI; ++i)
-        a[i] = *reinterpret_cast<const u32x4_t*>(sp + a_off + i * 32 * 128 + pos);
+        a[i] = *reinterpret_cast<const u32x4_t*>(sp + a_off + i * 32 * SLAB + pos);
 #pragma unroll
       for (int j = 0; j < BJ; ++j)
-        b[j] = *reinterpret_cast<const u32x4_t*>(sp + b_off + j * 32 * 128 + pos);
-#pragma unroll
-      for (int i = 0; i < BI; ++i)
-#pragma unroll
-        for (int j = 0; j < BJ; ++j) Mma<uint16_t>::run(a[i], b[j], acc[i][j]);
+        b[j] = *reinterpret_cast<const u32x4_t*>(sp + b_off + j * 32 * SLAB + pos);
+      static_for<BI>([&](auto I) {
+        static_for<BJ>([&](auto J) { Mma<uint16_t>::run(a[I.value], b[J.value], acc[I.value][J.value]); });
+      });
     }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // slab ks+1 must have landed; later slabs may still be in flight
+    if constexpr (D == 1)
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    else
+      wait_slabs_in_flight<LPS>(min(nk - 1, ks + D) - (ks + 1));
     __syncthreads();
   }
 
@@ -649,17 +727,15 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm256(GemmArgs ga) {
   const bool tr = FINAL ? md->transposed != 0 : false;
   const bool v4 = FINAL ? md->vec4_ok != 0 : false;
   const int q4 = lane & 3;
-  const int row_base = bm * kBig + wm * (kBig / WM) + 4 * fsel;
-  const int col_base = bn * kBig + wn * (kBig / WN) + frow;
+  const int row_base = bm * BM + wm * (BM / WM) + 4 * fsel;
+  const int col_base = bn * BN + wn * (BN / WN) + frow;
   char* const C = ga.C + mat * ga.c_mat;
   char* const CT = ga.CT + mat * ga.ct_mat;
   const char* const ET = ga.ET + mat * ga.et_mat;
-#pragma unroll
-  for (int i = 0; i < BI; ++i)
-#pragma unroll
-    for (int j = 0; j < BJ; ++j)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
+  static_for<BI>([&](auto I) {
+  static_for<BJ>([&](auto J) {
+  static_for<4>([&](auto G) {
+        constexpr int i = decltype(I)::value, j = decltype(J)::value, g = decltype(G)::value;
         const int row0 = row_base + i * 32 + 8 * g;  // rows row0 .. row0 + 3
         const int col = col_base + j * 32;
         float v[4];
@@ -715,7 +791,9 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm256(GemmArgs ga) {
             }
           }
         }
-      }
+  });
+  });
+  });
 }
 
 // Update from X0 when K = 0: O is X0 in the caller's layout (the direct
@@ -746,34 +824,42 @@ __global__ __launch_bounds__(256) void k_apply_x0(const MatDesc* __restrict__ de
 // ---------------------------------------------------------------------------
 // Host-side launch sequence for one chunk.
 // ---------------------------------------------------------------------------
-// 256-wide tiles for bf16 products whose extents allow them, else 128.
-template <typename T>
-bool use_big(const GemmArgs& ga128) {
-  return sizeof(T) == 2 && (ga128.tiles_m % 2 == 0) && (ga128.tiles_n % 2 == 0);
+#ifndef MUON_UPDATE_RECT
+#define MUON_UPDATE_RECT 0
+#endif
+
+template <class Cfg>
+hipError_t launch_tile(int epi, GemmArgs ga, int nmat, hipStream_t st) {
+  // ga arrives in 128 x 128 tiles and 128-byte slabs
+  ga.tiles_m = ga.tiles_m * kTile / Cfg::BM;
+  ga.tiles_n = ga.tiles_n * kTile / Cfg::BN;
+  ga.tiles_per_mat = ga.syrk ? ga.tiles_m * (ga.tiles_m + 1) / 2 : ga.tiles_m * ga.tiles_n;
+  ga.k_slabs = ga.k_slabs * 128 / Cfg::SLAB;
+  const dim3 grid(static_cast<unsigned>(ga.tiles_per_mat) * nmat), block(64 * Cfg::NW);
+  switch (epi) {
+    case EPI_GRAM: hipLaunchKernelGGL((k_gemm_tile<EPI_GRAM, Cfg>), grid, block, 0, st, ga); break;
+    case EPI_POLY: hipLaunchKernelGGL((k_gemm_tile<EPI_POLY, Cfg>), grid, block, 0, st, ga); break;
+    case EPI_UPDATE: hipLaunchKernelGGL((k_gemm_tile<EPI_UPDATE, Cfg>), grid, block, 0, st, ga); break;
+    default: {
+      const bool o = ga.final_kind != 0, f32 = ga.param_dtype == DT_F32;
+      if (!o && !f32) hipLaunchKernelGGL((k_gemm_tile<EPI_FINAL_W_BF16, Cfg>), grid, block, 0, st, ga);
+      else if (!o) hipLaunchKernelGGL((k_gemm_tile<EPI_FINAL_W_F32, Cfg>), grid, block, 0, st, ga);
+      else if (!f32) hipLaunchKernelGGL((k_gemm_tile<EPI_FINAL_O_BF16, Cfg>), grid, block, 0, st, ga);
+      else hipLaunchKernelGGL((k_gemm_tile<EPI_FINAL_O_F32, Cfg>), grid, block, 0, st, ga);
+      break;
+    }
+  }
+  return hipGetLastError();
 }
 
 template <typename T>
 hipError_t launch_gemm(int epi, GemmArgs ga, int nmat, hipStream_t st) {
-  if (use_big<T>(ga)) {
-    ga.tiles_m /= 2;
-    ga.tiles_n /= 2;
-    ga.tiles_per_mat = ga.syrk ? ga.tiles_m * (ga.tiles_m + 1) / 2 : ga.tiles_m * ga.tiles_n;
-    constexpr int WM = kBigWavesM, WN = kBigWavesN;
-    const dim3 grid(static_cast<unsigned>(ga.tiles_per_mat) * nmat), block(64 * WM * WN);
-    switch (epi) {
-      case EPI_GRAM: hipLaunchKernelGGL((k_gemm256<EPI_GRAM, WM, WN>), grid, block, 0, st, ga); break;
-      case EPI_POLY: hipLaunchKernelGGL((k_gemm256<EPI_POLY, WM, WN>), grid, block, 0, st, ga); break;
-      case EPI_UPDATE: hipLaunchKernelGGL((k_gemm256<EPI_UPDATE, WM, WN>), grid, block, 0, st, ga); break;
-      default: {
-        const bool o = ga.final_kind != 0, f32 = ga.param_dtype == DT_F32;
-        if (!o && !f32) hipLaunchKernelGGL((k_gemm256<EPI_FINAL_W_BF16, WM, WN>), grid, block, 0, st, ga);
-        else if (!o) hipLaunchKernelGGL((k_gemm256<EPI_FINAL_W_F32, WM, WN>), grid, block, 0, st, ga);
-        else if (!f32) hipLaunchKernelGGL((k_gemm256<EPI_FINAL_O_BF16, WM, WN>), grid, block, 0, st, ga);
-        else hipLaunchKernelGGL((k_gemm256<EPI_FINAL_O_F32, WM, WN>), grid, block, 0, st, ga);
-        break;
-      }
-    }
-    return hipGetLastError();
+  // bf16 products on the direct-to-LDS kernels when the padded extents allow
+  // their tiles (multiples of 256 rows); else the 128 x 128 kernel.
+  if (sizeof(T) == 2 && ga.tiles_m % 2 == 0) {
+    if (ga.syrk) return launch_tile<CfgSquare>(epi, ga, nmat, st);
+    if (MUON_UPDATE_RECT) return launch_tile<CfgRect>(epi, ga, nmat, st);
+    if (ga.tiles_n % 2 == 0) return launch_tile<CfgSquare>(epi, ga, nmat, st);
   }
   const dim3 grid(static_cast<unsigned>(ga.tiles_per_mat) * nmat), block(256);
   switch (epi) {
