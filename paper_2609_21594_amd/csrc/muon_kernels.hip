@@ -249,6 +249,7 @@ struct GemmArgs {
   const MatDesc* desc;
   int32_t final_kind, param_dtype;
   int32_t s, l;
+  int32_t total_tiles;                           // tiles_per_mat * matrices
 };
 
 constexpr int kRowBytes = 144;                   // 128 data + 16 pad per LDS row
@@ -557,11 +558,10 @@ using CfgSquare = TileCfg<256, 256, 2, 4, 128, 2, 2>;
 // 256 x 128, 4 wavefronts, two workgroups per CU.
 using CfgRect = TileCfg<256, 128, 2, 2, 64, 2, 2>;
 
-__device__ __forceinline__ void tile_coords(const GemmArgs& ga, int& mat, int& bm, int& bn) {
-  const int total = static_cast<int>(gridDim.x);
-  const int b = blockIdx.x;
-  const int per = total >> 3, rem = total & 7, x = b & 7, idx = b >> 3;
-  const int logical = x * per + min(x, rem) + idx;
+// Tile `logical` of the launch: matrix-major; inside a matrix, banded
+// (GS / GM tile-rows per band, column by column inside a band).
+__device__ __forceinline__ void tile_from_logical(const GemmArgs& ga, int logical, int& mat, int& bm,
+                                                  int& bn) {
   mat = logical / ga.tiles_per_mat;
   int t = logical - mat * ga.tiles_per_mat;
   if (ga.syrk) {
@@ -608,8 +608,7 @@ __device__ __forceinline__ void wait_slabs_in_flight(int n) {
 }
 
 template <int EPI, class Cfg>
-__global__ __launch_bounds__(64 * Cfg::NW) __attribute__((amdgpu_waves_per_eu(Cfg::WPE, Cfg::WPE)))
-void k_gemm_tile(GemmArgs ga) {
+__device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, int mat, int bm, int bn) {
   constexpr int BM = Cfg::BM, BN = Cfg::BN, WM = Cfg::WM, WN = Cfg::WN, NW = Cfg::NW;
   constexpr int SLAB = Cfg::SLAB, NS = Cfg::NS;
   constexpr int BI = BM / WM / 32;            // 32x32 blocks per wave, rows
@@ -629,12 +628,9 @@ void k_gemm_tile(GemmArgs ga) {
   constexpr bool FINAL = EPI >= EPI_FINAL_W_BF16;
   constexpr int FK = (EPI == EPI_FINAL_O_BF16 || EPI == EPI_FINAL_O_F32) ? 1 : 0;
   constexpr int PDT = (EPI == EPI_FINAL_W_F32 || EPI == EPI_FINAL_O_F32) ? DT_F32 : DT_BF16;
-  __shared__ __attribute__((aligned(1024))) char smem[Cfg::LDS];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
-  int mat, bm, bn;
-  tile_coords(ga, mat, bm, bn);
   const char* Pb = ga.P + mat * ga.p_mat + static_cast<int64_t>(bm) * BM * ga.ldp;
   const char* Qb = ga.Q + mat * ga.q_mat + static_cast<int64_t>(bn) * BN * ga.ldq;
 
@@ -796,6 +792,25 @@ void k_gemm_tile(GemmArgs ga) {
   });
 }
 
+// Persistent launch: one workgroup per CU slot loops over tiles in rounds.
+// Workgroup b runs on XCD b % 8; in round r the XCD's workgroups take the
+// contiguous logical range r*G + (b % 8)*(G/8) + [0, G/8), i.e. a compact
+// block of the banded order, and start it together, so the tiles of a block
+// stay in step and share each operand slab through the XCD's L2.
+template <int EPI, class Cfg>
+__global__ __launch_bounds__(64 * Cfg::NW) __attribute__((amdgpu_waves_per_eu(Cfg::WPE, Cfg::WPE)))
+void k_gemm_tile(GemmArgs ga) {
+  __shared__ __attribute__((aligned(1024))) char smem[Cfg::LDS];
+  const int G = static_cast<int>(gridDim.x), b = static_cast<int>(blockIdx.x);
+  for (int r = 0;; ++r) {
+    const int logical = (G % 8 == 0) ? r * G + (b & 7) * (G / 8) + (b >> 3) : r * G + b;
+    if (logical >= ga.total_tiles) break;
+    int mat, bm, bn;
+    tile_from_logical(ga, logical, mat, bm, bn);
+    gemm_tile_body<EPI, Cfg>(ga, smem, mat, bm, bn);
+  }
+}
+
 // Update from X0 when K = 0: O is X0 in the caller's layout (the direct
 // buffer), one thread per element of the u-domain; grid = (ceil(rows*cols /
 // 256), matrices).
@@ -827,6 +842,22 @@ __global__ __launch_bounds__(256) void k_apply_x0(const MatDesc* __restrict__ de
 #ifndef MUON_UPDATE_RECT
 #define MUON_UPDATE_RECT 0
 #endif
+#ifndef MUON_PERSISTENT
+#define MUON_PERSISTENT 1
+#endif
+
+// Compute units of the current device (queried once per device).
+int device_cu_count() {
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
 
 template <class Cfg>
 hipError_t launch_tile(int epi, GemmArgs ga, int nmat, hipStream_t st) {
@@ -835,7 +866,11 @@ hipError_t launch_tile(int epi, GemmArgs ga, int nmat, hipStream_t st) {
   ga.tiles_n = ga.tiles_n * kTile / Cfg::BN;
   ga.tiles_per_mat = ga.syrk ? ga.tiles_m * (ga.tiles_m + 1) / 2 : ga.tiles_m * ga.tiles_n;
   ga.k_slabs = ga.k_slabs * 128 / Cfg::SLAB;
-  const dim3 grid(static_cast<unsigned>(ga.tiles_per_mat) * nmat), block(64 * Cfg::NW);
+  ga.total_tiles = ga.tiles_per_mat * nmat;
+  // one workgroup per CU slot (persistent), never more workgroups than tiles
+  const int slots = device_cu_count() * (160 * 1024 / Cfg::LDS);
+  const int g = MUON_PERSISTENT ? min(ga.total_tiles, slots) : ga.total_tiles;
+  const dim3 grid(static_cast<unsigned>(g)), block(64 * Cfg::NW);
   switch (epi) {
     case EPI_GRAM: hipLaunchKernelGGL((k_gemm_tile<EPI_GRAM, Cfg>), grid, block, 0, st, ga); break;
     case EPI_POLY: hipLaunchKernelGGL((k_gemm_tile<EPI_POLY, Cfg>), grid, block, 0, st, ga); break;
