@@ -554,7 +554,11 @@ struct TileCfg {
   static_assert(LDS <= 160 * 1024, "LDS budget");
 };
 // 256 x 256, 8 wavefronts, one workgroup per CU (symmetric products).
-using CfgSquare = TileCfg<256, 256, 2, 4, 128, 2, 2>;
+#ifndef MUON_SQ_SLAB
+#define MUON_SQ_SLAB 128
+#define MUON_SQ_STAGES 2
+#endif
+using CfgSquare = TileCfg<256, 256, 2, 4, MUON_SQ_SLAB, MUON_SQ_STAGES, 2>;
 // 256 x 128, 4 wavefronts, two workgroups per CU.
 using CfgRect = TileCfg<256, 128, 2, 2, 64, 2, 2>;
 
@@ -688,6 +692,53 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   else
     wait_slabs_in_flight<LPS>(min(D, nk) - 1);
   __syncthreads();
+#ifndef MUON_SCHED
+#define MUON_SCHED 1
+#endif
+  if constexpr (MUON_SCHED && D == 1 && GPS == 4) {
+    // Software pipeline with explicit interleaving: the fragments of group
+    // g+1 are read into the other register set while group g's MFMAs issue,
+    // one LDS read between consecutive MFMAs; the slab barrier sits before
+    // the last group's MFMAs.
+    u32x4_t fa[2][BI], fb[2][BJ];
+    auto rd = [&](const char* sp, int grp, int set) {
+      const int pos = ((2 * grp + fsel) ^ fsw) * 16;
+#pragma unroll
+      for (int i = 0; i < BI; ++i) fa[set][i] = *reinterpret_cast<const u32x4_t*>(sp + a_off + i * 32 * SLAB + pos);
+#pragma unroll
+      for (int j = 0; j < BJ; ++j) fb[set][j] = *reinterpret_cast<const u32x4_t*>(sp + b_off + j * 32 * SLAB + pos);
+    };
+    auto mm = [&](int set) {
+      static_for<BI>([&](auto I) {
+        static_for<BJ>([&](auto J) { Mma<uint16_t>::run(fa[set][I.value], fb[set][J.value], acc[I.value][J.value]); });
+      });
+    };
+    auto interleave = [&]() {
+#pragma unroll
+      for (int i = 0; i < BI + BJ; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, BI * BJ - (BI + BJ), 0);
+    };
+    rd(smem, 0, 0);
+    for (int ks = 0; ks < nk; ++ks) {
+      const char* sp = smem + (ks & 1) * STAGE;
+      if (ks + 1 < nk) issue(ks + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      rd(sp, 1, 1); mm(0); interleave();
+      __builtin_amdgcn_sched_barrier(0);
+      rd(sp, 2, 0); mm(1); interleave();
+      __builtin_amdgcn_sched_barrier(0);
+      rd(sp, 3, 1); mm(0); interleave();
+      __builtin_amdgcn_sched_barrier(0);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+      rd(smem + ((ks + 1) & 1) * STAGE, 0, 0);  // next slab (unused after the last)
+      mm(1); interleave();
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else
   for (int ks = 0; ks < nk; ++ks) {
     if (ks + D < nk) issue(ks + D);
     const char* sp = smem + (ks % NS) * STAGE;
