@@ -721,10 +721,16 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
       }
       __builtin_amdgcn_sched_group_barrier(0x008, BI * BJ - (BI + BJ), 0);
     };
+#ifndef MUON_PRIO
+#define MUON_PRIO 0
+#endif
+    if (MUON_PRIO == 2 && (wave & 4)) __builtin_amdgcn_s_setprio(1);
     rd(smem, 0, 0);
     for (int ks = 0; ks < nk; ++ks) {
       const char* sp = smem + (ks & 1) * STAGE;
+      if (MUON_PRIO == 1) __builtin_amdgcn_s_setprio(0);
       if (ks + 1 < nk) issue(ks + 1);
+      if (MUON_PRIO == 1) __builtin_amdgcn_s_setprio(1);
       __builtin_amdgcn_sched_barrier(0);
       rd(sp, 1, 1); mm(0); interleave();
       __builtin_amdgcn_sched_barrier(0);
@@ -738,6 +744,7 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
       mm(1); interleave();
       __builtin_amdgcn_sched_barrier(0);
     }
+    if (MUON_PRIO) __builtin_amdgcn_s_setprio(0);
   } else
   for (int ks = 0; ks < nk; ++ks) {
     if (ks + D < nk) issue(ks + D);
