@@ -483,6 +483,28 @@ __device__ __forceinline__ void quad_transpose(float x[4]) {
   for (int r = 0; r < 4; ++r) x[r] = ((r ^ t) & 2) ? y[r ^ 2] : n[r];
 }
 
+#ifndef MUON_NT
+#define MUON_NT 1
+#endif
+// Epilogue outputs are written once and read by a later launch: streaming
+// (non-temporal) stores keep them from displacing operand data in L2.
+__device__ __forceinline__ void store_out(uint2* p, uint2 v) {
+  if (MUON_NT) {
+    __builtin_nontemporal_store(v.x, &p->x);
+    __builtin_nontemporal_store(v.y, &p->y);
+  } else {
+    *p = v;
+  }
+}
+__device__ __forceinline__ void store_out(u32x4_t* p, u32x4_t v) {
+  if (MUON_NT) __builtin_nontemporal_store(v, p);
+  else *p = v;
+}
+__device__ __forceinline__ uint2 load_once(const uint2* p) {
+  if (MUON_NT) return uint2{__builtin_nontemporal_load(&p->x), __builtin_nontemporal_load(&p->y)};
+  return *p;
+}
+
 __device__ __forceinline__ uint2 pack_bf16x4(const float v[4]) {
   uint2 p;
   p.x = static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
@@ -773,9 +795,12 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
 
   // ---- epilogue from registers ----------------------------------------------
   // Lane l holds, per block and register group g, rows row0..row0+3 of one
-  // column.  The transposed orientation takes those 4 values as one 8-byte
-  // vector; a 4-lane transpose gives the direct orientation the same shape
-  // (lane t of a quad: row row0+t, columns c0..c0+3).
+  // column.  A 4-lane transpose turns that into row row0+t, columns
+  // c0..c0+3 (t = lane % 4), so the direct orientation is read and written
+  // as 8-byte vectors with 8 lanes covering 64 contiguous bytes of a row.
+  // The transposed orientation is staged in LDS (padded rows) and written
+  // out as whole 512-byte rows.  Diagonal tiles of the symmetric products
+  // keep a per-element path.
   const bool diag = ga.syrk && bm == bn;
   const MatDesc* md = FINAL ? ga.desc + mat : nullptr;
   const bool tr = FINAL ? md->transposed != 0 : false;
@@ -785,69 +810,113 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   const int col_base = bn * BN + wn * (BN / WN) + frow;
   char* const C = ga.C + mat * ga.c_mat;
   char* const CT = ga.CT + mat * ga.ct_mat;
+  const char* const E = ga.E + mat * ga.e_mat;
   const char* const ET = ga.ET + mat * ga.et_mat;
+  constexpr int TST = BM * 2 + 8;             // staged transposed row, bytes
+  const bool stage_t = !FINAL && !diag;
+  if (stage_t) __syncthreads();               // every wave is done with the operand slabs
+  // Every load of the epilogue is issued before its first store, so one
+  // memory latency is exposed instead of one per group.
+  uint2 ev[BI][BJ][4];
+  if (EPI != EPI_GRAM && !diag) {
+    static_for<BI>([&](auto I) {
+      static_for<BJ>([&](auto J) {
+        static_for<4>([&](auto G) {
+          constexpr int i = decltype(I)::value, j = decltype(J)::value, g = decltype(G)::value;
+          const int row0 = row_base + i * 32 + 8 * g;
+          const int c0 = col_base + j * 32 - q4;
+          ev[i][j][g] = load_once(reinterpret_cast<const uint2*>(E + static_cast<int64_t>(row0 + q4) * ga.lde + c0 * 2));
+        });
+      });
+    });
+  }
   static_for<BI>([&](auto I) {
   static_for<BJ>([&](auto J) {
   static_for<4>([&](auto G) {
         constexpr int i = decltype(I)::value, j = decltype(J)::value, g = decltype(G)::value;
         const int row0 = row_base + i * 32 + 8 * g;  // rows row0 .. row0 + 3
         const int col = col_base + j * 32;
-        float v[4];
-        if (EPI == EPI_GRAM) {
+        const int c0 = col - q4;                     // after the quad transpose
+        if (!FINAL && diag) {
+          float v[4];
+          if (EPI == EPI_GRAM) {
 #pragma unroll
-          for (int q = 0; q < 4; ++q) v[q] = acc[i][j][4 * g + q];
-        } else {
-          // the a*X (or b*A) term: 4 consecutive rows of column `col`, read
-          // from the transposed copy (same bits) as one 8-byte vector
-          const uint2 raw = *reinterpret_cast<const uint2*>(ET + static_cast<int64_t>(col) * ga.ldet + row0 * 2);
+            for (int q = 0; q < 4; ++q) v[q] = acc[i][j][4 * g + q];
+          } else {
+            const uint2 raw = *reinterpret_cast<const uint2*>(ET + static_cast<int64_t>(col) * ga.ldet + row0 * 2);
+            const float e[4] = {__uint_as_float(raw.x << 16), __uint_as_float(raw.x & 0xffff0000u),
+                                __uint_as_float(raw.y << 16), __uint_as_float(raw.y & 0xffff0000u)};
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              v[q] = EPI == EPI_POLY ? fmaf(ga.alpha, e[q], ga.beta * acc[i][j][4 * g + q])
+                                     : fmaf(ga.alpha, e[q], acc[i][j][4 * g + q]);
+          }
+          // symmetric diagonal tile: the upper triangle (row <= col) is the
+          // value of both (row, col) and (col, row)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int row = row0 + q;
+            if (row <= col) {
+              const uint16_t h = f32_to_bf16(v[q]);
+              *reinterpret_cast<uint16_t*>(C + static_cast<int64_t>(row) * ga.ldc + col * 2) = h;
+              *reinterpret_cast<uint16_t*>(C + static_cast<int64_t>(col) * ga.ldc + row * 2) = h;
+            }
+          }
+          return;
+        }
+        // direct-layout values of row row0 + q4, columns c0 .. c0 + 3
+        float v[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[q] = acc[i][j][4 * g + q];
+        quad_transpose(v);
+        if (EPI != EPI_GRAM) {
+          const uint2 raw = ev[i][j][g];
           const float e[4] = {__uint_as_float(raw.x << 16), __uint_as_float(raw.x & 0xffff0000u),
                               __uint_as_float(raw.y << 16), __uint_as_float(raw.y & 0xffff0000u)};
 #pragma unroll
           for (int q = 0; q < 4; ++q)
-            v[q] = EPI == EPI_POLY ? fmaf(ga.alpha, e[q], ga.beta * acc[i][j][4 * g + q])
-                                   : fmaf(ga.alpha, e[q], acc[i][j][4 * g + q]);
+            v[q] = EPI == EPI_POLY ? fmaf(ga.alpha, e[q], ga.beta * v[q]) : fmaf(ga.alpha, e[q], v[q]);
         }
-        if (EPI == EPI_GRAM || EPI == EPI_POLY || EPI == EPI_UPDATE) {
+        if (!FINAL) {
           float o[4];
 #pragma unroll
           for (int q = 0; q < 4; ++q) o[q] = bf16_to_f32(f32_to_bf16(v[q]));
-          if (!diag) {
-            *reinterpret_cast<uint2*>(CT + static_cast<int64_t>(col) * ga.ldct + row0 * 2) = pack_bf16x4(o);
-            quad_transpose(o);
-            *reinterpret_cast<uint2*>(C + static_cast<int64_t>(row0 + q4) * ga.ldc + (col - q4) * 2) = pack_bf16x4(o);
-          } else {
-            // symmetric diagonal tile: the upper triangle (row <= col) is the
-            // value of both (row, col) and (col, row)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int row = row0 + q;
-              if (row <= col) {
-                const uint16_t h = f32_to_bf16(o[q]);
-                *reinterpret_cast<uint16_t*>(C + static_cast<int64_t>(row) * ga.ldc + col * 2) = h;
-                *reinterpret_cast<uint16_t*>(C + static_cast<int64_t>(col) * ga.ldc + row * 2) = h;
-              }
-            }
+          store_out(reinterpret_cast<uint2*>(C + static_cast<int64_t>(row0 + q4) * ga.ldc + c0 * 2), pack_bf16x4(o));
+          // back to 4 rows of one column: the transposed tile's row, staged
+          quad_transpose(o);
+          *reinterpret_cast<uint2*>(smem + (col - bn * BN) * TST + (row0 - bm * BM) * 2) = pack_bf16x4(o);
+        } else if (!tr) {  // parameter is s x l: elements (row0 + q4, c0 .. c0 + 3)
+          const int row = row0 + q4;
+          if (row < ga.s) {
+            const int n = min(4, ga.l - c0);
+            if (n > 0)
+              apply4<FK, PDT>(md, static_cast<int64_t>(row) * md->cols + c0, v, v4 && n == 4, n);
           }
-        } else {  // final step: O = v (fp32) -> parameter update or output
-          if (tr) {  // parameter is l x s: elements (col, row0 .. row0 + 3)
-            if (col < ga.l) {
-              const int n = min(4, ga.s - row0);
-              if (n > 0)
-                apply4<FK, PDT>(md, static_cast<int64_t>(col) * md->cols + row0, v, v4 && n == 4, n);
-            }
-          } else {   // parameter is s x l: elements (row0 + q4, c0 .. c0 + 3)
-            quad_transpose(v);
-            const int row = row0 + q4, c0 = col - q4;
-            if (row < ga.s) {
-              const int n = min(4, ga.l - c0);
-              if (n > 0)
-                apply4<FK, PDT>(md, static_cast<int64_t>(row) * md->cols + c0, v, v4 && n == 4, n);
-            }
+        } else {           // parameter is l x s: elements (col, row0 .. row0 + 3)
+          quad_transpose(v);
+          if (col < ga.l) {
+            const int n = min(4, ga.s - row0);
+            if (n > 0)
+              apply4<FK, PDT>(md, static_cast<int64_t>(col) * md->cols + row0, v, v4 && n == 4, n);
           }
         }
   });
   });
   });
+  if (stage_t) {
+    __syncthreads();
+    // transposed tile rows (BM bf16 = BM*2 bytes each) -> CT, 16 bytes a thread
+    constexpr int CH = BM * 2 / 16;
+    for (int idx = threadIdx.x; idx < BN * CH; idx += 64 * NW) {
+      const int c = idx / CH, ch = idx - c * CH;
+      const char* src = smem + c * TST + ch * 16;
+      const uint2 lo = *reinterpret_cast<const uint2*>(src);
+      const uint2 hi = *reinterpret_cast<const uint2*>(src + 8);
+      store_out(reinterpret_cast<u32x4_t*>(CT + static_cast<int64_t>(bn * BN + c) * ga.ldct + bm * BM * 2 + ch * 16),
+                u32x4_t{lo.x, lo.y, hi.x, hi.y});
+    }
+    __syncthreads();  // the next tile's loads overwrite the staging area
+  }
 }
 
 // Persistent launch: one workgroup per CU slot loops over tiles in rounds.
@@ -858,7 +927,8 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
 template <int EPI, class Cfg>
 __global__ __launch_bounds__(64 * Cfg::NW) __attribute__((amdgpu_waves_per_eu(Cfg::WPE, Cfg::WPE)))
 void k_gemm_tile(GemmArgs ga) {
-  __shared__ __attribute__((aligned(1024))) char smem[Cfg::LDS];
+  constexpr int STAGED = Cfg::BN * (Cfg::BM * 2 + 8);  // epilogue staging of a transposed tile
+  __shared__ __attribute__((aligned(1024))) char smem[Cfg::LDS > STAGED ? Cfg::LDS : STAGED];
   const int G = static_cast<int>(gridDim.x), b = static_cast<int>(blockIdx.x);
   for (int r = 0;; ++r) {
     const int logical = (G % 8 == 0) ? r * G + (b & 7) * (G / 8) + (b >> 3) : r * G + b;
