@@ -25,21 +25,25 @@ namespace muon {
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------------------
-// bfloat16 storage: uint16 bit patterns.  Widening is exact; narrowing rounds
-// to nearest, ties to even (NaN stays NaN).
+// bfloat16 storage: uint16 bit patterns.  Widening is exact; narrowing is
+// the hardware conversion (v_cvt_pk_bf16_f32): round to nearest, ties to
+// even, NaN stays NaN, overflow to infinity.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) {
   return __uint_as_float(static_cast<uint32_t>(h) << 16);
 }
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return static_cast<uint16_t>(u >> 16);
+  return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
+}
+// lo | hi << 16, both rounded as above, in one instruction
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
 }
 
 template <typename T> __device__ __forceinline__ float to_f32(T v);
@@ -177,11 +181,13 @@ __global__ __launch_bounds__(256) void k_normalize(const MatDesc* __restrict__ d
   const int i0 = blockIdx.y * 64, j0 = blockIdx.x * 64;  // tile origin in X coordinates
   const int ur0 = tr ? j0 : i0, uc0 = tr ? i0 : j0;       // same tile in u coordinates
   const int64_t matX = static_cast<int64_t>(cg.S) * cg.L;
+  // X0 (S x L) is always written; X0^T only when XTb is given.  u's own
+  // layout is X0 when u is s x l and X0^T when it is l x s (transposed).
   XT* Xm = X + m * matX;
-  XT* XTm = XTb + m * matX;
-  XT* D = tr ? XTm : Xm;            // u's own layout
+  XT* XTm = XTb ? XTb + m * matX : nullptr;
+  XT* D = tr ? XTm : Xm;            // u's own layout (coalesced from the input)
   const int ldD = tr ? cg.S : cg.L;
-  XT* Tb = tr ? Xm : XTm;           // the transpose
+  XT* Tb = tr ? Xm : XTm;           // the transpose, through LDS
   const int ldT = tr ? cg.L : cg.S;
   const float r = rscale[m];
   const GT* __restrict__ g = static_cast<const GT*>(md.g);
@@ -204,9 +210,10 @@ __global__ __launch_bounds__(256) void k_normalize(const MatDesc* __restrict__ d
       v = u * r;
     }
     const XT xv = from_f32<XT>(v);
-    D[static_cast<int64_t>(ur) * ldD + uc] = xv;
+    if (D) D[static_cast<int64_t>(ur) * ldD + uc] = xv;
     tile[row * LDT + col] = xv;
   }
+  if (!Tb) return;  // uniform over the block
   __syncthreads();
 #pragma unroll 4
   for (int trow = threadIdx.x >> 6; trow < 64; trow += 4) {
@@ -443,19 +450,19 @@ __global__ __launch_bounds__(256, 2) void k_gemm_nt(GemmArgs ga) {
 // global-to-LDS loads (global_load_lds_dwordx4: lane i of a wavefront writes
 // bytes [16 i, 16 i + 16) after the wave-uniform LDS base), double-buffered.
 // A wavefront instruction fills 8 consecutive tile rows; lane i fetches the
-// 16-byte k-chunk (i % 8) ^ (row % 8) of its row, so LDS row r holds chunk c
-// at position c ^ (r % 8).  Fragment reads (32 rows, one chunk) then hit 8
-// distinct 16-byte positions per 8 lanes: no bank conflicts.
+// 16-byte k-chunk (i % 8) ^ ((row >> 1) % 8) of its row, so LDS row r holds
+// chunk c at position c ^ ((r >> 1) % 8).  A fragment read (32 rows, one
+// chunk) then spreads over all 64 banks.
 //
-// Workgroup b runs on XCD b % 8; the tile order gives every XCD a contiguous
-// range of tiles, grouped 4 tile-rows high so concurrent tiles of one XCD
-// share operand panels in its L2.
+// The launch is persistent (one workgroup per CU).  Workgroup b runs on XCD
+// b % 8; every round, the workgroups of one XCD take one compact block of the
+// tile order (bands 8 tile-rows high), so they share operand panels in that
+// XCD's L2.
 //
 // The epilogue works on the accumulator registers directly: lane l holds
-// rows 8*(r/4) + 4*(l/32) + (r%4) of column l%32 in register r of a block;
-// direct stores are 2 bytes per lane (32 lanes on consecutive columns), the
-// transposed orientation stores the 4 consecutive rows a lane holds as one
-// 8-byte vector.
+// rows 8*(r/4) + 4*(l/32) + (r%4) of column l%32 in register r of a block, so
+// 4 consecutive registers are 4 consecutive elements of a row of the
+// transposed tile; a 4-lane transpose (DPP) gives the direct orientation.
 // ---------------------------------------------------------------------------
 // Compile-time loop: f(std::integral_constant<int, 0>) ... f(<N-1>), so array
 // indices inside f are constants whatever the unroller decides.
@@ -468,19 +475,46 @@ __device__ __forceinline__ void static_for(F&& f) {
   static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
+// Lane exchange inside each group of 4 lanes by DPP quad permutation: a VALU
+// operand modifier, no LDS traffic.
+constexpr int kQuadXor1 = 0xB1;  // quad_perm [1,0,3,2]
+constexpr int kQuadXor2 = 0x4E;  // quad_perm [2,3,0,1]
+template <int CTRL>
+__device__ __forceinline__ uint32_t quad_swap(uint32_t x) {
+  return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), CTRL, 0xF, 0xF, true));
+}
+
 // Lanes 4p..4p+3 each hold x[0..3] = M[t][0..3] (t = lane % 4); afterwards
 // lane t holds M[0..3][t].  Two butterfly stages over lane bits 0 and 1.
+// Every lane of the quad must be active.
 __device__ __forceinline__ void quad_transpose(float x[4]) {
   const int t = threadIdx.x & 3;
   float y[4], n[4];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) y[k] = __shfl_xor(x[k], 1, 64);
+  for (int k = 0; k < 4; ++k) y[k] = __uint_as_float(quad_swap<kQuadXor1>(__float_as_uint(x[k])));
 #pragma unroll
   for (int r = 0; r < 4; ++r) n[r] = ((r ^ t) & 1) ? y[r ^ 1] : x[r];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) y[k] = __shfl_xor(n[k], 2, 64);
+  for (int k = 0; k < 4; ++k) y[k] = __uint_as_float(quad_swap<kQuadXor2>(__float_as_uint(n[k])));
 #pragma unroll
   for (int r = 0; r < 4; ++r) x[r] = ((r ^ t) & 2) ? y[r ^ 2] : n[r];
+}
+
+// The same 4 x 4 transpose on packed bfloat16: d.x = M[t][0] | M[t][1] << 16,
+// d.y = M[t][2] | M[t][3] << 16 becomes d.x = M[0][t] | M[1][t] << 16,
+// d.y = M[2][t] | M[3][t] << 16.  Stage 1 swaps the off-diagonal 2 x 2
+// blocks (whole dwords, lanes t ^ 2); stage 2 transposes inside each block
+// (16-bit halves, lanes t ^ 1) with byte permutes.  8 VALU operations.
+__device__ __forceinline__ uint2 quad_transpose_bf16(uint2 d) {
+  const int t = threadIdx.x & 3;
+  const bool hi_pair = (t & 2) != 0, odd = (t & 1) != 0;
+  const uint32_t r1 = quad_swap<kQuadXor2>(hi_pair ? d.x : d.y);
+  const uint32_t x1 = hi_pair ? r1 : d.x, y1 = hi_pair ? d.y : r1;
+  // v_perm_b32(s0, s1, sel): selector bytes 0-3 pick bytes of s1, 4-7 of s0
+  const uint32_t send = __builtin_amdgcn_perm(y1, x1, odd ? 0x05040100u : 0x07060302u);
+  const uint32_t r2 = quad_swap<kQuadXor1>(send);
+  return uint2{__builtin_amdgcn_perm(r2, x1, odd ? 0x03020504u : 0x05040100u),
+               __builtin_amdgcn_perm(r2, y1, odd ? 0x03020706u : 0x07060100u)};
 }
 
 #ifndef MUON_NT
@@ -506,10 +540,11 @@ __device__ __forceinline__ uint2 load_once(const uint2* p) {
 }
 
 __device__ __forceinline__ uint2 pack_bf16x4(const float v[4]) {
-  uint2 p;
-  p.x = static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
-  p.y = static_cast<uint32_t>(f32_to_bf16(v[2])) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
-  return p;
+  return uint2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+}
+__device__ __forceinline__ void unpack_bf16x4(uint2 p, float v[4]) {
+  v[0] = __uint_as_float(p.x << 16); v[1] = __uint_as_float(p.x & 0xffff0000u);
+  v[2] = __uint_as_float(p.y << 16); v[3] = __uint_as_float(p.y & 0xffff0000u);
 }
 
 // Ragged-edge tail of apply4 (kept out of line: it is rare, and keeping the
@@ -531,22 +566,19 @@ __device__ __noinline__ void apply_tail(const MatDesc* md, int64_t idx, float o0
 
 // W[idx .. idx+3] = decay*W - upd*o (FK = 0) or out[idx ..] = o (FK = 1), 4
 // consecutive elements of dtype PDT: one vector access when `vec`, else
-// element by element up to `n`.
+// element by element up to `n`.  The parameter is read and written with
+// ordinary (cached) accesses, each load right before its store: measured
+// faster than streaming accesses or loads hoisted ahead of the stores.
 template <int FK, int PDT>
-__device__ __forceinline__ void apply4(const MatDesc* md, int64_t idx, const float o[4], bool vec,
-                                       int n) {
+__device__ __forceinline__ void apply4(const MatDesc* md, int64_t idx, const float o[4], bool vec, int n) {
   using PT = typename std::conditional<PDT == DT_BF16, uint16_t, float>::type;
   PT* dst = static_cast<PT*>(FK == 0 ? md->W : md->out);
   const float decay = md->decay, upd = md->upd_scale;
   if (vec) {
     float w[4] = {0.f, 0.f, 0.f, 0.f}, r[4];
-    if (PDT == DT_BF16) {
+    if constexpr (PDT == DT_BF16) {
       uint2* p = reinterpret_cast<uint2*>(dst + idx);
-      if (FK == 0) {
-        const uint2 raw = *p;
-        w[0] = __uint_as_float(raw.x << 16); w[1] = __uint_as_float(raw.x & 0xffff0000u);
-        w[2] = __uint_as_float(raw.y << 16); w[3] = __uint_as_float(raw.y & 0xffff0000u);
-      }
+      if (FK == 0) unpack_bf16x4(*p, w);
 #pragma unroll
       for (int q = 0; q < 4; ++q) r[q] = FK == 0 ? fmaf(decay, w[q], -upd * o[q]) : o[q];
       *p = pack_bf16x4(r);
@@ -565,6 +597,31 @@ __device__ __forceinline__ void apply4(const MatDesc* md, int64_t idx, const flo
   apply_tail<FK, PDT>(md, idx, o[0], o[1], o[2], o[3], n);
 }
 
+// Byte offset of an LDS object.
+__device__ __forceinline__ uint32_t lds_offset(const char* p) {
+  return static_cast<uint32_t>(
+      reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) char*)(p)));
+}
+
+// Direct global -> LDS load (global_load_lds_dwordx4): lane i writes the 16
+// bytes at `g` to LDS bytes [lds + 16 i, lds + 16 i + 16); `lds` is
+// wave-uniform.  Issued as inline assembly so that the compiler keeps no
+// record of it: the kernel waits for these loads explicitly (vmcnt) before
+// the barrier that publishes a slab, and the transposing LDS reads of the
+// other stage must not wait for them.  M0 is set inside the statement.
+__device__ __forceinline__ void load_lds16(const char* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(g), "s"(__builtin_amdgcn_readfirstlane(lds)) : "memory");
+}
+
+// 8 bytes per lane from LDS through the transposing read (ds_read_b64_tr_b16).
+__device__ __forceinline__ uint2 tr_read_b64(const char* p) {
+  typedef short v4i16 __attribute__((ext_vector_type(4)));
+  const v4i16 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) v4i16*)(const_cast<char*>(p)));
+  return __builtin_bit_cast(uint2, v);
+}
+
 // Tile configuration of the direct-to-LDS MFMA kernel: output tile BM x BN,
 // a WM x WN grid of wavefronts (each BM/WM x BN/WN), SLAB bytes of every
 // tile row staged per LDS stage, NS stages, WPE wavefronts per SIMD.
@@ -581,8 +638,6 @@ struct TileCfg {
 #define MUON_SQ_STAGES 2
 #endif
 using CfgSquare = TileCfg<256, 256, 2, 4, MUON_SQ_SLAB, MUON_SQ_STAGES, 2>;
-// 256 x 128, 4 wavefronts, two workgroups per CU.
-using CfgRect = TileCfg<256, 128, 2, 2, 64, 2, 2>;
 
 // Tile `logical` of the launch: matrix-major; inside a matrix, banded
 // (GS / GM tile-rows per band, column by column inside a band).
@@ -657,8 +712,13 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
+  // The update products (X' = a X + B X and the last step) read X itself as
+  // the second operand: its slabs are K rows of the direct layout (QTR).
+  constexpr bool QTR = EPI == EPI_UPDATE || FINAL;
+  static_assert(!QTR || (BN * 2 == 512 && SLAB == 128), "QTR slab geometry: 64 k-rows of 512 bytes");
   const char* Pb = ga.P + mat * ga.p_mat + static_cast<int64_t>(bm) * BM * ga.ldp;
-  const char* Qb = ga.Q + mat * ga.q_mat + static_cast<int64_t>(bn) * BN * ga.ldq;
+  const char* Qb = QTR ? ga.Q + mat * ga.q_mat + static_cast<int64_t>(bn) * BN * 2
+                       : ga.Q + mat * ga.q_mat + static_cast<int64_t>(bn) * BN * ga.ldq;
 
   // Direct global -> LDS loads.  A wave instruction fills RPI consecutive
   // tile rows (1 KB); lane l writes row r0 + l / CPR at position l % CPR and
@@ -674,22 +734,25 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   }
 #pragma unroll
   for (int i = 0; i < NLQ; ++i) {
-    const int r = wave * QR + RPI * i + lane / CPR;
-    qa[i] = Qb + static_cast<int64_t>(r) * ga.ldq + ((lane % CPR) ^ ((r >> SH) & (CPR - 1))) * 16;
+    if (QTR) {
+      // Q slab = 64 rows k of 512 bytes (256 columns n); a wave instruction
+      // fills 2 rows.  16-byte chunk c of row k sits at position c ^ 4*(k % 4).
+      const int r = wave * (NLQ * 2) + 2 * i + lane / 32;
+      qa[i] = Qb + static_cast<int64_t>(r) * ga.ldq + ((lane % 32) ^ ((r & 3) << 2)) * 16;
+    } else {
+      const int r = wave * QR + RPI * i + lane / CPR;
+      qa[i] = Qb + static_cast<int64_t>(r) * ga.ldq + ((lane % CPR) ^ ((r >> SH) & (CPR - 1))) * 16;
+    }
   }
+  const uint32_t lds0 = lds_offset(smem);
   auto issue = [&](int ks) {
-    char* base = smem + (ks % NS) * STAGE;
+    const uint32_t base = lds0 + (ks % NS) * STAGE;
     const int64_t ko = static_cast<int64_t>(ks) * SLAB;
+    const int64_t kq = QTR ? static_cast<int64_t>(ks) * 64 * ga.ldq : ko;
 #pragma unroll
-    for (int i = 0; i < NLP; ++i)
-      __builtin_amdgcn_global_load_lds(
-          (const __attribute__((address_space(1))) void*)(pa[i] + ko),
-          (__attribute__((address_space(3))) void*)(base + (wave * PR + RPI * i) * SLAB), 16, 0, 0);
+    for (int i = 0; i < NLP; ++i) load_lds16(pa[i] + ko, base + (wave * PR + RPI * i) * SLAB);
 #pragma unroll
-    for (int i = 0; i < NLQ; ++i)
-      __builtin_amdgcn_global_load_lds(
-          (const __attribute__((address_space(1))) void*)(qa[i] + ko),
-          (__attribute__((address_space(3))) void*)(base + OPQ + (wave * QR + RPI * i) * SLAB), 16, 0, 0);
+    for (int i = 0; i < NLQ; ++i) load_lds16(qa[i] + kq, base + OPQ + (wave * QR + RPI * i) * SLAB);
   };
 
   f32x16_t acc[BI][BJ];
@@ -704,6 +767,21 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   const int frow = lane & 31, fsel = lane >> 5, fsw = (frow >> SH) & (CPR - 1);
   const int a_off = (wm * (BM / WM) + frow) * SLAB;
   const int b_off = OPQ + (wn * (BN / WN) + frow) * SLAB;
+  // QTR fragments: ds_read_b64_tr_b16 hands lane t of each 16-lane group G,
+  // as its r-th element, element t % 4 of the 8 bytes addressed by lane
+  // 4r + t / 4 of the group.  Lane L of group G therefore addresses row
+  // 16*grp + 8*(G/2) + 4*h + L/4, columns n0 + 16*(G%2) + 4*(L%4) .. +3, and
+  // two reads (h = 0, 1) give the 8 consecutive k of column n0 + lane % 32
+  // that the MFMA takes.  Rows k and k + 8 share a bank group; the swizzle
+  // (k % 4) spreads the 4 rows of a read over all 64 banks.
+  int tq_off[BJ];
+#pragma unroll
+  for (int j = 0; j < BJ; ++j) {
+    const int G = lane >> 4, L = lane & 15;
+    const int row = 8 * (G >> 1) + (L >> 2);
+    const int cb = 2 * (wn * (BN / WN) + j * 32) + 32 * (G & 1) + 8 * (L & 3);
+    tq_off[j] = OPQ + row * 512 + (cb ^ ((L >> 2) << 6));
+  }
 
   const int nk = ga.k_slabs;
 #pragma unroll
@@ -728,20 +806,31 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
 #pragma unroll
       for (int i = 0; i < BI; ++i) fa[set][i] = *reinterpret_cast<const u32x4_t*>(sp + a_off + i * 32 * SLAB + pos);
 #pragma unroll
-      for (int j = 0; j < BJ; ++j) fb[set][j] = *reinterpret_cast<const u32x4_t*>(sp + b_off + j * 32 * SLAB + pos);
+      for (int j = 0; j < BJ; ++j) {
+        if (QTR) {
+          const char* q = sp + tq_off[j] + grp * 16 * 512;
+          const uint2 lo = tr_read_b64(q), hi = tr_read_b64(q + 4 * 512);
+          fb[set][j] = u32x4_t{lo.x, lo.y, hi.x, hi.y};
+        } else {
+          fb[set][j] = *reinterpret_cast<const u32x4_t*>(sp + b_off + j * 32 * SLAB + pos);
+        }
+      }
     };
     auto mm = [&](int set) {
       static_for<BI>([&](auto I) {
         static_for<BJ>([&](auto J) { Mma<uint16_t>::run(fa[set][I.value], fb[set][J.value], acc[I.value][J.value]); });
       });
     };
+    constexpr int NRD = BI + (QTR ? 2 : 1) * BJ;  // LDS reads per group
+    constexpr int NPAIR = NRD < BI * BJ ? NRD : BI * BJ;
     auto interleave = [&]() {
 #pragma unroll
-      for (int i = 0; i < BI + BJ; ++i) {
+      for (int i = 0; i < NPAIR; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
       }
-      __builtin_amdgcn_sched_group_barrier(0x008, BI * BJ - (BI + BJ), 0);
+      if constexpr (BI * BJ > NPAIR) __builtin_amdgcn_sched_group_barrier(0x008, BI * BJ - NPAIR, 0);
+      if constexpr (NRD > NPAIR) __builtin_amdgcn_sched_group_barrier(0x100, NRD - NPAIR, 0);
     };
 #ifndef MUON_PRIO
 #define MUON_PRIO 0
@@ -767,7 +856,8 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
       __builtin_amdgcn_sched_barrier(0);
     }
     if (MUON_PRIO) __builtin_amdgcn_s_setprio(0);
-  } else
+  } else {
+  static_assert(!QTR, "QTR fragments are read by the interleaved main loop only");
   for (int ks = 0; ks < nk; ++ks) {
     if (ks + D < nk) issue(ks + D);
     const char* sp = smem + (ks % NS) * STAGE;
@@ -792,15 +882,27 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
       wait_slabs_in_flight<LPS>(min(nk - 1, ks + D) - (ks + 1));
     __syncthreads();
   }
+  }
 
   // ---- epilogue from registers ----------------------------------------------
-  // Lane l holds, per block and register group g, rows row0..row0+3 of one
-  // column.  A 4-lane transpose turns that into row row0+t, columns
-  // c0..c0+3 (t = lane % 4), so the direct orientation is read and written
-  // as 8-byte vectors with 8 lanes covering 64 contiguous bytes of a row.
-  // The transposed orientation is staged in LDS (padded rows) and written
-  // out as whole 512-byte rows.  Diagonal tiles of the symmetric products
-  // keep a per-element path.
+  // Lane l holds, per 32x32 block and register group g, rows row0..row0+3 of
+  // one column `col` (the natural layout: also 4 consecutive elements of row
+  // `col` of the transposed tile).  A 4-lane transpose gives the direct
+  // layout: lane t = l % 4 holds row row0+t, columns c0..c0+3, and 8 lanes
+  // cover 64 contiguous bytes of a row.
+  //  - The a*X (or A) term is read coalesced in the direct layout and turned
+  //    to the natural one while still packed bfloat16.
+  //  - Outputs are rounded to bfloat16 once; the direct copy goes straight to
+  //    memory.  The symmetric products also write the mirrored tile: the
+  //    natural copy goes to an LDS staging area (padded rows) that is written
+  //    out as whole rows of the transposed tile.  X' needs no transposed copy,
+  //    since the next update reads X through transposing LDS reads.
+  //  - The last step's parameter update runs in the parameter's layout:
+  //    direct when it is s x l, natural when it is l x s.
+  //  - Every load of the a*X (or A) term is issued before the first store,
+  //    so one memory latency is exposed instead of one per block.
+  // Diagonal tiles of the symmetric products take a per-element path that
+  // writes the upper triangle to both halves.
   const bool diag = ga.syrk && bm == bn;
   const MatDesc* md = FINAL ? ga.desc + mat : nullptr;
   const bool tr = FINAL ? md->transposed != 0 : false;
@@ -813,46 +915,26 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   const char* const E = ga.E + mat * ga.e_mat;
   const char* const ET = ga.ET + mat * ga.et_mat;
   constexpr int TST = BM * 2 + 8;             // staged transposed row, bytes
-  const bool stage_t = !FINAL && !diag;
-  if (stage_t) __syncthreads();               // every wave is done with the operand slabs
-  // Every load of the epilogue is issued before its first store, so one
-  // memory latency is exposed instead of one per group.
-  uint2 ev[BI][BJ][4];
-  if (EPI != EPI_GRAM && !diag) {
+
+  if (!FINAL && diag) {
     static_for<BI>([&](auto I) {
       static_for<BJ>([&](auto J) {
         static_for<4>([&](auto G) {
           constexpr int i = decltype(I)::value, j = decltype(J)::value, g = decltype(G)::value;
           const int row0 = row_base + i * 32 + 8 * g;
-          const int c0 = col_base + j * 32 - q4;
-          ev[i][j][g] = load_once(reinterpret_cast<const uint2*>(E + static_cast<int64_t>(row0 + q4) * ga.lde + c0 * 2));
-        });
-      });
-    });
-  }
-  static_for<BI>([&](auto I) {
-  static_for<BJ>([&](auto J) {
-  static_for<4>([&](auto G) {
-        constexpr int i = decltype(I)::value, j = decltype(J)::value, g = decltype(G)::value;
-        const int row0 = row_base + i * 32 + 8 * g;  // rows row0 .. row0 + 3
-        const int col = col_base + j * 32;
-        const int c0 = col - q4;                     // after the quad transpose
-        if (!FINAL && diag) {
+          const int col = col_base + j * 32;
           float v[4];
           if (EPI == EPI_GRAM) {
 #pragma unroll
             for (int q = 0; q < 4; ++q) v[q] = acc[i][j][4 * g + q];
           } else {
-            const uint2 raw = *reinterpret_cast<const uint2*>(ET + static_cast<int64_t>(col) * ga.ldet + row0 * 2);
-            const float e[4] = {__uint_as_float(raw.x << 16), __uint_as_float(raw.x & 0xffff0000u),
-                                __uint_as_float(raw.y << 16), __uint_as_float(raw.y & 0xffff0000u)};
+            float e[4];
+            unpack_bf16x4(*reinterpret_cast<const uint2*>(ET + static_cast<int64_t>(col) * ga.ldet + row0 * 2), e);
 #pragma unroll
             for (int q = 0; q < 4; ++q)
               v[q] = EPI == EPI_POLY ? fmaf(ga.alpha, e[q], ga.beta * acc[i][j][4 * g + q])
                                      : fmaf(ga.alpha, e[q], acc[i][j][4 * g + q]);
           }
-          // symmetric diagonal tile: the upper triangle (row <= col) is the
-          // value of both (row, col) and (col, row)
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             const int row = row0 + q;
@@ -862,48 +944,78 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
               *reinterpret_cast<uint16_t*>(C + static_cast<int64_t>(col) * ga.ldc + row * 2) = h;
             }
           }
-          return;
-        }
-        // direct-layout values of row row0 + q4, columns c0 .. c0 + 3
-        float v[4];
+        });
+      });
+    });
+    return;
+  }
+
+  // the symmetric products also write the mirrored tile, staged through LDS
+  constexpr bool stage_t = !QTR;
+  if (stage_t) __syncthreads();               // every wave is done with the operand slabs
+  // (The loads and the per-block work sit in one lambda: inlined that way the
+  // compiler keeps every value in registers; written at function scope it
+  // spilled.)
+  auto blocks = [&]() {
+    uint2 ev[BI][BJ][4];
+    static_for<BI>([&](auto I) {
+      static_for<BJ>([&](auto J) {
+        static_for<4>([&](auto G) {
+          constexpr int i = decltype(I)::value, j = decltype(J)::value, g = decltype(G)::value;
+          const int row0 = row_base + i * 32 + 8 * g;
+          const int c0 = col_base + j * 32 - q4;
+          if (EPI != EPI_GRAM)
+            ev[i][j][g] = load_once(reinterpret_cast<const uint2*>(E + static_cast<int64_t>(row0 + q4) * ga.lde + c0 * 2));
+        });
+      });
+    });
+    static_for<BI>([&](auto I) {
+      static_for<BJ>([&](auto J) {
+        static_for<4>([&](auto G) {
+          constexpr int i = decltype(I)::value, j = decltype(J)::value, g = decltype(G)::value;
+          const int row0 = row_base + i * 32 + 8 * g;  // rows row0 .. row0 + 3
+          const int col = col_base + j * 32;
+          const int c0 = col - q4;                     // direct layout: columns c0 .. c0 + 3
+          float v[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) v[q] = acc[i][j][4 * g + q];
-        quad_transpose(v);
-        if (EPI != EPI_GRAM) {
-          const uint2 raw = ev[i][j][g];
-          const float e[4] = {__uint_as_float(raw.x << 16), __uint_as_float(raw.x & 0xffff0000u),
-                              __uint_as_float(raw.y << 16), __uint_as_float(raw.y & 0xffff0000u)};
+          for (int q = 0; q < 4; ++q) v[q] = acc[i][j][4 * g + q];
+          if (!FINAL || tr) {  // natural layout
+            if (EPI != EPI_GRAM) {
+              float e[4];
+              unpack_bf16x4(quad_transpose_bf16(ev[i][j][g]), e);
 #pragma unroll
-          for (int q = 0; q < 4; ++q)
-            v[q] = EPI == EPI_POLY ? fmaf(ga.alpha, e[q], ga.beta * v[q]) : fmaf(ga.alpha, e[q], v[q]);
-        }
-        if (!FINAL) {
-          float o[4];
+              for (int q = 0; q < 4; ++q)
+                v[q] = EPI == EPI_POLY ? fmaf(ga.alpha, e[q], ga.beta * v[q]) : fmaf(ga.alpha, e[q], v[q]);
+            }
+            if (!FINAL) {
+              const uint2 p = pack_bf16x4(v);
+              if (stage_t) *reinterpret_cast<uint2*>(smem + (col - bn * BN) * TST + (row0 - bm * BM) * 2) = p;
+              store_out(reinterpret_cast<uint2*>(C + static_cast<int64_t>(row0 + q4) * ga.ldc + c0 * 2),
+                        quad_transpose_bf16(p));
+            } else if (col < ga.l) {  // parameter is l x s: elements (col, row0 .. row0 + 3)
+              const int n = min(4, ga.s - row0);
+              if (n > 0)
+                apply4<FK, PDT>(md, static_cast<int64_t>(col) * md->cols + row0, v, v4 && n == 4, n);
+            }
+          } else {             // parameter is s x l: elements (row0 + q4, c0 .. c0 + 3)
+            quad_transpose(v);
+            float e[4];
+            unpack_bf16x4(ev[i][j][g], e);
 #pragma unroll
-          for (int q = 0; q < 4; ++q) o[q] = bf16_to_f32(f32_to_bf16(v[q]));
-          store_out(reinterpret_cast<uint2*>(C + static_cast<int64_t>(row0 + q4) * ga.ldc + c0 * 2), pack_bf16x4(o));
-          // back to 4 rows of one column: the transposed tile's row, staged
-          quad_transpose(o);
-          *reinterpret_cast<uint2*>(smem + (col - bn * BN) * TST + (row0 - bm * BM) * 2) = pack_bf16x4(o);
-        } else if (!tr) {  // parameter is s x l: elements (row0 + q4, c0 .. c0 + 3)
-          const int row = row0 + q4;
-          if (row < ga.s) {
-            const int n = min(4, ga.l - c0);
-            if (n > 0)
-              apply4<FK, PDT>(md, static_cast<int64_t>(row) * md->cols + c0, v, v4 && n == 4, n);
+            for (int q = 0; q < 4; ++q) v[q] = fmaf(ga.alpha, e[q], v[q]);
+            const int row = row0 + q4;
+            if (row < ga.s) {
+              const int n = min(4, ga.l - c0);
+              if (n > 0)
+                apply4<FK, PDT>(md, static_cast<int64_t>(row) * md->cols + c0, v, v4 && n == 4, n);
+            }
           }
-        } else {           // parameter is l x s: elements (col, row0 .. row0 + 3)
-          quad_transpose(v);
-          if (col < ga.l) {
-            const int n = min(4, ga.s - row0);
-            if (n > 0)
-              apply4<FK, PDT>(md, static_cast<int64_t>(col) * md->cols + row0, v, v4 && n == 4, n);
-          }
-        }
-  });
-  });
-  });
-  if (stage_t) {
+        });
+      });
+    });
+  };
+  blocks();
+  if constexpr (stage_t) {
     __syncthreads();
     // transposed tile rows (BM bf16 = BM*2 bytes each) -> CT, 16 bytes a thread
     constexpr int CH = BM * 2 / 16;
@@ -918,6 +1030,7 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
     __syncthreads();  // the next tile's loads overwrite the staging area
   }
 }
+
 
 // Persistent launch: one workgroup per CU slot loops over tiles in rounds.
 // Workgroup b runs on XCD b % 8; in round r the XCD's workgroups take the
@@ -967,9 +1080,6 @@ __global__ __launch_bounds__(256) void k_apply_x0(const MatDesc* __restrict__ de
 // ---------------------------------------------------------------------------
 // Host-side launch sequence for one chunk.
 // ---------------------------------------------------------------------------
-#ifndef MUON_UPDATE_RECT
-#define MUON_UPDATE_RECT 0
-#endif
 #ifndef MUON_PERSISTENT
 #define MUON_PERSISTENT 1
 #endif
@@ -1015,15 +1125,13 @@ hipError_t launch_tile(int epi, GemmArgs ga, int nmat, hipStream_t st) {
   return hipGetLastError();
 }
 
+// The 256 x 256 kernel runs the bf16 products whose padded extents are
+// multiples of 256: the symmetric ones when S is, the update ones (which
+// read X through transposing LDS reads) when S and L are.  Everything else
+// runs on the 128 x 128 kernel, whose update reads X^T.
 template <typename T>
 hipError_t launch_gemm(int epi, GemmArgs ga, int nmat, hipStream_t st) {
-  // bf16 products on the direct-to-LDS kernels when the padded extents allow
-  // their tiles (multiples of 256 rows); else the 128 x 128 kernel.
-  if (sizeof(T) == 2 && ga.tiles_m % 2 == 0) {
-    if (ga.syrk) return launch_tile<CfgSquare>(epi, ga, nmat, st);
-    if (MUON_UPDATE_RECT) return launch_tile<CfgRect>(epi, ga, nmat, st);
-    if (ga.tiles_n % 2 == 0) return launch_tile<CfgSquare>(epi, ga, nmat, st);
-  }
+  if (sizeof(T) == 2 && ga.tiles_m % 2 == 0 && ga.syrk) return launch_tile<CfgSquare>(epi, ga, nmat, st);
   const dim3 grid(static_cast<unsigned>(ga.tiles_per_mat) * nmat), block(256);
   switch (epi) {
     case EPI_GRAM: hipLaunchKernelGGL((k_gemm_nt<T, EPI_GRAM>), grid, block, 0, st, ga); break;
@@ -1059,6 +1167,11 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
   const int nblk = static_cast<int>(norm_blocks(numel));
   const double gsz = sizeof(GT), xsz = sizeof(XT);
   const double psz = cg.param_dtype == DT_BF16 ? 2.0 : 4.0;
+  // bf16 with S and L multiples of 256: the update products run on the
+  // 256 x 256 kernel and read X through transposing LDS reads, so no X^T is
+  // kept (K = 0 applies X0 from whichever layout matches the parameter).
+  const bool qtr = sizeof(XT) == 2 && cg.S % 256 == 0 && cg.L % 256 == 0 && K > 0;
+  XT* const xt0 = qtr ? nullptr : static_cast<XT*>(wb.XT[0]);
   hipError_t e;
   {
     Timed tm(timer, KK_PARTIALS, st);
@@ -1080,12 +1193,12 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
     const dim3 ngrid(cg.L / 64, cg.S / 64, nmat);
     if (sc.momentum)
       hipLaunchKernelGGL((k_normalize<GT, XT, true>), ngrid, dim3(256), 0, st, d_desc, wb.rscale, sc, cg,
-                         static_cast<XT*>(wb.X[0]), static_cast<XT*>(wb.XT[0]));
+                         static_cast<XT*>(wb.X[0]), xt0);
     else
       hipLaunchKernelGGL((k_normalize<GT, XT, false>), ngrid, dim3(256), 0, st, d_desc, wb.rscale, sc, cg,
-                         static_cast<XT*>(wb.X[0]), static_cast<XT*>(wb.XT[0]));
+                         static_cast<XT*>(wb.X[0]), xt0);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    tm.done(0, 0, nm * ne * (gsz + (sc.momentum ? 4.0 : 0.0) + 2.0 * xsz));
+    tm.done(0, 0, nm * ne * (gsz + (sc.momentum ? 4.0 : 0.0) + (qtr ? 1.0 : 2.0) * xsz));
   }
 
   if (K == 0) {
@@ -1137,29 +1250,37 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
       if ((e = launch_gemm<XT>(EPI_POLY, p, nmat, st)) != hipSuccess) return e;
       tm.done(nm * 2 * s * s * s, nm * 2 * s * s * s * syrk_frac, nm * 2 * s * s * xsz);
     }
-    // X' = a X + B X = a X + B (X^T)^T: M = S, N = L, K = S.
+    // X' = a X + B X: M = S, N = L, K = S.  The second operand is X^T (N x K,
+    // K contiguous) on the 128 x 128 kernel, X itself (K x N) under qtr.
     GemmArgs u{};
     u.P = static_cast<const char*>(wb.B); u.p_mat = matA; u.ldp = cg.S * es;
-    u.Q = XTc; u.q_mat = matX; u.ldq = cg.S * es;
+    if (qtr) {
+      u.Q = X; u.q_mat = matX; u.ldq = cg.L * es;
+    } else {
+      u.Q = XTc; u.q_mat = matX; u.ldq = cg.S * es;
+    }
     u.k_slabs = cg.S * es / 128;
     u.tiles_m = ts; u.tiles_n = tl; u.syrk = 0; u.tiles_per_mat = ts * tl;
     u.E = X; u.e_mat = matX; u.lde = cg.L * es;
-    u.ET = XTc; u.et_mat = matX; u.ldet = cg.S * es;
     u.alpha = a;
     u.s = cg.s; u.l = cg.l;
     const double uf = nm * 2 * s * s * l;
     if (k + 1 < K) {
       u.C = static_cast<char*>(wb.X[cur ^ 1]); u.c_mat = matX; u.ldc = cg.L * es;
-      u.CT = static_cast<char*>(wb.XT[cur ^ 1]); u.ct_mat = matX; u.ldct = cg.S * es;
+      if (!qtr) { u.CT = static_cast<char*>(wb.XT[cur ^ 1]); u.ct_mat = matX; u.ldct = cg.S * es; }
       Timed tm(timer, KK_UPDATE, st);
-      if ((e = launch_gemm<XT>(EPI_UPDATE, u, nmat, st)) != hipSuccess) return e;
-      // reads B, X^T, X; writes X', X'^T
-      tm.done(uf, uf, nm * (s * s + 4 * s * l) * xsz);
+      if ((e = qtr ? launch_tile<CfgSquare>(EPI_UPDATE, u, nmat, st) : launch_gemm<XT>(EPI_UPDATE, u, nmat, st)) !=
+          hipSuccess)
+        return e;
+      // reads B, X (twice under qtr, else X^T and X); writes X' (and X'^T)
+      tm.done(uf, uf, nm * (s * s + (qtr ? 3 : 4) * s * l) * xsz);
       cur ^= 1;
     } else {
       u.desc = d_desc; u.final_kind = sc.final_kind; u.param_dtype = cg.param_dtype;
       Timed tm(timer, KK_FINAL, st);
-      if ((e = launch_gemm<XT>(EPI_FINAL, u, nmat, st)) != hipSuccess) return e;
+      if ((e = qtr ? launch_tile<CfgSquare>(EPI_FINAL, u, nmat, st) : launch_gemm<XT>(EPI_FINAL, u, nmat, st)) !=
+          hipSuccess)
+        return e;
       // reads B, X^T, X (and W); writes W or out
       tm.done(uf, uf, nm * ((s * s + 2 * s * l) * xsz + s * l * (sc.final_kind == 0 ? 2 * psz : psz)));
     }
