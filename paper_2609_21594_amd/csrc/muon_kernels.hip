@@ -257,6 +257,9 @@ struct GemmArgs {
   int32_t final_kind, param_dtype;
   int32_t s, l;
   int32_t total_tiles;                           // tiles_per_mat * matrices
+  // operand storage, 256 x 256 kernel only: 0 row-major over K; 1 symmetric,
+  // upper-triangle 256 x 256 tiles only; 2 (Q) stored K x N
+  int32_t p_mode, q_mode;
 };
 
 constexpr int kRowBytes = 144;                   // 128 data + 16 pad per LDS row
@@ -474,6 +477,8 @@ template <int N, typename F>
 __device__ __forceinline__ void static_for(F&& f) {
   static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
+template <int V>
+using I_ = std::integral_constant<int, V>;
 
 // Lane exchange inside each group of 4 lanes by DPP quad permutation: a VALU
 // operand modifier, no LDS traffic.
@@ -604,14 +609,20 @@ __device__ __forceinline__ uint32_t lds_offset(const char* p) {
 }
 
 // Direct global -> LDS load (global_load_lds_dwordx4): lane i writes the 16
-// bytes at `g` to LDS bytes [lds + 16 i, lds + 16 i + 16); `lds` is
-// wave-uniform.  Issued as inline assembly so that the compiler keeps no
-// record of it: the kernel waits for these loads explicitly (vmcnt) before
-// the barrier that publishes a slab, and the transposing LDS reads of the
-// other stage must not wait for them.  M0 is set inside the statement.
-__device__ __forceinline__ void load_lds16(const char* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :: "v"(g), "s"(__builtin_amdgcn_readfirstlane(lds)) : "memory");
+// bytes at base + off (base wave-uniform, off a 32-bit lane offset) to LDS
+// bytes [lds + 16 i, lds + 16 i + 16); `lds` is wave-uniform.  Issued as
+// inline assembly so that the compiler keeps no record of it: the kernel
+// waits for these loads explicitly (vmcnt) before the barrier that publishes
+// a slab, and the transposing LDS reads of the other stage must not wait for
+// them.  M0 is set inside the statement.
+__device__ __forceinline__ void load_lds16(const char* base, uint32_t off, uint32_t lds) {
+  // (readfirstlane returns int: widen each half as unsigned, never by sign)
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b >> 32)));
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b & 0xffffffffu)));
+  const uint64_t bs = (static_cast<uint64_t>(hi) << 32) | static_cast<uint64_t>(lo);
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(off), "s"(bs), "s"(__builtin_amdgcn_readfirstlane(lds)) : "memory");
 }
 
 // 8 bytes per lane from LDS through the transposing read (ds_read_b64_tr_b16).
@@ -679,15 +690,6 @@ __device__ __forceinline__ void tile_from_logical(const GemmArgs& ga, int logica
   }
 }
 
-// Waits until at most `n` slabs of this wave's direct-to-LDS loads are still
-// in flight (LPS load instructions per slab).
-template <int LPS>
-__device__ __forceinline__ void wait_slabs_in_flight(int n) {
-  if (n >= 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * LPS) : "memory");
-  else if (n == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPS) : "memory");
-  else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-}
-
 template <int EPI, class Cfg>
 __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, int mat, int bm, int bn) {
   constexpr int BM = Cfg::BM, BN = Cfg::BN, WM = Cfg::WM, WN = Cfg::WN, NW = Cfg::NW;
@@ -700,10 +702,7 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   constexpr int PR = BM / NW, QR = BN / NW;   // operand rows each wave loads
   constexpr int NLP = PR / RPI, NLQ = QR / RPI;
   static_assert(NLP * RPI == PR && NLQ * RPI == QR, "load split");
-  constexpr int LPS = NLP + NLQ;              // load instructions per wave and slab
   constexpr int GPS = SLAB / 32;              // 16-k MFMA groups per slab
-  constexpr int D = NS - 1;                   // prefetch distance in slabs
-  static_assert(D >= 1 && D <= 3, "wait_slabs_in_flight handles up to 2 slabs in flight");
   constexpr int OPQ = BM * SLAB;              // Q slab offset in a stage
   constexpr int STAGE = (BM + BN) * SLAB;
   constexpr bool FINAL = EPI >= EPI_FINAL_W_BF16;
@@ -712,47 +711,75 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
-  // The update products (X' = a X + B X and the last step) read X itself as
-  // the second operand: its slabs are K rows of the direct layout (QTR).
-  constexpr bool QTR = EPI == EPI_UPDATE || FINAL;
-  static_assert(!QTR || (BN * 2 == 512 && SLAB == 128), "QTR slab geometry: 64 k-rows of 512 bytes");
-  const char* Pb = ga.P + mat * ga.p_mat + static_cast<int64_t>(bm) * BM * ga.ldp;
-  const char* Qb = QTR ? ga.Q + mat * ga.q_mat + static_cast<int64_t>(bn) * BN * 2
-                       : ga.Q + mat * ga.q_mat + static_cast<int64_t>(bn) * BN * ga.ldq;
+  static_assert(SLAB == 128 && NS == 2 && GPS == 4 && BM * 2 == 512 && BN * 2 == 512 && RPI == 8,
+                "slab geometry: 64 k of 256 rows, or 64 k-rows of 256 columns");
 
-  // Direct global -> LDS loads.  A wave instruction fills RPI consecutive
-  // tile rows (1 KB); lane l writes row r0 + l / CPR at position l % CPR and
-  // therefore fetches k-chunk (l % CPR) ^ key(row): LDS row r holds chunk c at
-  // position c ^ key(r), key(r) = (r >> SH) & (CPR - 1), which spreads the 32
-  // rows of a fragment read over all banks.
-  const char* pa[NLP];
-  const char* qa[NLQ];
+  // ---- operand slabs ---------------------------------------------------------
+  // A slab holds 64 consecutive k of the tile's 256 rows of P (and of Q), in
+  // one of two geometries:
+  //  - direct: 256 rows of 128 bytes (k contiguous), for an operand stored
+  //    row-major over k;
+  //  - transposed: 64 rows k of 512 bytes (the tile's rows contiguous), for
+  //    an operand stored K x rows, read back with ds_read_b64_tr_b16.
+  // Mode 0 reads every slab direct; mode 2 (Q only) every slab transposed:
+  // the update products read X itself as their second operand.  Mode 1 is
+  // the symmetric matrices A and B stored as their upper-triangle 256 x 256
+  // tiles only: rows of tile-row b below the diagonal block (k < 256 b) are
+  // columns of the stored tile (k-block, b), read transposed.
+  const int nk = ga.k_slabs;
+  const int p_tr_end = ga.p_mode == 1 ? bm * (BM / 64) : 0;   // slabs [0, p_tr_end) transposed
+  const int q_tr_end = ga.q_mode == 2 ? nk : (ga.q_mode == 1 ? bn * (BN / 64) : 0);
+  constexpr bool QTR = EPI == EPI_UPDATE || FINAL;           // update products: Q always transposed
+  constexpr bool CAN_PT = EPI != EPI_GRAM, CAN_QT = EPI != EPI_GRAM, CAN_QD = !QTR;
+  const char* const Pm = ga.P + mat * ga.p_mat;
+  const char* const Qm = ga.Q + mat * ga.q_mat;
+  const char* const Pd = Pm + static_cast<int64_t>(bm) * BM * ga.ldp;   // + ks * SLAB
+  const char* const Qd = Qm + static_cast<int64_t>(bn) * BN * ga.ldq;
+  const char* const Pt = Pm + bm * BM * 2;                               // + ks * 64 * ld
+  const char* const Qt = Qm + bn * BN * 2;
+
+  // Loads: a wave instruction fills 1 KB of the stage (8 direct rows or 2
+  // transposed rows); lane l writes 16 bytes at 16 l and fetches the chunk
+  // that belongs there.  Direct: LDS row r holds k-chunk c at position
+  // c ^ ((r >> 1) % 8), which spreads the 32 rows of a fragment read over all
+  // 64 banks.  Transposed: row k holds 16-byte chunk c at position
+  // c ^ 4*(k % 4).  Per-lane offsets are 32-bit, added to a wave-uniform base.
+  uint32_t pdo[NLP], pto[NLP], qdo[NLQ], qto[NLQ];
 #pragma unroll
   for (int i = 0; i < NLP; ++i) {
     const int r = wave * PR + RPI * i + lane / CPR;
-    pa[i] = Pb + static_cast<int64_t>(r) * ga.ldp + ((lane % CPR) ^ ((r >> SH) & (CPR - 1))) * 16;
+    pdo[i] = static_cast<uint32_t>(r * ga.ldp + ((lane % CPR) ^ ((r >> SH) & (CPR - 1))) * 16);
+    const int t = wave * (2 * NLP) + 2 * i + lane / 32;
+    pto[i] = static_cast<uint32_t>(t * ga.ldp + ((lane % 32) ^ ((t & 3) << 2)) * 16);
   }
 #pragma unroll
   for (int i = 0; i < NLQ; ++i) {
-    if (QTR) {
-      // Q slab = 64 rows k of 512 bytes (256 columns n); a wave instruction
-      // fills 2 rows.  16-byte chunk c of row k sits at position c ^ 4*(k % 4).
-      const int r = wave * (NLQ * 2) + 2 * i + lane / 32;
-      qa[i] = Qb + static_cast<int64_t>(r) * ga.ldq + ((lane % 32) ^ ((r & 3) << 2)) * 16;
-    } else {
-      const int r = wave * QR + RPI * i + lane / CPR;
-      qa[i] = Qb + static_cast<int64_t>(r) * ga.ldq + ((lane % CPR) ^ ((r >> SH) & (CPR - 1))) * 16;
-    }
+    const int r = wave * QR + RPI * i + lane / CPR;
+    qdo[i] = static_cast<uint32_t>(r * ga.ldq + ((lane % CPR) ^ ((r >> SH) & (CPR - 1))) * 16);
+    const int t = wave * (2 * NLQ) + 2 * i + lane / 32;
+    qto[i] = static_cast<uint32_t>(t * ga.ldq + ((lane % 32) ^ ((t & 3) << 2)) * 16);
   }
   const uint32_t lds0 = lds_offset(smem);
   auto issue = [&](int ks) {
-    const uint32_t base = lds0 + (ks % NS) * STAGE;
-    const int64_t ko = static_cast<int64_t>(ks) * SLAB;
-    const int64_t kq = QTR ? static_cast<int64_t>(ks) * 64 * ga.ldq : ko;
+    const uint32_t base = lds0 + (ks & 1) * STAGE;
+    if (CAN_PT && ks < p_tr_end) {
+      const char* b = Pt + static_cast<int64_t>(ks) * 64 * ga.ldp;
 #pragma unroll
-    for (int i = 0; i < NLP; ++i) load_lds16(pa[i] + ko, base + (wave * PR + RPI * i) * SLAB);
+      for (int i = 0; i < NLP; ++i) load_lds16(b, pto[i], base + (wave * PR + RPI * i) * SLAB);
+    } else {
+      const char* b = Pd + ks * SLAB;
 #pragma unroll
-    for (int i = 0; i < NLQ; ++i) load_lds16(qa[i] + kq, base + OPQ + (wave * QR + RPI * i) * SLAB);
+      for (int i = 0; i < NLP; ++i) load_lds16(b, pdo[i], base + (wave * PR + RPI * i) * SLAB);
+    }
+    if (CAN_QT && (!CAN_QD || ks < q_tr_end)) {
+      const char* b = Qt + static_cast<int64_t>(ks) * 64 * ga.ldq;
+#pragma unroll
+      for (int i = 0; i < NLQ; ++i) load_lds16(b, qto[i], base + OPQ + (wave * QR + RPI * i) * SLAB);
+    } else {
+      const char* b = Qd + ks * SLAB;
+#pragma unroll
+      for (int i = 0; i < NLQ; ++i) load_lds16(b, qdo[i], base + OPQ + (wave * QR + RPI * i) * SLAB);
+    }
   };
 
   f32x16_t acc[BI][BJ];
@@ -763,125 +790,125 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // fragment addressing: row (..+ lane%32), chunk (2*grp + lane/32) at position chunk ^ key(row)
+  // Fragments.  Direct: row (.. + lane % 32), k-chunk 2*grp + lane / 32 at its
+  // swizzled position, one ds_read_b128.  Transposed: ds_read_b64_tr_b16
+  // hands lane t of each 16-lane group G, as its r-th element, element t % 4
+  // of the 8 bytes addressed by lane 4r + t / 4 of the group.  Lane L of
+  // group G therefore addresses row 16*grp + 8*(G/2) + 4*h + L/4, columns
+  // c0 + 16*(G%2) + 4*(L%4) .. +3, and two reads (h = 0, 1) give the 8
+  // consecutive k of column c0 + lane % 32 that the MFMA takes.  The 4 rows k
+  // of one read differ in k % 4, so the swizzle spreads them over all banks.
   const int frow = lane & 31, fsel = lane >> 5, fsw = (frow >> SH) & (CPR - 1);
   const int a_off = (wm * (BM / WM) + frow) * SLAB;
   const int b_off = OPQ + (wn * (BN / WN) + frow) * SLAB;
-  // QTR fragments: ds_read_b64_tr_b16 hands lane t of each 16-lane group G,
-  // as its r-th element, element t % 4 of the 8 bytes addressed by lane
-  // 4r + t / 4 of the group.  Lane L of group G therefore addresses row
-  // 16*grp + 8*(G/2) + 4*h + L/4, columns n0 + 16*(G%2) + 4*(L%4) .. +3, and
-  // two reads (h = 0, 1) give the 8 consecutive k of column n0 + lane % 32
-  // that the MFMA takes.  Rows k and k + 8 share a bank group; the swizzle
-  // (k % 4) spreads the 4 rows of a read over all 64 banks.
-  int tq_off[BJ];
-#pragma unroll
-  for (int j = 0; j < BJ; ++j) {
+  auto tr_off = [&](int c0) {
     const int G = lane >> 4, L = lane & 15;
     const int row = 8 * (G >> 1) + (L >> 2);
-    const int cb = 2 * (wn * (BN / WN) + j * 32) + 32 * (G & 1) + 8 * (L & 3);
-    tq_off[j] = OPQ + row * 512 + (cb ^ ((L >> 2) << 6));
-  }
+    const int cb = 2 * c0 + 32 * (G & 1) + 8 * (L & 3);
+    return row * 512 + (cb ^ ((L >> 2) << 6));
+  };
+  int tpo[BI], tqo[BJ];
+#pragma unroll
+  for (int i = 0; i < BI; ++i) tpo[i] = tr_off(wm * (BM / WM) + i * 32);
+#pragma unroll
+  for (int j = 0; j < BJ; ++j) tqo[j] = OPQ + tr_off(wn * (BN / WN) + j * 32);
 
-  const int nk = ga.k_slabs;
+  // Software pipeline: the fragments of group g+1 are read into the other
+  // register set while group g's MFMAs issue, one LDS read between
+  // consecutive MFMAs; the slab barrier sits before the last group's MFMAs.
+  u32x4_t fa[2][BI], fb[2][BJ];
+  auto rd = [&](auto ptc, auto qtc, const char* sp, auto grpc, auto setc) {
+    constexpr bool PT = decltype(ptc)::value, QT = decltype(qtc)::value;
+    constexpr int grp = decltype(grpc)::value, set = decltype(setc)::value;
+    const int pos = ((2 * grp + fsel) ^ fsw) * 16;
 #pragma unroll
-  for (int s = 0; s < D; ++s)
-    if (s < nk) issue(s);
-  if constexpr (D == 1)
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  else
-    wait_slabs_in_flight<LPS>(min(D, nk) - 1);
-  __syncthreads();
-#ifndef MUON_SCHED
-#define MUON_SCHED 1
-#endif
-  if constexpr (MUON_SCHED && D == 1 && GPS == 4) {
-    // Software pipeline with explicit interleaving: the fragments of group
-    // g+1 are read into the other register set while group g's MFMAs issue,
-    // one LDS read between consecutive MFMAs; the slab barrier sits before
-    // the last group's MFMAs.
-    u32x4_t fa[2][BI], fb[2][BJ];
-    auto rd = [&](const char* sp, int grp, int set) {
-      const int pos = ((2 * grp + fsel) ^ fsw) * 16;
-#pragma unroll
-      for (int i = 0; i < BI; ++i) fa[set][i] = *reinterpret_cast<const u32x4_t*>(sp + a_off + i * 32 * SLAB + pos);
-#pragma unroll
-      for (int j = 0; j < BJ; ++j) {
-        if (QTR) {
-          const char* q = sp + tq_off[j] + grp * 16 * 512;
-          const uint2 lo = tr_read_b64(q), hi = tr_read_b64(q + 4 * 512);
-          fb[set][j] = u32x4_t{lo.x, lo.y, hi.x, hi.y};
-        } else {
-          fb[set][j] = *reinterpret_cast<const u32x4_t*>(sp + b_off + j * 32 * SLAB + pos);
-        }
+    for (int i = 0; i < BI; ++i) {
+      if (PT) {
+        const char* q = sp + tpo[i] + grp * 16 * 512;
+        const uint2 lo = tr_read_b64(q), hi = tr_read_b64(q + 4 * 512);
+        fa[set][i] = u32x4_t{lo.x, lo.y, hi.x, hi.y};
+      } else {
+        fa[set][i] = *reinterpret_cast<const u32x4_t*>(sp + a_off + i * 32 * SLAB + pos);
       }
-    };
-    auto mm = [&](int set) {
-      static_for<BI>([&](auto I) {
-        static_for<BJ>([&](auto J) { Mma<uint16_t>::run(fa[set][I.value], fb[set][J.value], acc[I.value][J.value]); });
-      });
-    };
-    constexpr int NRD = BI + (QTR ? 2 : 1) * BJ;  // LDS reads per group
+    }
+#pragma unroll
+    for (int j = 0; j < BJ; ++j) {
+      if (QT) {
+        const char* q = sp + tqo[j] + grp * 16 * 512;
+        const uint2 lo = tr_read_b64(q), hi = tr_read_b64(q + 4 * 512);
+        fb[set][j] = u32x4_t{lo.x, lo.y, hi.x, hi.y};
+      } else {
+        fb[set][j] = *reinterpret_cast<const u32x4_t*>(sp + b_off + j * 32 * SLAB + pos);
+      }
+    }
+  };
+  auto mm = [&](auto setc) {
+    constexpr int set = decltype(setc)::value;
+    static_for<BI>([&](auto I) {
+      static_for<BJ>([&](auto J) { Mma<uint16_t>::run(fa[set][I.value], fb[set][J.value], acc[I.value][J.value]); });
+    });
+  };
+  auto interleave = [&](auto ptc, auto qtc) {
+    constexpr int NRD = (decltype(ptc)::value ? 2 : 1) * BI + (decltype(qtc)::value ? 2 : 1) * BJ;
     constexpr int NPAIR = NRD < BI * BJ ? NRD : BI * BJ;
-    auto interleave = [&]() {
 #pragma unroll
-      for (int i = 0; i < NPAIR; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
-      }
-      if constexpr (BI * BJ > NPAIR) __builtin_amdgcn_sched_group_barrier(0x008, BI * BJ - NPAIR, 0);
-      if constexpr (NRD > NPAIR) __builtin_amdgcn_sched_group_barrier(0x100, NRD - NPAIR, 0);
-    };
-#ifndef MUON_PRIO
-#define MUON_PRIO 0
-#endif
-    if (MUON_PRIO == 2 && (wave & 4)) __builtin_amdgcn_s_setprio(1);
-    rd(smem, 0, 0);
-    for (int ks = 0; ks < nk; ++ks) {
-      const char* sp = smem + (ks & 1) * STAGE;
-      if (MUON_PRIO == 1) __builtin_amdgcn_s_setprio(0);
-      if (ks + 1 < nk) issue(ks + 1);
-      if (MUON_PRIO == 1) __builtin_amdgcn_s_setprio(1);
-      __builtin_amdgcn_sched_barrier(0);
-      rd(sp, 1, 1); mm(0); interleave();
-      __builtin_amdgcn_sched_barrier(0);
-      rd(sp, 2, 0); mm(1); interleave();
-      __builtin_amdgcn_sched_barrier(0);
-      rd(sp, 3, 1); mm(0); interleave();
-      __builtin_amdgcn_sched_barrier(0);
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      __syncthreads();
-      rd(smem + ((ks + 1) & 1) * STAGE, 0, 0);  // next slab (unused after the last)
-      mm(1); interleave();
-      __builtin_amdgcn_sched_barrier(0);
+    for (int i = 0; i < NPAIR; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
     }
-    if (MUON_PRIO) __builtin_amdgcn_s_setprio(0);
-  } else {
-  static_assert(!QTR, "QTR fragments are read by the interleaved main loop only");
-  for (int ks = 0; ks < nk; ++ks) {
-    if (ks + D < nk) issue(ks + D);
-    const char* sp = smem + (ks % NS) * STAGE;
-#pragma unroll
-    for (int grp = 0; grp < GPS; ++grp) {
-      const int pos = ((2 * grp + fsel) ^ fsw) * 16;
-      u32x4_t a[BI], b[BJ];
-#pragma unroll
-      for (int i = 0; i < BI; ++i)
-        a[i] = *reinterpret_cast<const u32x4_t*>(sp + a_off + i * 32 * SLAB + pos);
-#pragma unroll
-      for (int j = 0; j < BJ; ++j)
-        b[j] = *reinterpret_cast<const u32x4_t*>(sp + b_off + j * 32 * SLAB + pos);
-      static_for<BI>([&](auto I) {
-        static_for<BJ>([&](auto J) { Mma<uint16_t>::run(a[I.value], b[J.value], acc[I.value][J.value]); });
-      });
-    }
-    // slab ks+1 must have landed; later slabs may still be in flight
-    if constexpr (D == 1)
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    else
-      wait_slabs_in_flight<LPS>(min(nk - 1, ks + D) - (ks + 1));
+    if constexpr (BI * BJ > NPAIR) __builtin_amdgcn_sched_group_barrier(0x008, BI * BJ - NPAIR, 0);
+    if constexpr (NRD > NPAIR) __builtin_amdgcn_sched_group_barrier(0x100, NRD - NPAIR, 0);
+  };
+  // One slab in mode (PT, QT); group 0's fragments are already in set 0.
+  // With NEXT, the fragments of the next slab's group 0 (same mode) are read
+  // while the last group's MFMAs issue; without, the last group runs alone
+  // (the slab before a change of mode, and the last one).
+  auto slab = [&](auto ptc, auto qtc, auto nextc, int ks) {
+    const char* sp = smem + (ks & 1) * STAGE;
+    if (ks + 1 < nk) issue(ks + 1);
+    __builtin_amdgcn_sched_barrier(0);
+    rd(ptc, qtc, sp, I_<1>{}, I_<1>{}); mm(I_<0>{}); interleave(ptc, qtc);
+    __builtin_amdgcn_sched_barrier(0);
+    rd(ptc, qtc, sp, I_<2>{}, I_<0>{}); mm(I_<1>{}); interleave(ptc, qtc);
+    __builtin_amdgcn_sched_barrier(0);
+    rd(ptc, qtc, sp, I_<3>{}, I_<1>{}); mm(I_<0>{}); interleave(ptc, qtc);
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // slab ks + 1 has landed
     __syncthreads();
-  }
+    if constexpr (decltype(nextc)::value) {
+      rd(ptc, qtc, smem + ((ks + 1) & 1) * STAGE, I_<0>{}, I_<0>{});
+      mm(I_<1>{}); interleave(ptc, qtc);
+    } else {
+      mm(I_<1>{});
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // Slabs [a, b) in one mode.  Each run starts from a published slab and
+  // ends with the next one published, so runs chain without carrying
+  // fragments across a change of mode (which happens at most twice a tile).
+  auto run = [&](auto ptc, auto qtc, int a, int b) {
+    if (a >= b) return;
+    rd(ptc, qtc, smem + (a & 1) * STAGE, I_<0>{}, I_<0>{});
+    for (int ks = a; ks < b - 1; ++ks) slab(ptc, qtc, std::true_type{}, ks);
+    slab(ptc, qtc, std::false_type{}, b - 1);
+  };
+  using T_ = std::true_type;
+  using F_ = std::false_type;
+  issue(0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  // Mode runs: P transposed for [0, p_tr_end), Q for [0, q_tr_end).  The
+  // launches keep p_tr_end <= q_tr_end (GRAM none, POLY bm <= bn, update
+  // products Q transposed throughout).
+  if constexpr (EPI == EPI_GRAM) {
+    run(F_{}, F_{}, 0, nk);
+  } else if constexpr (QTR) {
+    run(T_{}, T_{}, 0, p_tr_end);
+    run(F_{}, T_{}, p_tr_end, nk);
+  } else {
+    run(T_{}, T_{}, 0, p_tr_end);
+    run(F_{}, T_{}, p_tr_end, q_tr_end);
+    run(F_{}, F_{}, max(p_tr_end, q_tr_end), nk);
   }
 
   // ---- epilogue from registers ----------------------------------------------
@@ -950,8 +977,9 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
     return;
   }
 
-  // the symmetric products also write the mirrored tile, staged through LDS
-  constexpr bool stage_t = !QTR;
+  // the symmetric products also write the mirrored tile, staged through LDS,
+  // unless their consumers read the upper triangle only (CT null)
+  const bool stage_t = !QTR && ga.CT != nullptr;
   if (stage_t) __syncthreads();               // every wave is done with the operand slabs
   // (The loads and the per-block work sit in one lambda: inlined that way the
   // compiler keeps every value in registers; written at function scope it
@@ -1015,7 +1043,7 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
     });
   };
   blocks();
-  if constexpr (stage_t) {
+  if (stage_t) {
     __syncthreads();
     // transposed tile rows (BM bf16 = BM*2 bytes each) -> CT, 16 bytes a thread
     constexpr int CH = BM * 2 / 16;
@@ -1230,7 +1258,10 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
     g.k_slabs = cg.L * es / 128;
     g.tiles_m = ts; g.tiles_n = ts; g.syrk = 1; g.tiles_per_mat = ts * (ts + 1) / 2;
     g.C = static_cast<char*>(wb.A); g.c_mat = matA; g.ldc = cg.S * es;
-    g.CT = g.C; g.ct_mat = matA; g.ldct = g.ldc;
+    // Under qtr every consumer of A and B runs on the 256 x 256 kernel and
+    // reads them as upper-triangle tiles (mode 1): no mirrored tile is
+    // written.  Otherwise the lower triangle is written as the mirror.
+    if (!qtr) { g.CT = g.C; g.ct_mat = matA; g.ldct = g.ldc; }
     {
       Timed tm(timer, KK_GRAM, st);
       if ((e = launch_gemm<XT>(EPI_GRAM, g, nmat, st)) != hipSuccess) return e;
@@ -1243,7 +1274,8 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
     p.k_slabs = cg.S * es / 128;
     p.E = p.P; p.e_mat = matA; p.lde = p.ldp;
     p.ET = p.P; p.et_mat = matA; p.ldet = p.ldp;  // A is symmetric
-    p.C = static_cast<char*>(wb.B); p.CT = p.C;
+    p.C = static_cast<char*>(wb.B); p.CT = qtr ? nullptr : p.C;
+    p.p_mode = p.q_mode = qtr ? 1 : 0;
     p.alpha = b; p.beta = c;
     {
       Timed tm(timer, KK_POLY, st);
@@ -1256,6 +1288,8 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
     u.P = static_cast<const char*>(wb.B); u.p_mat = matA; u.ldp = cg.S * es;
     if (qtr) {
       u.Q = X; u.q_mat = matX; u.ldq = cg.L * es;
+      u.p_mode = 1;  // B: upper-triangle tiles
+      u.q_mode = 2;  // X: K x N
     } else {
       u.Q = XTc; u.q_mat = matX; u.ldq = cg.S * es;
     }
