@@ -203,6 +203,17 @@ def main():
         if tr.get("kernel_source_sha") == kernel_source_sha() and tr.get("kernel") == dom:
             roof["traffic"] = tr.get("hbm_bytes_per_launch")
 
+    # The Newton-Schulz contractions alone: dense flops (Eq. 1 count) and the
+    # MFMA work the kernels execute (upper tiles of the symmetric products,
+    # padded extents), over the summed kernel time.
+    gemm_names = [k for k in ("gram_syrk", "poly_syrk", "update_gemm", "update_apply_gemm") if k in stats]
+    g_ms = sum(stats[k]["total_ms"] for k in gemm_names) / args.steps
+    g_exec = sum(stats[k]["exec_flops"] for k in gemm_names) / args.steps
+    ns_gemm = {"ms_per_step": g_ms,
+               "dense_tflops": ns_flops / (g_ms * 1e-3) / 1e12,
+               "dense_pct_peak": 100.0 * ns_flops / (g_ms * 1e-3) / 1e12 / peak,
+               "executed_tflops": g_exec / (g_ms * 1e-3) / 1e12,
+               "executed_pct_peak": 100.0 * g_exec / (g_ms * 1e-3) / 1e12 / peak}
     out = {
         "metric": METRIC, "value": n_mat / (ms * 1e-3), "unit": "matrices/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
@@ -216,6 +227,7 @@ def main():
                    "momentum_dtype": "f32", "parallelism": "none (one GPU)"},
         "ns_tflops": ns_flops / (ms * 1e-3) / 1e12,
         "ns_pct_peak": 100.0 * ns_flops / (ms * 1e-3) / 1e12 / peak,
+        "ns_gemm": ns_gemm,
         "roofline": roof,
         "kernels": kernels,
         "input_generation_s": gen_s,

@@ -863,9 +863,15 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   // With NEXT, the fragments of the next slab's group 0 (same mode) are read
   // while the last group's MFMAs issue; without, the last group runs alone
   // (the slab before a change of mode, and the last one).
+  // When a slab's loads are issued: right after the barrier that frees its
+  // stage (a whole slab of MFMA work ahead of the barrier that publishes it;
+  // measured faster for the Gram product, whose long K streams the most
+  // operand data), or at the top of the slab before it (3/4 of a slab ahead;
+  // measured faster for the other products).
+  constexpr bool EARLY = EPI == EPI_GRAM;
   auto slab = [&](auto ptc, auto qtc, auto nextc, int ks) {
     const char* sp = smem + (ks & 1) * STAGE;
-    if (ks + 1 < nk) issue(ks + 1);
+    if (!EARLY && ks + 1 < nk) issue(ks + 1);
     __builtin_amdgcn_sched_barrier(0);
     rd(ptc, qtc, sp, I_<1>{}, I_<1>{}); mm(I_<0>{}); interleave(ptc, qtc);
     __builtin_amdgcn_sched_barrier(0);
@@ -875,6 +881,9 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
     __builtin_amdgcn_sched_barrier(0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // slab ks + 1 has landed
     __syncthreads();
+    // every wave is done with slab ks: its stage can take slab ks + 2
+    if (EARLY && ks + 2 < nk) issue(ks + 2);
+    __builtin_amdgcn_sched_barrier(0);
     if constexpr (decltype(nextc)::value) {
       rd(ptc, qtc, smem + ((ks + 1) & 1) * STAGE, I_<0>{}, I_<0>{});
       mm(I_<1>{}); interleave(ptc, qtc);
@@ -894,8 +903,14 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   };
   using T_ = std::true_type;
   using F_ = std::false_type;
+  static_assert(NLP + NLQ == 8, "slab 0 wait below counts 8 load instructions per slab");
   issue(0);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  if (EARLY && nk > 1) {
+    issue(1);
+    asm volatile("s_waitcnt vmcnt(8)" ::: "memory");  // slab 0 has landed, slab 1 may not
+  } else {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
   __syncthreads();
   // Mode runs: P transposed for [0, p_tr_end), Q for [0, q_tr_end).  The
   // launches keep p_tr_end <= q_tr_end (GRAM none, POLY bm <= bn, update
@@ -1244,8 +1259,13 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
   const int64_t matX = static_cast<int64_t>(cg.S) * cg.L * es;
   const int64_t matA = static_cast<int64_t>(cg.S) * cg.S * es;
   const int ts = cg.S / kTile, tl = cg.L / kTile;
-  // flops the symmetric products issue: upper tiles only, on the real extent
-  const double syrk_frac = double(ts * (ts + 1) / 2) / double(ts * ts);
+  // Work accounting: `flops` is the dense count of each product on the real
+  // extents (Eq. 1); `exec` is what the MFMAs execute: padded extents, and
+  // for the symmetric products the upper tiles of the kernel that runs them
+  // (256 x 256 tiles when bf16 and S is a multiple of 256, else 128 x 128).
+  const int tsy = (sizeof(XT) == 2 && cg.S % 256 == 0) ? cg.S / 256 : ts;
+  const double syrk_frac = double(tsy * (tsy + 1) / 2) / double(tsy * tsy);
+  const double Sp = cg.S, Lp = cg.L;
   int cur = 0;
   for (int k = 0; k < K; ++k) {
     const float a = coeffs[3 * k], b = coeffs[3 * k + 1], c = coeffs[3 * k + 2];
@@ -1265,7 +1285,7 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
     {
       Timed tm(timer, KK_GRAM, st);
       if ((e = launch_gemm<XT>(EPI_GRAM, g, nmat, st)) != hipSuccess) return e;
-      tm.done(nm * 2 * s * s * l, nm * 2 * s * s * l * syrk_frac, nm * (s * l + s * s) * xsz);
+      tm.done(nm * 2 * s * s * l, nm * 2 * Sp * Sp * Lp * syrk_frac, nm * (s * l + s * s) * xsz);
     }
     // B = b A + c A A^T: M = N = K = S.
     GemmArgs p = g;
@@ -1280,7 +1300,7 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
     {
       Timed tm(timer, KK_POLY, st);
       if ((e = launch_gemm<XT>(EPI_POLY, p, nmat, st)) != hipSuccess) return e;
-      tm.done(nm * 2 * s * s * s, nm * 2 * s * s * s * syrk_frac, nm * 2 * s * s * xsz);
+      tm.done(nm * 2 * s * s * s, nm * 2 * Sp * Sp * Sp * syrk_frac, nm * 2 * s * s * xsz);
     }
     // X' = a X + B X: M = S, N = L, K = S.  The second operand is X^T (N x K,
     // K contiguous) on the 128 x 128 kernel, X itself (K x N) under qtr.
@@ -1298,7 +1318,7 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
     u.E = X; u.e_mat = matX; u.lde = cg.L * es;
     u.alpha = a;
     u.s = cg.s; u.l = cg.l;
-    const double uf = nm * 2 * s * s * l;
+    const double uf = nm * 2 * s * s * l, ufx = nm * 2 * Sp * Sp * Lp;
     if (k + 1 < K) {
       u.C = static_cast<char*>(wb.X[cur ^ 1]); u.c_mat = matX; u.ldc = cg.L * es;
       if (!qtr) { u.CT = static_cast<char*>(wb.XT[cur ^ 1]); u.ct_mat = matX; u.ldct = cg.S * es; }
@@ -1307,7 +1327,7 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
           hipSuccess)
         return e;
       // reads B, X (twice under qtr, else X^T and X); writes X' (and X'^T)
-      tm.done(uf, uf, nm * (s * s + (qtr ? 3 : 4) * s * l) * xsz);
+      tm.done(uf, ufx, nm * (s * s + (qtr ? 3 : 4) * s * l) * xsz);
       cur ^= 1;
     } else {
       u.desc = d_desc; u.final_kind = sc.final_kind; u.param_dtype = cg.param_dtype;
@@ -1316,7 +1336,7 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
           hipSuccess)
         return e;
       // reads B, X^T, X (and W); writes W or out
-      tm.done(uf, uf, nm * ((s * s + 2 * s * l) * xsz + s * l * (sc.final_kind == 0 ? 2 * psz : psz)));
+      tm.done(uf, ufx, nm * ((s * s + 2 * s * l) * xsz + s * l * (sc.final_kind == 0 ? 2 * psz : psz)));
     }
   }
   return hipSuccess;

@@ -81,6 +81,41 @@ def test_muon_step_matches_oracle(muon, pdt, gdt, prec, nesterov):
         assert rel(to_host(b_dev), r.buf_new) <= MOMENTUM_TOL, s
 
 
+# Padded extents that are multiples of 256 on both sides take the 256 x 256
+# path with upper-triangle storage of A and B (read back transposed below the
+# diagonal) and X read through transposing LDS reads.  Several tile rows, so
+# every operand mode and mode change occurs; one transposed parameter.
+UPPER_SHAPES = [(512, 1024), (1024, 512), (768, 768), (500, 1200)]
+
+
+def test_upper_tile_path_step_matches_oracle(muon):
+    import torch
+    hp = ref.MuonHParams(lr=0.02, beta=0.95, weight_decay=0.01, nesterov=True)
+    Ws = [gen(s, 0.02, "bf16", 20, i, 0) for i, s in enumerate(UPPER_SHAPES)]
+    gs = [gen(s, 1e-3, "bf16", 20, i, 1) for i, s in enumerate(UPPER_SHAPES)]
+    bs = [gen(s, 1e-3, "f32", 20, i, 2) for i, s in enumerate(UPPER_SHAPES)]
+    dW = [to_dev(w, "bf16") for w in Ws]
+    dg = [to_dev(g, "bf16") for g in gs]
+    db = [to_dev(b, "f32") for b in bs]
+    muon.step(dW, dg, db, lr=hp.lr, beta=hp.beta, weight_decay=hp.weight_decay, ns_precision="bf16")
+    torch.cuda.synchronize()
+    for s, W, g, b, w_dev, b_dev in zip(UPPER_SHAPES, Ws, gs, bs, dW, db):
+        W0 = decode(W, "bf16")
+        r = ref.muon_step_matrix(W0, decode(g, "bf16"), np.asarray(b, np.float64), hp)
+        err, rho = w_gate(to_host(w_dev), r.W_new, W0, "bf16")
+        print(f"upper-tile path {s}: W err {err:.3e} (rho {rho:.1e})", flush=True)
+        assert err <= tol_for("bf16", s) + rho, (s, err, rho)
+        assert rel(to_host(b_dev), r.buf_new) <= MOMENTUM_TOL, s
+
+
+def test_upper_tile_path_orthogonalize_matches_oracle(muon):
+    G, outs = run_orth(muon, UPPER_SHAPES, "bf16", "bf16", key=21)
+    for s, g, o in zip(UPPER_SHAPES, G, outs):
+        want = ref.orthogonalize(decode(g, "bf16"), 5)
+        err, rho = o_gate(to_host(o), want, "bf16")
+        assert err <= tol_for("bf16", s) + rho, (s, err, rho)
+
+
 def test_fp32_step_recovers_orthogonalised_update(muon):
     # fp32 parameters: O = (decay*W - W') / (lr*scale) is checked at 1e-4.
     import torch
@@ -185,18 +220,19 @@ def _step_bits(muon, shapes, dtypes=("bf16", "bf16"), prec="bf16", key=10, **kw)
     return [to_bits(t) for t in dW], [to_bits(t) for t in db]
 
 
-def test_deterministic_repeat(muon):
-    shapes = [(256, 384), (384, 256), (200, 200)]
+@pytest.mark.parametrize("shapes", [[(256, 384), (384, 256), (200, 200)], UPPER_SHAPES])
+def test_deterministic_repeat(muon, shapes):
     a = _step_bits(muon, shapes)
     b = _step_bits(muon, shapes)
     for x, y in zip(a[0] + a[1], b[0] + b[1]):
         np.testing.assert_array_equal(x, y)
 
 
-def test_batched_equals_single(muon):
+@pytest.mark.parametrize("shapes", [[(256, 384), (384, 256), (200, 200), (256, 384)],
+                                    [(512, 1024), (768, 768), (1024, 512), (512, 1024)]])
+def test_batched_equals_single(muon, shapes):
     # a matrix's bits do not depend on which other matrices share the call
     import torch
-    shapes = [(256, 384), (384, 256), (200, 200), (256, 384)]
     together = _step_bits(muon, shapes)
     for i, s in enumerate(shapes):
         dW = to_dev(gen(s, 0.02, "bf16", 10, i, 0), "bf16")
