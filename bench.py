@@ -52,6 +52,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this size (HBM counter calibration)")
+    ap.add_argument("--reference-gemm", action="store_true",
+                    help="instead of the step, time torch.matmul (the vendor bf16 GEMM) on the "
+                         "workload's update shapes and a plain device copy, as context for the roofline")
     return ap.parse_args()
 
 
@@ -116,6 +119,48 @@ def cpu_baseline(wl, inputs):
                        f"{len(wl.matrices)} matrices; {cores} BLAS threads on {cpu}")}
 
 
+def reference_gemm(wl):
+    """Vendor-library context on the same GPU: torch.matmul (hipBLASLt) for
+    the update product B(s x s) @ X(s x l) of each shape bucket, batched over
+    the bucket's matrices, and the rate of a plain 4 GiB device copy."""
+    import torch
+    shapes = sorted({(min(m.rows, m.cols), max(m.rows, m.cols)) for m in wl.matrices})
+    out = {"kind": "vendor reference", "gemm": [], "copy": None}
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    for s_, l_ in shapes:
+        n = sum(1 for m in wl.matrices if (min(m.rows, m.cols), max(m.rows, m.cols)) == (s_, l_))
+        a = torch.randn(n, s_, s_, device="cuda", dtype=torch.bfloat16)
+        b = torch.randn(n, s_, l_, device="cuda", dtype=torch.bfloat16)
+        for _ in range(3):
+            torch.bmm(a, b)
+        torch.cuda.synchronize()
+        e0, e1 = ev(), ev()
+        e0.record()
+        for _ in range(10):
+            torch.bmm(a, b)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / 10
+        tf = n * 2.0 * s_ * s_ * l_ / (ms * 1e-3) / 1e12
+        out["gemm"].append({"batch": n, "m": s_, "k": s_, "n": l_, "ms": ms, "tflops": tf,
+                            "pct_peak": 100 * tf / PEAK_BF16_TFLOPS})
+        del a, b
+    x = torch.ones(1 << 30, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(3):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    e0, e1 = ev(), ev()
+    e0.record()
+    for _ in range(10):
+        y.copy_(x)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / 10
+    out["copy"] = {"bytes": 2 * 4 * (1 << 30), "ms": ms, "tb_per_s": 2 * 4 * (1 << 30) / (ms * 1e-3) / 1e12}
+    return out
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -131,6 +176,9 @@ def main():
     from paper_2609_21594_amd.binding import Muon
 
     wl = synth.WORKLOADS[args.workload]
+    if args.reference_gemm:
+        print(json.dumps(reference_gemm(wl)), flush=True)
+        return
     if wl.orthogonalize_only:
         raise SystemExit("bench.py times the Muon step; pick a workload with optimizer state")
     t_gen = time.perf_counter()
