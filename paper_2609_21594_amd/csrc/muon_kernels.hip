@@ -934,11 +934,11 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   // cover 64 contiguous bytes of a row.
   //  - The a*X (or A) term is read coalesced in the direct layout and turned
   //    to the natural one while still packed bfloat16.
-  //  - Outputs are rounded to bfloat16 once; the direct copy goes straight to
-  //    memory.  The symmetric products also write the mirrored tile: the
-  //    natural copy goes to an LDS staging area (padded rows) that is written
-  //    out as whole rows of the transposed tile.  X' needs no transposed copy,
-  //    since the next update reads X through transposing LDS reads.
+  //  - Outputs are rounded to bfloat16 once and leave through LDS as whole
+  //    512-byte rows.  When the symmetric products must also write their
+  //    mirrored tile (see below), that one is staged instead and the direct
+  //    copy goes straight to memory.  X' needs no transposed copy, since the
+  //    next update reads X through transposing LDS reads.
   //  - The last step's parameter update runs in the parameter's layout:
   //    direct when it is s x l, natural when it is l x s.
   //  - Every load of the a*X (or A) term is issued before the first store,
@@ -992,10 +992,16 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
     return;
   }
 
-  // the symmetric products also write the mirrored tile, staged through LDS,
-  // unless their consumers read the upper triangle only (CT null)
+  // The symmetric products also write the mirrored tile, staged through LDS,
+  // unless their consumers read the upper triangle only (CT null).  Without
+  // a mirror, the output tile itself is staged through LDS (direct layout,
+  // 576-byte row pitch: 16 banks apart per row) and written out as whole
+  // 512-byte rows, which measured faster than 64-byte row pieces straight
+  // from the registers.
   const bool stage_t = !QTR && ga.CT != nullptr;
-  if (stage_t) __syncthreads();               // every wave is done with the operand slabs
+  const bool stage_c = !FINAL && !stage_t;
+  constexpr int CST = BN * 2 + 64;            // staged direct row, bytes
+  if (stage_t || stage_c) __syncthreads();    // every wave is done with the operand slabs
   // (The loads and the per-block work sit in one lambda: inlined that way the
   // compiler keeps every value in registers; written at function scope it
   // spilled.)
@@ -1032,9 +1038,13 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
             }
             if (!FINAL) {
               const uint2 p = pack_bf16x4(v);
-              if (stage_t) *reinterpret_cast<uint2*>(smem + (col - bn * BN) * TST + (row0 - bm * BM) * 2) = p;
-              store_out(reinterpret_cast<uint2*>(C + static_cast<int64_t>(row0 + q4) * ga.ldc + c0 * 2),
-                        quad_transpose_bf16(p));
+              const uint2 d = quad_transpose_bf16(p);  // row row0 + q4, columns c0 .. c0 + 3
+              if (stage_c) {
+                *reinterpret_cast<uint2*>(smem + (row0 + q4 - bm * BM) * CST + (c0 - bn * BN) * 2) = d;
+              } else {
+                *reinterpret_cast<uint2*>(smem + (col - bn * BN) * TST + (row0 - bm * BM) * 2) = p;
+                store_out(reinterpret_cast<uint2*>(C + static_cast<int64_t>(row0 + q4) * ga.ldc + c0 * 2), d);
+              }
             } else if (col < ga.l) {  // parameter is l x s: elements (col, row0 .. row0 + 3)
               const int n = min(4, ga.s - row0);
               if (n > 0)
@@ -1058,6 +1068,17 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
     });
   };
   blocks();
+  if (stage_c) {
+    __syncthreads();
+    // output tile rows (BN bf16 = 512 bytes each) -> C, 16 bytes a thread
+    constexpr int CH = BN * 2 / 16;
+    for (int idx = threadIdx.x; idx < BM * CH; idx += 64 * NW) {
+      const int r = idx / CH, ch = idx - r * CH;
+      store_out(reinterpret_cast<u32x4_t*>(C + static_cast<int64_t>(bm * BM + r) * ga.ldc + bn * BN * 2 + ch * 16),
+                *reinterpret_cast<const u32x4_t*>(smem + r * CST + ch * 16));
+    }
+    __syncthreads();  // the next tile's loads overwrite the staging area
+  }
   if (stage_t) {
     __syncthreads();
     // transposed tile rows (BM bf16 = BM*2 bytes each) -> CT, 16 bytes a thread
@@ -1083,7 +1104,10 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
 template <int EPI, class Cfg>
 __global__ __launch_bounds__(64 * Cfg::NW) __attribute__((amdgpu_waves_per_eu(Cfg::WPE, Cfg::WPE)))
 void k_gemm_tile(GemmArgs ga) {
-  constexpr int STAGED = Cfg::BN * (Cfg::BM * 2 + 8);  // epilogue staging of a transposed tile
+  // epilogue staging: the output tile (direct rows) or the mirrored tile
+  constexpr int STAGED_C = Cfg::BM * (Cfg::BN * 2 + 64), STAGED_T = Cfg::BN * (Cfg::BM * 2 + 8);
+  constexpr int STAGED = STAGED_C > STAGED_T ? STAGED_C : STAGED_T;
+  static_assert(STAGED <= 160 * 1024, "LDS budget");
   __shared__ __attribute__((aligned(1024))) char smem[Cfg::LDS > STAGED ? Cfg::LDS : STAGED];
   const int G = static_cast<int>(gridDim.x), b = static_cast<int>(blockIdx.x);
   for (int r = 0;; ++r) {
