@@ -994,14 +994,34 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
 
   // The symmetric products also write the mirrored tile, staged through LDS,
   // unless their consumers read the upper triangle only (CT null).  Without
-  // a mirror, the output tile itself is staged through LDS (direct layout,
-  // 576-byte row pitch: 16 banks apart per row) and written out as whole
-  // 512-byte rows, which measured faster than 64-byte row pieces straight
-  // from the registers.
+  // a mirror, the output tile itself goes through LDS (stage_c): the a*X (or
+  // A) tile is loaded into it as whole 512-byte rows by direct-to-LDS loads,
+  // every lane combines its values in place, and the result leaves as whole
+  // rows again, which measured faster than 64-byte row pieces to and from
+  // the registers.  Staged rows are 512 bytes; row r holds 16-byte chunk c at
+  // position c ^ 4*(r % 4), so the 8 rows x 64 bytes a lane instruction
+  // touches spread over all banks.
   const bool stage_t = !QTR && ga.CT != nullptr;
   const bool stage_c = !FINAL && !stage_t;
-  constexpr int CST = BN * 2 + 64;            // staged direct row, bytes
+  auto cpos = [](int r, int b) {  // staged byte position of tile row r, byte b
+    return r * (BN * 2) + ((((b >> 4) ^ ((r & 3) << 2))) << 4) + (b & 15);
+  };
   if (stage_t || stage_c) __syncthreads();    // every wave is done with the operand slabs
+  if (EPI != EPI_GRAM && stage_c) {
+    // a wave instruction fills 2 staged rows (1 KB); lane l: row 2k + l/32,
+    // position l % 32, which holds chunk (l % 32) ^ 4*(row % 4)
+    static_assert(BM * BN * 2 / 1024 == 16 * NW, "E tile: 16 load instructions per wave");
+    const char* eb = E + static_cast<int64_t>(bm) * BM * ga.lde + bn * BN * 2;
+    const uint32_t lds0 = lds_offset(smem);
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int row = 2 * (wave * 16 + k) + lane / 32;
+      const int c = (lane % 32) ^ ((row & 3) << 2);
+      load_lds16(eb, static_cast<uint32_t>(row * ga.lde + c * 16), lds0 + (wave * 16 + k) * 1024);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+  }
   // (The loads and the per-block work sit in one lambda: inlined that way the
   // compiler keeps every value in registers; written at function scope it
   // spilled.)
@@ -1013,7 +1033,7 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
           constexpr int i = decltype(I)::value, j = decltype(J)::value, g = decltype(G)::value;
           const int row0 = row_base + i * 32 + 8 * g;
           const int c0 = col_base + j * 32 - q4;
-          if (EPI != EPI_GRAM)
+          if (EPI != EPI_GRAM && !stage_c)
             ev[i][j][g] = load_once(reinterpret_cast<const uint2*>(E + static_cast<int64_t>(row0 + q4) * ga.lde + c0 * 2));
         });
       });
@@ -1031,7 +1051,9 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
           if (!FINAL || tr) {  // natural layout
             if (EPI != EPI_GRAM) {
               float e[4];
-              unpack_bf16x4(quad_transpose_bf16(ev[i][j][g]), e);
+              const uint2 ed = stage_c ? *reinterpret_cast<const uint2*>(smem + cpos(row0 + q4 - bm * BM, (c0 - bn * BN) * 2))
+                                       : ev[i][j][g];
+              unpack_bf16x4(quad_transpose_bf16(ed), e);
 #pragma unroll
               for (int q = 0; q < 4; ++q)
                 v[q] = EPI == EPI_POLY ? fmaf(ga.alpha, e[q], ga.beta * v[q]) : fmaf(ga.alpha, e[q], v[q]);
@@ -1040,7 +1062,7 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
               const uint2 p = pack_bf16x4(v);
               const uint2 d = quad_transpose_bf16(p);  // row row0 + q4, columns c0 .. c0 + 3
               if (stage_c) {
-                *reinterpret_cast<uint2*>(smem + (row0 + q4 - bm * BM) * CST + (c0 - bn * BN) * 2) = d;
+                *reinterpret_cast<uint2*>(smem + cpos(row0 + q4 - bm * BM, (c0 - bn * BN) * 2)) = d;
               } else {
                 *reinterpret_cast<uint2*>(smem + (col - bn * BN) * TST + (row0 - bm * BM) * 2) = p;
                 store_out(reinterpret_cast<uint2*>(C + static_cast<int64_t>(row0 + q4) * ga.ldc + c0 * 2), d);
@@ -1075,7 +1097,7 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
     for (int idx = threadIdx.x; idx < BM * CH; idx += 64 * NW) {
       const int r = idx / CH, ch = idx - r * CH;
       store_out(reinterpret_cast<u32x4_t*>(C + static_cast<int64_t>(bm * BM + r) * ga.ldc + bn * BN * 2 + ch * 16),
-                *reinterpret_cast<const u32x4_t*>(smem + r * CST + ch * 16));
+                *reinterpret_cast<const u32x4_t*>(smem + cpos(r, ch * 16)));
     }
     __syncthreads();  // the next tile's loads overwrite the staging area
   }
@@ -1105,7 +1127,7 @@ template <int EPI, class Cfg>
 __global__ __launch_bounds__(64 * Cfg::NW) __attribute__((amdgpu_waves_per_eu(Cfg::WPE, Cfg::WPE)))
 void k_gemm_tile(GemmArgs ga) {
   // epilogue staging: the output tile (direct rows) or the mirrored tile
-  constexpr int STAGED_C = Cfg::BM * (Cfg::BN * 2 + 64), STAGED_T = Cfg::BN * (Cfg::BM * 2 + 8);
+  constexpr int STAGED_C = Cfg::BM * Cfg::BN * 2, STAGED_T = Cfg::BN * (Cfg::BM * 2 + 8);
   constexpr int STAGED = STAGED_C > STAGED_T ? STAGED_C : STAGED_T;
   static_assert(STAGED <= 160 * 1024, "LDS budget");
   __shared__ __attribute__((aligned(1024))) char smem[Cfg::LDS > STAGED ? Cfg::LDS : STAGED];
