@@ -1006,7 +1006,32 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   auto cpos = [](int r, int b) {  // staged byte position of tile row r, byte b
     return r * (BN * 2) + ((((b >> 4) ^ ((r & 3) << 2))) << 4) + (b & 15);
   };
-  if (stage_t || stage_c) __syncthreads();    // every wave is done with the operand slabs
+  // The last step with a bfloat16 parameter whose 256 x 256 block lies fully
+  // inside the matrix (and 16-byte rows): W goes through LDS the same way,
+  // loaded and written back as whole 512-byte rows of its own layout.  Its
+  // staged row r holds chunk c at c ^ key(r), key(r) = 4*(r % 4) + (r / 4) % 4,
+  // which spreads both the direct accesses (8 rows x 64 bytes) and the
+  // natural ones (32 rows x 16 bytes) over all banks.
+  bool stage_w = false;
+  if constexpr (FINAL && FK == 0 && PDT == DT_BF16)
+    stage_w = v4 && md->cols % 8 == 0 && (bm + 1) * BM <= ga.s && (bn + 1) * BN <= ga.l;
+  auto wpos = [](int r, int b) {
+    const int key = ((r & 3) << 2) | ((r >> 2) & 3);
+    return r * 512 + (((b >> 4) ^ key) << 4) + (b & 15);
+  };
+  const int wr0 = tr ? bn * BN : bm * BM, wc0 = tr ? bm * BM : bn * BN;  // W block origin
+  if (stage_t || stage_c || stage_w) __syncthreads();  // every wave is done with the operand slabs
+  if (stage_w) {
+    static_assert(BM * BN * 2 / 1024 == 16 * NW, "W tile: 16 load instructions per wave");
+    const char* wb = static_cast<const char*>(md->W) + (static_cast<int64_t>(wr0) * md->cols + wc0) * 2;
+    const uint32_t lds0 = lds_offset(smem);
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int row = 2 * (wave * 16 + k) + lane / 32;
+      const int c = (lane % 32) ^ (((row & 3) << 2) | ((row >> 2) & 3));
+      load_lds16(wb, static_cast<uint32_t>(row * md->cols * 2 + c * 16), lds0 + (wave * 16 + k) * 1024);
+    }
+  }
   if (EPI != EPI_GRAM && stage_c) {
     // a wave instruction fills 2 staged rows (1 KB); lane l: row 2k + l/32,
     // position l % 32, which holds chunk (l % 32) ^ 4*(row % 4)
@@ -1038,6 +1063,18 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
         });
       });
     });
+    if (stage_w) {  // the W block has landed in LDS (and the a*X loads with it)
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+    }
+    const float decay = FINAL ? md->decay : 0.f, upd = FINAL ? md->upd_scale : 0.f;
+    auto w_update = [&](char* p, const float o[4]) {  // 4 staged W values, in place
+      float w[4], r[4];
+      unpack_bf16x4(*reinterpret_cast<const uint2*>(p), w);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) r[q] = fmaf(decay, w[q], -upd * o[q]);
+      *reinterpret_cast<uint2*>(p) = pack_bf16x4(r);
+    };
     static_for<BI>([&](auto I) {
       static_for<BJ>([&](auto J) {
         static_for<4>([&](auto G) {
@@ -1067,7 +1104,9 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
                 *reinterpret_cast<uint2*>(smem + (col - bn * BN) * TST + (row0 - bm * BM) * 2) = p;
                 store_out(reinterpret_cast<uint2*>(C + static_cast<int64_t>(row0 + q4) * ga.ldc + c0 * 2), d);
               }
-            } else if (col < ga.l) {  // parameter is l x s: elements (col, row0 .. row0 + 3)
+            } else if (stage_w) {      // parameter is l x s: elements (col, row0 .. row0 + 3)
+              w_update(smem + wpos(col - wr0, (row0 - wc0) * 2), v);
+            } else if (col < ga.l) {
               const int n = min(4, ga.s - row0);
               if (n > 0)
                 apply4<FK, PDT>(md, static_cast<int64_t>(col) * md->cols + row0, v, v4 && n == 4, n);
@@ -1079,7 +1118,9 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
 #pragma unroll
             for (int q = 0; q < 4; ++q) v[q] = fmaf(ga.alpha, e[q], v[q]);
             const int row = row0 + q4;
-            if (row < ga.s) {
+            if (stage_w) {
+              w_update(smem + wpos(row - wr0, (c0 - wc0) * 2), v);
+            } else if (row < ga.s) {
               const int n = min(4, ga.l - c0);
               if (n > 0)
                 apply4<FK, PDT>(md, static_cast<int64_t>(row) * md->cols + c0, v, v4 && n == 4, n);
@@ -1090,6 +1131,16 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
     });
   };
   blocks();
+  if (stage_w) {
+    __syncthreads();
+    // updated W rows (512 bytes each) -> W, 16 bytes a thread
+    for (int idx = threadIdx.x; idx < BM * 32; idx += 64 * NW) {
+      const int r = idx >> 5, ch = idx & 31;
+      *reinterpret_cast<u32x4_t*>(static_cast<char*>(md->W) + (static_cast<int64_t>(wr0 + r) * md->cols + wc0) * 2 +
+                                  ch * 16) = *reinterpret_cast<const u32x4_t*>(smem + wpos(r, ch * 16));
+    }
+    __syncthreads();  // the next tile's loads overwrite the staging area
+  }
   if (stage_c) {
     __syncthreads();
     // output tile rows (BN bf16 = 512 bytes each) -> C, 16 bytes a thread
