@@ -943,8 +943,6 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   //    direct when it is s x l, natural when it is l x s.
   //  - Every load of the a*X (or A) term is issued before the first store,
   //    so one memory latency is exposed instead of one per block.
-  // Diagonal tiles of the symmetric products take a per-element path that
-  // writes the upper triangle to both halves.
   const bool diag = ga.syrk && bm == bn;
   const MatDesc* md = FINAL ? ga.desc + mat : nullptr;
   const bool tr = FINAL ? md->transposed != 0 : false;
@@ -957,8 +955,14 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   const char* const E = ga.E + mat * ga.e_mat;
   const char* const ET = ga.ET + mat * ga.et_mat;
   constexpr int TST = BM * 2 + 8;             // staged transposed row, bytes
+  const bool stage_t = !QTR && ga.CT != nullptr;
+  const bool stage_c = !FINAL && !stage_t;
 
-  if (!FINAL && diag) {
+  // Diagonal tiles of the symmetric products are written exactly symmetric:
+  // the value computed for (row, col) with row <= col also goes to (col, row).
+  // With a mirror (stage_t) this happens element by element in memory;
+  // otherwise in the LDS staging area below.
+  if (!FINAL && diag && stage_t) {
     static_for<BI>([&](auto I) {
       static_for<BJ>([&](auto J) {
         static_for<4>([&](auto G) {
@@ -1001,8 +1005,6 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   // the registers.  Staged rows are 512 bytes; row r holds 16-byte chunk c at
   // position c ^ 4*(r % 4), so the 8 rows x 64 bytes a lane instruction
   // touches spread over all banks.
-  const bool stage_t = !QTR && ga.CT != nullptr;
-  const bool stage_c = !FINAL && !stage_t;
   auto cpos = [](int r, int b) {  // staged byte position of tile row r, byte b
     return r * (BN * 2) + ((((b >> 4) ^ ((r & 3) << 2))) << 4) + (b & 15);
   };
@@ -1060,9 +1062,12 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
           const int c0 = col_base + j * 32 - q4;
           if (EPI != EPI_GRAM && !stage_c)
             ev[i][j][g] = load_once(reinterpret_cast<const uint2*>(E + static_cast<int64_t>(row0 + q4) * ga.lde + c0 * 2));
+          else if (EPI != EPI_GRAM && diag)  // the mirrored writes below reach other lanes' inputs
+            ev[i][j][g] = *reinterpret_cast<const uint2*>(smem + cpos(row0 + q4 - bm * BM, (c0 - bn * BN) * 2));
         });
       });
     });
+    if (EPI != EPI_GRAM && stage_c && diag) __syncthreads();
     if (stage_w) {  // the W block has landed in LDS (and the a*X loads with it)
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
@@ -1088,14 +1093,25 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
           if (!FINAL || tr) {  // natural layout
             if (EPI != EPI_GRAM) {
               float e[4];
-              const uint2 ed = stage_c ? *reinterpret_cast<const uint2*>(smem + cpos(row0 + q4 - bm * BM, (c0 - bn * BN) * 2))
-                                       : ev[i][j][g];
+              const uint2 ed = (stage_c && !diag) ? *reinterpret_cast<const uint2*>(smem + cpos(row0 + q4 - bm * BM, (c0 - bn * BN) * 2))
+                                                  : ev[i][j][g];
               unpack_bf16x4(quad_transpose_bf16(ed), e);
 #pragma unroll
               for (int q = 0; q < 4; ++q)
                 v[q] = EPI == EPI_POLY ? fmaf(ga.alpha, e[q], ga.beta * v[q]) : fmaf(ga.alpha, e[q], v[q]);
             }
-            if (!FINAL) {
+            if (!FINAL && diag) {  // stage_c: (row, col) and (col, row) for row <= col
+              const int cl = col - bn * BN;
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                const int rl = row0 + q - bm * BM;
+                if (rl <= cl) {
+                  const uint16_t h = f32_to_bf16(v[q]);
+                  *reinterpret_cast<uint16_t*>(smem + cpos(rl, cl * 2)) = h;
+                  *reinterpret_cast<uint16_t*>(smem + cpos(cl, rl * 2)) = h;
+                }
+              }
+            } else if (!FINAL) {
               const uint2 p = pack_bf16x4(v);
               const uint2 d = quad_transpose_bf16(p);  // row row0 + q4, columns c0 .. c0 + 3
               if (stage_c) {
