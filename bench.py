@@ -98,8 +98,11 @@ def cpu_baseline(wl, inputs):
             i = idx[0]
             m = inputs[i]
             t0 = time.perf_counter()
-            ref.muon_step_matrix(dec(m.W, wl.param_dtype), dec(m.g, wl.grad_dtype),
-                                 np.asarray(m.buf, np.float64), hp)
+            if wl.orthogonalize_only:
+                ref.orthogonalize(dec(m.g, wl.grad_dtype), wl.ns_steps)
+            else:
+                ref.muon_step_matrix(dec(m.W, wl.param_dtype), dec(m.g, wl.grad_dtype),
+                                     np.asarray(m.buf, np.float64), hp)
             dt = time.perf_counter() - t0
             total += dt * len(idx)
             sampled.append(f"{wl.matrices[i].name} {wl.matrices[i].rows}x{wl.matrices[i].cols}: {dt:.2f}s")
@@ -114,7 +117,7 @@ def cpu_baseline(wl, inputs):
         pass
     return {"value": len(wl.matrices) / total, "unit": "matrices/s", "cores": cores,
             "kind": "oracle",
-            "sample": (f"fp64 NumPy oracle, one full Muon step on one matrix per shape bucket "
+            "sample": (f"fp64 NumPy oracle, one full {'orthogonalisation' if wl.orthogonalize_only else 'Muon step'} on one matrix per shape bucket "
                        f"({'; '.join(sampled)}), extrapolated by bucket counts to all "
                        f"{len(wl.matrices)} matrices; {cores} BLAS threads on {cpu}")}
 
@@ -179,11 +182,18 @@ def main():
     if args.reference_gemm:
         print(json.dumps(reference_gemm(wl)), flush=True)
         return
-    if wl.orthogonalize_only:
-        raise SystemExit("bench.py times the Muon step; pick a workload with optimizer state")
     t_gen = time.perf_counter()
     inputs = synth.make_workload(wl)
-    W, G, B = upload(inputs, wl)
+    if wl.orthogonalize_only:
+        # the standalone batched NS: one ns_orthogonalize_batched call over
+        # every matrix is the step
+        G = [torch.from_numpy(np.ascontiguousarray(m.g).view(np.int16)).view(torch.bfloat16).cuda()
+             if wl.grad_dtype == "bf16" else torch.from_numpy(np.ascontiguousarray(m.g, dtype=np.float32)).cuda()
+             for m in inputs]
+        outs = [torch.empty_like(t) for t in G]
+        W = B = None
+    else:
+        W, G, B = upload(inputs, wl)
     torch.cuda.synchronize()
     gen_s = time.perf_counter() - t_gen
 
@@ -196,10 +206,15 @@ def main():
         del src, dst
 
     muon = Muon(0)
-    hp = dict(lr=wl.lr, beta=wl.beta, weight_decay=wl.weight_decay, ns_steps=wl.ns_steps,
-              nesterov=wl.nesterov, ns_precision=wl.ns_precision)
+    if wl.orthogonalize_only:
+        ohp = dict(ns_steps=wl.ns_steps, ns_precision=wl.ns_precision)
+        run_step = lambda: muon.orthogonalize(G, outs, **ohp)
+    else:
+        hp = dict(lr=wl.lr, beta=wl.beta, weight_decay=wl.weight_decay, ns_steps=wl.ns_steps,
+                  nesterov=wl.nesterov, ns_precision=wl.ns_precision)
+        run_step = lambda: muon.step(W, G, B, **hp)
     for _ in range(args.warmup):
-        muon.step(W, G, B, **hp)
+        run_step()
     torch.cuda.synchronize()
     muon.profile(True)
     muon.profile_read(reset=True)
@@ -207,7 +222,7 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        muon.step(W, G, B, **hp)
+        run_step()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     stats = muon.profile_read(reset=True)

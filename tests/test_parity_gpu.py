@@ -88,21 +88,24 @@ def test_muon_step_matches_oracle(muon, pdt, gdt, prec, nesterov):
 UPPER_SHAPES = [(512, 1024), (1024, 512), (768, 768), (500, 1200)]
 
 
-def test_upper_tile_path_step_matches_oracle(muon):
+@pytest.mark.parametrize("pdt,gdt", [("bf16", "bf16"), ("f32", "f32")])
+def test_upper_tile_path_step_matches_oracle(muon, pdt, gdt):
+    # bf16 parameters take the staged in-place update for interior blocks and
+    # the per-vector one at ragged edges; fp32 parameters always the latter
     import torch
     hp = ref.MuonHParams(lr=0.02, beta=0.95, weight_decay=0.01, nesterov=True)
-    Ws = [gen(s, 0.02, "bf16", 20, i, 0) for i, s in enumerate(UPPER_SHAPES)]
-    gs = [gen(s, 1e-3, "bf16", 20, i, 1) for i, s in enumerate(UPPER_SHAPES)]
+    Ws = [gen(s, 0.02, pdt, 20, i, 0) for i, s in enumerate(UPPER_SHAPES)]
+    gs = [gen(s, 1e-3, gdt, 20, i, 1) for i, s in enumerate(UPPER_SHAPES)]
     bs = [gen(s, 1e-3, "f32", 20, i, 2) for i, s in enumerate(UPPER_SHAPES)]
-    dW = [to_dev(w, "bf16") for w in Ws]
-    dg = [to_dev(g, "bf16") for g in gs]
+    dW = [to_dev(w, pdt) for w in Ws]
+    dg = [to_dev(g, gdt) for g in gs]
     db = [to_dev(b, "f32") for b in bs]
     muon.step(dW, dg, db, lr=hp.lr, beta=hp.beta, weight_decay=hp.weight_decay, ns_precision="bf16")
     torch.cuda.synchronize()
     for s, W, g, b, w_dev, b_dev in zip(UPPER_SHAPES, Ws, gs, bs, dW, db):
-        W0 = decode(W, "bf16")
-        r = ref.muon_step_matrix(W0, decode(g, "bf16"), np.asarray(b, np.float64), hp)
-        err, rho = w_gate(to_host(w_dev), r.W_new, W0, "bf16")
+        W0 = decode(W, pdt)
+        r = ref.muon_step_matrix(W0, decode(g, gdt), np.asarray(b, np.float64), hp)
+        err, rho = w_gate(to_host(w_dev), r.W_new, W0, pdt)
         print(f"upper-tile path {s}: W err {err:.3e} (rho {rho:.1e})", flush=True)
         assert err <= tol_for("bf16", s) + rho, (s, err, rho)
         assert rel(to_host(b_dev), r.buf_new) <= MOMENTUM_TOL, s
