@@ -260,6 +260,11 @@ struct GemmArgs {
   // operand storage, 256 x 256 kernel only: 0 row-major over K; 1 symmetric,
   // upper-triangle 256 x 256 tiles only; 2 (Q) stored K x N
   int32_t p_mode, q_mode;
+  // 256 x 256 kernel, polynomial product: the A term is added to the
+  // accumulators in the main loop (weight alpha = b/c, output beta * acc)
+  // instead of being read again in the epilogue.  The update products
+  // always add their a*X term that way on this kernel.
+  int32_t e_loop;
 };
 
 constexpr int kRowBytes = 144;                   // 128 data + 16 pad per LDS row
@@ -760,7 +765,7 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
     qto[i] = static_cast<uint32_t>(t * ga.ldq + ((lane % 32) ^ ((t & 3) << 2)) * 16);
   }
   const uint32_t lds0 = lds_offset(smem);
-  auto issue = [&](int ks) {
+  auto issue = [&](int ks) __attribute__((always_inline)) {
     const uint32_t base = lds0 + (ks & 1) * STAGE;
     if (CAN_PT && ks < p_tr_end) {
       const char* b = Pt + static_cast<int64_t>(ks) * 64 * ga.ldp;
@@ -813,11 +818,78 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
 #pragma unroll
   for (int j = 0; j < BJ; ++j) tqo[j] = OPQ + tr_off(wn * (BN / WN) + j * 32);
 
+  // ---- the a*X (or A) term, taken from the operand slabs ----------------------
+  // The tile that the epilogue combines with the product passes through LDS
+  // as part of an operand, so it is added to the accumulators there instead
+  // of being read from memory again:
+  //  - update products: rows bm*256 + [0, 256) of X are the Q slabs
+  //    4 bm .. 4 bm + 3 (transposed geometry); the wave's 128 rows are slabs
+  //    4 bm + 2 wm + h, h = 0, 1, holding its row blocks 2h and 2h + 1;
+  //  - polynomial: A[bm, bn] is the P slabs 4 bn .. 4 bn + 3 (direct, as
+  //    bn >= bm); the wave's 64 columns are slab 4 bn + wn.
+  // One transposing read gives a lane the 4 consecutive rows of one column
+  // that 4 accumulator registers hold: lane 4e + q of 16-lane group G
+  // addresses row 4(G/2) + e, columns 16(G%2) + 4q .. +3 of the block's
+  // register group, and lane t receives column 16(G%2) + t, rows 0..3.
+  // The polynomial adds alpha = b/c times A and scales by beta = c at the
+  // end; with c = 0 the launch keeps the epilogue path (e_loop = 0).
+  constexpr bool EUPD = QTR;
+  const bool epoly = EPI == EPI_POLY && ga.e_loop != 0;
+  int e_ks0 = -1, e_ks1 = -1;
+  if (EUPD) {
+    e_ks0 = bm * (BM / 64) + 2 * wm;
+    e_ks1 = e_ks0 + 1;
+  } else if (epoly) {
+    e_ks0 = bn * (BN / 64) + wn;
+  }
+  int eo[BJ][2];
+  {
+    const int G = lane >> 4, L = lane & 15;
+#pragma unroll
+    for (int j = 0; j < BJ; ++j)
+#pragma unroll
+      for (int gp = 0; gp < 2; ++gp) {
+        if (EUPD)  // Q slab: row k holds chunk c at c ^ 4(k % 4)
+          eo[j][gp] = OPQ + (4 * (G >> 1) + (L >> 2)) * 512 +
+                      ((2 * (wn * (BN / WN) + 32 * j) + 32 * (G & 1) + 8 * (L & 3)) ^ ((L >> 2) << 6));
+        else       // P slab: row r holds chunk c at c ^ ((r >> 1) % 8)
+          eo[j][gp] = (wm * (BM / WM) + 4 * (G >> 1) + (L >> 2)) * SLAB +
+                      (((4 * j + 2 * (G & 1) + ((L >> 1) & 1)) ^ (4 * gp + 2 * (G >> 1) + (L >> 3))) << 4) +
+                      8 * (L & 1);
+      }
+  }
+  auto add_e = [&](const char* sp, auto i0c, auto nic) __attribute__((always_inline)) {
+    constexpr int i0 = decltype(i0c)::value, ni = decltype(nic)::value;
+    static_for<ni>([&](auto II) {
+      constexpr int i = i0 + decltype(II)::value;
+      uint2 ev[BJ][4];
+      static_for<BJ>([&](auto J) {
+        static_for<4>([&](auto Gc) {
+          constexpr int j = decltype(J)::value, g = decltype(Gc)::value;
+          ev[j][g] = EUPD ? tr_read_b64(sp + eo[j][0] + (32 * (i & 1) + 8 * g) * 512)
+                          : tr_read_b64(sp + eo[j][g & 1] + (32 * i + 8 * g) * SLAB);
+        });
+      });
+      static_for<BJ>([&](auto J) {
+        static_for<4>([&](auto Gc) {
+          constexpr int j = decltype(J)::value, g = decltype(Gc)::value;
+          float e[4];
+          unpack_bf16x4(ev[j][g], e);
+          f32x16_t& c = acc[i][j];
+          c[4 * g + 0] = fmaf(ga.alpha, e[0], c[4 * g + 0]);
+          c[4 * g + 1] = fmaf(ga.alpha, e[1], c[4 * g + 1]);
+          c[4 * g + 2] = fmaf(ga.alpha, e[2], c[4 * g + 2]);
+          c[4 * g + 3] = fmaf(ga.alpha, e[3], c[4 * g + 3]);
+        });
+      });
+    });
+  };
+
   // Software pipeline: the fragments of group g+1 are read into the other
   // register set while group g's MFMAs issue, one LDS read between
   // consecutive MFMAs; the slab barrier sits before the last group's MFMAs.
   u32x4_t fa[2][BI], fb[2][BJ];
-  auto rd = [&](auto ptc, auto qtc, const char* sp, auto grpc, auto setc) {
+  auto rd = [&](auto ptc, auto qtc, const char* sp, auto grpc, auto setc) __attribute__((always_inline)) {
     constexpr bool PT = decltype(ptc)::value, QT = decltype(qtc)::value;
     constexpr int grp = decltype(grpc)::value, set = decltype(setc)::value;
     const int pos = ((2 * grp + fsel) ^ fsw) * 16;
@@ -842,13 +914,13 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
       }
     }
   };
-  auto mm = [&](auto setc) {
+  auto mm = [&](auto setc) __attribute__((always_inline)) {
     constexpr int set = decltype(setc)::value;
     static_for<BI>([&](auto I) {
       static_for<BJ>([&](auto J) { Mma<uint16_t>::run(fa[set][I.value], fb[set][J.value], acc[I.value][J.value]); });
     });
   };
-  auto interleave = [&](auto ptc, auto qtc) {
+  auto interleave = [&](auto ptc, auto qtc) __attribute__((always_inline)) {
     constexpr int NRD = (decltype(ptc)::value ? 2 : 1) * BI + (decltype(qtc)::value ? 2 : 1) * BJ;
     constexpr int NPAIR = NRD < BI * BJ ? NRD : BI * BJ;
 #pragma unroll
@@ -869,9 +941,20 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   // operand data), or at the top of the slab before it (3/4 of a slab ahead;
   // measured faster for the other products).
   constexpr bool EARLY = EPI == EPI_GRAM;
-  auto slab = [&](auto ptc, auto qtc, auto nextc, int ks) {
+  auto slab = [&](auto ptc, auto qtc, auto nextc, auto ec, int ks) __attribute__((always_inline)) {
     const char* sp = smem + (ks & 1) * STAGE;
     if (!EARLY && ks + 1 < nk) issue(ks + 1);
+    if constexpr (decltype(ec)::value) {
+      if (ks == e_ks0 || ks == e_ks1) {  // wave-uniform; at most twice a tile
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (EUPD) {
+          if (ks == e_ks0) add_e(sp, I_<0>{}, I_<2>{});
+          else add_e(sp, I_<2>{}, I_<2>{});
+        } else {
+          add_e(sp, I_<0>{}, I_<BI>{});
+        }
+      }
+    }
     __builtin_amdgcn_sched_barrier(0);
     rd(ptc, qtc, sp, I_<1>{}, I_<1>{}); mm(I_<0>{}); interleave(ptc, qtc);
     __builtin_amdgcn_sched_barrier(0);
@@ -895,11 +978,12 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   // Slabs [a, b) in one mode.  Each run starts from a published slab and
   // ends with the next one published, so runs chain without carrying
   // fragments across a change of mode (which happens at most twice a tile).
-  auto run = [&](auto ptc, auto qtc, int a, int b) {
+  // With ec, the run may hold the slabs that carry the a*X (or A) term.
+  auto run = [&](auto ptc, auto qtc, auto ec, int a, int b) __attribute__((always_inline)) {
     if (a >= b) return;
     rd(ptc, qtc, smem + (a & 1) * STAGE, I_<0>{}, I_<0>{});
-    for (int ks = a; ks < b - 1; ++ks) slab(ptc, qtc, std::true_type{}, ks);
-    slab(ptc, qtc, std::false_type{}, b - 1);
+    for (int ks = a; ks < b - 1; ++ks) slab(ptc, qtc, std::true_type{}, ec, ks);
+    slab(ptc, qtc, std::false_type{}, ec, b - 1);
   };
   using T_ = std::true_type;
   using F_ = std::false_type;
@@ -915,15 +999,17 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   // Mode runs: P transposed for [0, p_tr_end), Q for [0, q_tr_end).  The
   // launches keep p_tr_end <= q_tr_end (GRAM none, POLY bm <= bn, update
   // products Q transposed throughout).
+  // The term's slabs lie in the last run (k >= 256 bm for the update
+  // products, k >= 256 bn for the polynomial).
   if constexpr (EPI == EPI_GRAM) {
-    run(F_{}, F_{}, 0, nk);
+    run(F_{}, F_{}, F_{}, 0, nk);
   } else if constexpr (QTR) {
-    run(T_{}, T_{}, 0, p_tr_end);
-    run(F_{}, T_{}, p_tr_end, nk);
+    run(T_{}, T_{}, F_{}, 0, p_tr_end);
+    run(F_{}, T_{}, T_{}, p_tr_end, nk);
   } else {
-    run(T_{}, T_{}, 0, p_tr_end);
-    run(F_{}, T_{}, p_tr_end, q_tr_end);
-    run(F_{}, F_{}, max(p_tr_end, q_tr_end), nk);
+    run(T_{}, T_{}, F_{}, 0, p_tr_end);
+    run(F_{}, T_{}, F_{}, p_tr_end, q_tr_end);
+    run(F_{}, F_{}, T_{}, max(p_tr_end, q_tr_end), nk);
   }
 
   // ---- epilogue from registers ----------------------------------------------
@@ -932,8 +1018,9 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   // `col` of the transposed tile).  A 4-lane transpose gives the direct
   // layout: lane t = l % 4 holds row row0+t, columns c0..c0+3, and 8 lanes
   // cover 64 contiguous bytes of a row.
-  //  - The a*X (or A) term is read coalesced in the direct layout and turned
-  //    to the natural one while still packed bfloat16.
+  //  - The a*X (or A) term is already in the accumulators (added in the main
+  //    loop), except for a polynomial launched with e_loop = 0, which reads
+  //    it here, through the staging area or coalesced in the direct layout.
   //  - Outputs are rounded to bfloat16 once and leave through LDS as whole
   //    512-byte rows.  When the symmetric products must also write their
   //    mirrored tile (see below), that one is staged instead and the direct
@@ -957,6 +1044,7 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   constexpr int TST = BM * 2 + 8;             // staged transposed row, bytes
   const bool stage_t = !QTR && ga.CT != nullptr;
   const bool stage_c = !FINAL && !stage_t;
+  const bool e_epi = EPI == EPI_POLY && !epoly;  // the term is read in the epilogue
 
   // Diagonal tiles of the symmetric products are written exactly symmetric:
   // the value computed for (row, col) with row <= col also goes to (col, row).
@@ -970,9 +1058,9 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
           const int row0 = row_base + i * 32 + 8 * g;
           const int col = col_base + j * 32;
           float v[4];
-          if (EPI == EPI_GRAM) {
+          if (!e_epi) {
 #pragma unroll
-            for (int q = 0; q < 4; ++q) v[q] = acc[i][j][4 * g + q];
+            for (int q = 0; q < 4; ++q) v[q] = EPI == EPI_POLY ? ga.beta * acc[i][j][4 * g + q] : acc[i][j][4 * g + q];
           } else {
             float e[4];
             unpack_bf16x4(*reinterpret_cast<const uint2*>(ET + static_cast<int64_t>(col) * ga.ldet + row0 * 2), e);
@@ -1034,7 +1122,7 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
       load_lds16(wb, static_cast<uint32_t>(row * md->cols * 2 + c * 16), lds0 + (wave * 16 + k) * 1024);
     }
   }
-  if (EPI != EPI_GRAM && stage_c) {
+  if (e_epi && stage_c) {
     // a wave instruction fills 2 staged rows (1 KB); lane l: row 2k + l/32,
     // position l % 32, which holds chunk (l % 32) ^ 4*(row % 4)
     static_assert(BM * BN * 2 / 1024 == 16 * NW, "E tile: 16 load instructions per wave");
@@ -1060,15 +1148,15 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
           constexpr int i = decltype(I)::value, j = decltype(J)::value, g = decltype(G)::value;
           const int row0 = row_base + i * 32 + 8 * g;
           const int c0 = col_base + j * 32 - q4;
-          if (EPI != EPI_GRAM && !stage_c)
+          if (e_epi && !stage_c)
             ev[i][j][g] = load_once(reinterpret_cast<const uint2*>(E + static_cast<int64_t>(row0 + q4) * ga.lde + c0 * 2));
-          else if (EPI != EPI_GRAM && diag)  // the mirrored writes below reach other lanes' inputs
+          else if (e_epi && diag)  // the mirrored writes below reach other lanes' inputs
             ev[i][j][g] = *reinterpret_cast<const uint2*>(smem + cpos(row0 + q4 - bm * BM, (c0 - bn * BN) * 2));
         });
       });
     });
-    if (EPI != EPI_GRAM && stage_c && diag) __syncthreads();
-    if (stage_w) {  // the W block has landed in LDS (and the a*X loads with it)
+    if (e_epi && stage_c && diag) __syncthreads();
+    if (stage_w) {  // the W block has landed in LDS
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
     }
@@ -1091,14 +1179,16 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
 #pragma unroll
           for (int q = 0; q < 4; ++q) v[q] = acc[i][j][4 * g + q];
           if (!FINAL || tr) {  // natural layout
-            if (EPI != EPI_GRAM) {
+            if (e_epi) {
               float e[4];
               const uint2 ed = (stage_c && !diag) ? *reinterpret_cast<const uint2*>(smem + cpos(row0 + q4 - bm * BM, (c0 - bn * BN) * 2))
                                                   : ev[i][j][g];
               unpack_bf16x4(quad_transpose_bf16(ed), e);
 #pragma unroll
-              for (int q = 0; q < 4; ++q)
-                v[q] = EPI == EPI_POLY ? fmaf(ga.alpha, e[q], ga.beta * v[q]) : fmaf(ga.alpha, e[q], v[q]);
+              for (int q = 0; q < 4; ++q) v[q] = fmaf(ga.alpha, e[q], ga.beta * v[q]);
+            } else if (EPI == EPI_POLY) {
+#pragma unroll
+              for (int q = 0; q < 4; ++q) v[q] *= ga.beta;
             }
             if (!FINAL && diag) {  // stage_c: (row, col) and (col, row) for row <= col
               const int cl = col - bn * BN;
@@ -1129,10 +1219,6 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
             }
           } else {             // parameter is s x l: elements (row0 + q4, c0 .. c0 + 3)
             quad_transpose(v);
-            float e[4];
-            unpack_bf16x4(ev[i][j][g], e);
-#pragma unroll
-            for (int q = 0; q < 4; ++q) v[q] = fmaf(ga.alpha, e[q], v[q]);
             const int row = row0 + q4;
             if (stage_w) {
               w_update(smem + wpos(row - wr0, (c0 - wc0) * 2), v);
@@ -1261,6 +1347,12 @@ hipError_t launch_tile(int epi, GemmArgs ga, int nmat, hipStream_t st) {
   ga.tiles_per_mat = ga.syrk ? ga.tiles_m * (ga.tiles_m + 1) / 2 : ga.tiles_m * ga.tiles_n;
   ga.k_slabs = ga.k_slabs * 128 / Cfg::SLAB;
   ga.total_tiles = ga.tiles_per_mat * nmat;
+  // B = b A + c A^2 = c (A^2 + (b/c) A): the A term joins the accumulators
+  // in the main loop unless c = 0
+  if (epi == EPI_POLY && ga.beta != 0.f) {
+    ga.e_loop = 1;
+    ga.alpha = ga.alpha / ga.beta;
+  }
   // one workgroup per CU slot (persistent), never more workgroups than tiles
   const int slots = device_cu_count() * (160 * 1024 / Cfg::LDS);
   const int g = MUON_PERSISTENT ? min(ga.total_tiles, slots) : ga.total_tiles;

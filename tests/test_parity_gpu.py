@@ -119,6 +119,19 @@ def test_upper_tile_path_orthogonalize_matches_oracle(muon):
         assert err <= tol_for("bf16", s) + rho, (s, err, rho)
 
 
+def test_upper_tile_path_zero_c_steps_match_oracle(muon):
+    # Steps with c = 0 (the cubic iteration) read the polynomial's A term in
+    # the epilogue; steps with c != 0 add it to the accumulators in the main
+    # loop.  Both kinds in one schedule.
+    coeffs = [(3.4445, -4.7750, 2.0315)] * 3 + [(1.5, -0.5, 0.0)] * 3
+    G, outs = run_orth(muon, UPPER_SHAPES, "bf16", "bf16", ns_steps=len(coeffs), coeffs=coeffs, key=22)
+    for s, g, o in zip(UPPER_SHAPES, G, outs):
+        want = ref.orthogonalize(decode(g, "bf16"), len(coeffs), coeffs)
+        err, rho = o_gate(to_host(o), want, "bf16")
+        print(f"zero-c schedule {s}: err {err:.3e} (rho {rho:.1e})", flush=True)
+        assert err <= tol_for("bf16", s) + rho, (s, err, rho)
+
+
 def test_fp32_step_recovers_orthogonalised_update(muon):
     # fp32 parameters: O = (decay*W - W') / (lr*scale) is checked at 1e-4.
     import torch
