@@ -1373,13 +1373,24 @@ hipError_t launch_tile(int epi, GemmArgs ga, int nmat, hipStream_t st) {
   return hipGetLastError();
 }
 
+// The 256 x 256 kernel addresses a tile's 256 rows (operands, the a*X
+// term, the parameter block) by 32-bit offsets from one base, so every row
+// it reads or writes must be shorter than 2^31 / 256 bytes.
+constexpr int64_t kTileMaxRowBytes = (int64_t(1) << 31) / 256;
+inline bool tile_rows_fit(int64_t S, int64_t L, int es) {
+  return S * es < kTileMaxRowBytes && L * es < kTileMaxRowBytes;
+}
+
 // The 256 x 256 kernel runs the bf16 products whose padded extents are
-// multiples of 256: the symmetric ones when S is, the update ones (which
-// read X through transposing LDS reads) when S and L are.  Everything else
-// runs on the 128 x 128 kernel, whose update reads X^T.
+// multiples of 256 (and whose rows fit its offsets): the symmetric ones when
+// S is, the update ones (which read X through transposing LDS reads) when S
+// and L are.  Everything else runs on the 128 x 128 kernel, whose update
+// reads X^T and whose offsets are 64-bit.
 template <typename T>
 hipError_t launch_gemm(int epi, GemmArgs ga, int nmat, hipStream_t st) {
-  if (sizeof(T) == 2 && ga.tiles_m % 2 == 0 && ga.syrk) return launch_tile<CfgSquare>(epi, ga, nmat, st);
+  if (sizeof(T) == 2 && ga.tiles_m % 2 == 0 && ga.syrk && ga.ldp < kTileMaxRowBytes &&
+      ga.ldq < kTileMaxRowBytes && (!ga.E || ga.lde < kTileMaxRowBytes))
+    return launch_tile<CfgSquare>(epi, ga, nmat, st);
   const dim3 grid(static_cast<unsigned>(ga.tiles_per_mat) * nmat), block(256);
   switch (epi) {
     case EPI_GRAM: hipLaunchKernelGGL((k_gemm_nt<T, EPI_GRAM>), grid, block, 0, st, ga); break;
@@ -1418,7 +1429,8 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
   // bf16 with S and L multiples of 256: the update products run on the
   // 256 x 256 kernel and read X through transposing LDS reads, so no X^T is
   // kept (K = 0 applies X0 from whichever layout matches the parameter).
-  const bool qtr = sizeof(XT) == 2 && cg.S % 256 == 0 && cg.L % 256 == 0 && K > 0;
+  const bool qtr = sizeof(XT) == 2 && cg.S % 256 == 0 && cg.L % 256 == 0 && K > 0 &&
+                   tile_rows_fit(cg.S, cg.L, sizeof(XT));
   XT* const xt0 = qtr ? nullptr : static_cast<XT*>(wb.XT[0]);
   hipError_t e;
   {
@@ -1467,9 +1479,15 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
   // Work accounting: `flops` is the dense count of each product on the real
   // extents (Eq. 1); `exec` is what the MFMAs execute: padded extents, and
   // for the symmetric products the upper tiles of the kernel that runs them
-  // (256 x 256 tiles when bf16 and S is a multiple of 256, else 128 x 128).
-  const int tsy = (sizeof(XT) == 2 && cg.S % 256 == 0) ? cg.S / 256 : ts;
-  const double syrk_frac = double(tsy * (tsy + 1) / 2) / double(tsy * tsy);
+  // (256 x 256 tiles when bf16, S a multiple of 256 and the rows short
+  // enough, else 128 x 128; see launch_gemm).
+  auto upper_frac = [&](bool tile) {
+    const int t = tile ? cg.S / 256 : ts;
+    return double(t * (t + 1) / 2) / double(t * t);
+  };
+  const bool tile_sym = sizeof(XT) == 2 && cg.S % 256 == 0;
+  const double gram_frac = upper_frac(tile_sym && tile_rows_fit(cg.S, cg.L, es));
+  const double poly_frac = upper_frac(tile_sym && tile_rows_fit(cg.S, cg.S, es));
   const double Sp = cg.S, Lp = cg.L;
   int cur = 0;
   for (int k = 0; k < K; ++k) {
@@ -1490,7 +1508,7 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
     {
       Timed tm(timer, KK_GRAM, st);
       if ((e = launch_gemm<XT>(EPI_GRAM, g, nmat, st)) != hipSuccess) return e;
-      tm.done(nm * 2 * s * s * l, nm * 2 * Sp * Sp * Lp * syrk_frac, nm * (s * l + s * s) * xsz);
+      tm.done(nm * 2 * s * s * l, nm * 2 * Sp * Sp * Lp * gram_frac, nm * (s * l + s * s) * xsz);
     }
     // B = b A + c A A^T: M = N = K = S.
     GemmArgs p = g;
@@ -1505,7 +1523,7 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
     {
       Timed tm(timer, KK_POLY, st);
       if ((e = launch_gemm<XT>(EPI_POLY, p, nmat, st)) != hipSuccess) return e;
-      tm.done(nm * 2 * s * s * s, nm * 2 * Sp * Sp * Sp * syrk_frac, nm * 2 * s * s * xsz);
+      tm.done(nm * 2 * s * s * s, nm * 2 * Sp * Sp * Sp * poly_frac, nm * 2 * s * s * xsz);
     }
     // X' = a X + B X: M = S, N = L, K = S.  The second operand is X^T (N x K,
     // K contiguous) on the 128 x 128 kernel, X itself (K x N) under qtr.

@@ -132,6 +132,44 @@ def test_upper_tile_path_zero_c_steps_match_oracle(muon):
         assert err <= tol_for("bf16", s) + rho, (s, err, rho)
 
 
+def test_rows_past_the_tile_kernel_offsets(muon):
+    # Rows of 2^22 + 256 bf16 elements are too long for the 256 x 256
+    # kernel's 32-bit row offsets, so this step runs on the 128 x 128 kernel.
+    # The gradient's rows have disjoint supports (row i holds v_i on column
+    # block i and zeros elsewhere), so the iteration acts on every row alone:
+    # the update keeps that pattern exactly, and row i's value follows from
+    # the oracle on the 256 x 256 diagonal matrix with the same singular
+    # values (v_i sqrt(blk)), divided by sqrt(blk).
+    import torch
+    s, blk = 256, 16385
+    l = s * blk
+    assert l * 2 * 256 >= 2 ** 31
+    vb = synth.draw((s,), 1.0, "bf16", rng(23))
+    v = decode(vb, "bf16")
+    lr = 0.02
+    G = torch.zeros((s, s, blk), dtype=torch.bfloat16, device="cuda")
+    ar = torch.arange(s, device="cuda")
+    G[ar, ar, :] = to_dev(vb, "bf16").view(s, 1)
+    G = G.view(s, l)
+    W = torch.zeros_like(G)
+    M = torch.zeros((s, l), dtype=torch.float32, device="cuda")
+    muon.step([W], [G], [M], lr=lr, beta=0.95, weight_decay=0.0, ns_precision="bf16")
+    torch.cuda.synchronize()
+    del G, M
+    W3 = W.view(s, s, blk)
+    dblk = W3[ar, ar, :]
+    assert bool((dblk == dblk[:, :1]).all())
+    assert int(torch.count_nonzero(W)) == int(torch.count_nonzero(dblk))
+    got = to_host(dblk[:, 0].contiguous())
+    # u = (1 - beta)(1 + beta) g is a multiple of g, so X0 is the same
+    O_small = ref.orthogonalize(np.diag(v * np.sqrt(blk)), 5)
+    want = -lr * 0.2 * np.sqrt(l) * np.diag(O_small) / np.sqrt(blk)
+    rho = rel(ref.round_to(want, "bf16"), want)
+    err = rel(got, want)
+    print(f"long rows ({s} x {l}): err {err:.3e} (rho {rho:.1e})", flush=True)
+    assert err <= TOL["bf16"] + rho
+
+
 def test_fp32_step_recovers_orthogonalised_update(muon):
     # fp32 parameters: O = (decay*W - W') / (lr*scale) is checked at 1e-4.
     import torch
