@@ -26,8 +26,9 @@
  *   - Device pointers are HIP device addresses on the handle's device; host
  *     pointers (arrays of descriptors, coefficient tables) are read during
  *     the call only and may be freed when it returns.
- *   - Matrices are dense and row-major: element (i, j) of an entry sits at
- *     base + (e*rows + i)*cols + j for plane e of a stacked entry.
+ *   - Matrices are row-major.  The outputs of ns_orthogonalize_batched and
+ *     its inputs are dense; a muon_step entry may be a strided view of a
+ *     larger parameter (see muon_param_t).
  *   - All work is enqueued on `stream` (a hipStream_t; NULL is the null
  *     stream) and the call returns without waiting for it.  Every buffer the
  *     caller passes must stay alive until that work has completed.
@@ -50,7 +51,7 @@
 extern "C" {
 #endif
 
-#define MUON_HIP_ABI_VERSION 1
+#define MUON_HIP_ABI_VERSION 2
 
 typedef struct muon_handle* muon_handle_t;
 
@@ -69,16 +70,40 @@ typedef enum { MUON_F32 = 0, MUON_BF16 = 1 } muon_dtype_t;
  * or fp32 throughout.  Momentum, norm and update are fp32 in both. */
 typedef enum { MUON_NS_BF16 = 0, MUON_NS_F32 = 1 } muon_ns_precision_t;
 
-/* One parameter entry (Sec. 6.3: a stacked entry is `batch` matrices). */
+/* One parameter entry: `batch` matrices of rows x cols (Sec. 6.3: a stacked
+ * expert weight is E independent matrices).
+ *
+ * Logical matrices (Sec. 6.6: the matrix as Muon sees it is defined apart
+ * from the storage layout): an entry may be a zero-copy strided view of a
+ * larger physical parameter, e.g. one of the heads of a fused QKV weight
+ * (row blocks), the gate or up half of a packed FC1 weight (a column range,
+ * ld > cols), or such a piece of every expert of a stack (plane_stride).
+ * Row i of plane e starts at element
+ *     e*plane_stride + (i / row_block)*block_stride + (i % row_block)*ld
+ * of param and grad (and of momentum unless momentum_dense), and its cols
+ * elements are contiguous; the update is written back through the same
+ * mapping and nothing outside the view is touched.  Zero selects each
+ * field's dense default, so a zeroed tail describes a dense
+ * batch x rows x cols array.  The views of all entries must be disjoint
+ * (grads may share elements with other grads). */
 typedef struct {
-  void* param;             /* in/out: batch x rows x cols, param_dtype */
-  const void* grad;        /* in:     batch x rows x cols, grad_dtype */
-  float* momentum;         /* in/out: batch x rows x cols, fp32 */
-  int64_t rows, cols;      /* the matrix plane (last two dims), >= 1 */
+  void* param;             /* in/out: param_dtype */
+  const void* grad;        /* in:     grad_dtype, same view as param */
+  float* momentum;         /* in/out: fp32, same view as param, or dense */
+  int64_t rows, cols;      /* the logical matrix, >= 1 */
   int64_t batch;           /* >= 1 */
-  int64_t ld;              /* row stride in elements: 0 or cols (dense only) */
+  int64_t ld;              /* row stride in elements: 0 (= cols) or >= cols */
   muon_dtype_t param_dtype;
   muon_dtype_t grad_dtype;
+  int64_t row_block;       /* rows per contiguous-stride block: 0 (= rows) or
+                              a divisor of rows */
+  int64_t block_stride;    /* elements from one row block to the next:
+                              0 (= row_block*ld), else >= (row_block-1)*ld + cols */
+  int64_t plane_stride;    /* elements from one plane to the next: 0 (= number
+                              of blocks * block_stride), else >= the span of a plane */
+  int32_t momentum_dense;  /* 0: momentum has param's view; 1: momentum is a
+                              dense batch x rows x cols array */
+  int32_t reserved;        /* must be 0 */
 } muon_param_t;
 
 typedef struct {

@@ -32,7 +32,10 @@ class MuonParam(ctypes.Structure):
     _fields_ = [("param", ctypes.c_void_p), ("grad", ctypes.c_void_p),
                 ("momentum", ctypes.c_void_p), ("rows", ctypes.c_int64),
                 ("cols", ctypes.c_int64), ("batch", ctypes.c_int64), ("ld", ctypes.c_int64),
-                ("param_dtype", ctypes.c_int), ("grad_dtype", ctypes.c_int)]
+                ("param_dtype", ctypes.c_int), ("grad_dtype", ctypes.c_int),
+                ("row_block", ctypes.c_int64), ("block_stride", ctypes.c_int64),
+                ("plane_stride", ctypes.c_int64), ("momentum_dense", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
 
 class MuonHParams(ctypes.Structure):
@@ -129,31 +132,76 @@ def _dtype_code(t) -> int:
     raise TypeError(f"unsupported dtype {t.dtype}")
 
 
-def _plane(t):
-    if t.dim() == 2:
-        return 1, t.shape[0], t.shape[1]
-    if t.dim() == 3:
-        return t.shape[0], t.shape[1], t.shape[2]
-    raise ValueError("Muon takes matrices [M, N] or stacks [E, M, N]")
+class RowBlocks:
+    """A logical matrix made of the row blocks of a view: `t` is
+    [nblk, rb, N] (or [E, nblk, rb, N]) with unit column stride, and its
+    blocks stack into one (nblk*rb) x N matrix (per plane), e.g. the heads of
+    one projection inside a fused, head-interleaved QKV weight."""
+
+    def __init__(self, t):
+        self.t = t
+
+
+def _view(x):
+    """(tensor, batch, rows, cols, ld, row_block, block_stride, plane_stride)
+    of a logical matrix: a tensor [M, N] or [E, M, N] whose columns are
+    contiguous (any row and plane strides), or RowBlocks.  Strides of
+    singleton dimensions do not matter and become 0, the dense default.
+    Dense tensors give all-zero strides except ld = N."""
+    blocks = isinstance(x, RowBlocks)
+    t = x.t if blocks else x
+    if t.dim() == 0 or (t.shape[-1] > 1 and t.stride(-1) != 1):
+        raise ValueError("a logical matrix needs contiguous columns")
+    if blocks:
+        if t.dim() == 3:
+            E, nb, rb, N = 1, *tuple(t.shape)
+            ps, bs, ld = 0, t.stride(0), t.stride(1)
+        elif t.dim() == 4:
+            E, nb, rb, N = tuple(t.shape)
+            ps, bs, ld = t.stride(0), t.stride(1), t.stride(2)
+        else:
+            raise ValueError("RowBlocks takes [nblk, rb, N] or [E, nblk, rb, N]")
+    elif t.dim() in (2, 3):
+        E = 1 if t.dim() == 2 else t.shape[0]
+        nb, rb, N = 1, t.shape[-2], t.shape[-1]
+        ps, bs, ld = (t.stride(0) if t.dim() == 3 else 0), 0, t.stride(-2)
+    else:
+        raise ValueError("Muon takes matrices [M, N] or stacks [E, M, N]")
+    rows = nb * rb
+    if rb == 1:
+        ld = 0
+    if nb == 1:
+        rb, bs = 0, 0
+    if E == 1:
+        ps = 0
+    if ld == 0 or (ld == N and rb == 0):
+        ld = N
+    return t, E, rows, N, ld, rb, bs, ps
 
 
 def params_array(params, grads, moms):
-    """MuonParam[] for lists of torch tensors ([M, N] or [E, M, N])."""
+    """MuonParam[] for lists of logical matrices (see _view).  grad takes
+    the param's view; momentum takes it too, or is a dense
+    [M, N] / [E, M, N] tensor."""
     import torch
     if not (len(params) == len(grads) == len(moms)):
         raise ValueError("params, grads and momenta must have equal length")
     arr = (MuonParam * max(1, len(params)))()
     for i, (W, g, m) in enumerate(zip(params, grads, moms)):
-        if W.shape != g.shape or W.shape != m.shape:
-            raise ValueError(f"entry {i}: shapes differ")
-        if m.dtype != torch.float32:
+        vw, vg, vm = _view(W), _view(g), _view(m)
+        if vw[1:] != vg[1:] or tuple(vw[0].shape) != tuple(vg[0].shape):
+            raise ValueError(f"entry {i}: grad must have the param's shape and strides")
+        if vm[0].dtype != torch.float32:
             raise TypeError(f"entry {i}: momentum must be float32")
-        for t in (W, g, m):
-            if not t.is_contiguous():
-                raise ValueError(f"entry {i}: tensors must be contiguous")
-        batch, rows, cols = _plane(W)
-        arr[i] = MuonParam(W.data_ptr(), g.data_ptr(), m.data_ptr(), rows, cols, batch, cols,
-                           _dtype_code(W), _dtype_code(g))
+        _, batch, rows, cols, ld, rb, bs, ps = vw
+        if vm[1:] == vw[1:] and tuple(vm[0].shape) == tuple(vw[0].shape):
+            mdense = 0
+        elif vm[0].is_contiguous() and vm[0].numel() == batch * rows * cols and vm[3] == cols:
+            mdense = 1
+        else:
+            raise ValueError(f"entry {i}: momentum must have the param's view or be dense")
+        arr[i] = MuonParam(vw[0].data_ptr(), vg[0].data_ptr(), vm[0].data_ptr(), rows, cols, batch,
+                           ld, _dtype_code(vw[0]), _dtype_code(vg[0]), rb, bs, ps, mdense, 0)
     return arr
 
 

@@ -119,13 +119,22 @@ void set_err(muon_handle_t h, const char* fmt, ...) {
 size_t dtype_size(int dt) { return dt == MUON_BF16 ? 2 : 4; }
 bool dtype_ok(int dt) { return dt == MUON_F32 || dt == MUON_BF16; }
 
-// One matrix of the request, before planning.
+// One matrix of the request, before planning.  Row i of the matrix starts at
+// element (i / rb)*bs + (i % rb)*ld of W, g and out, and (i / rb)*bs_b +
+// (i % rb)*ld_b of buf.
 struct Item {
   int64_t flat;            // entry-major, plane-minor index
   int64_t rows, cols;
   int32_t pdt, gdt;
   void* W; const void* g; float* buf; void* out;
+  int64_t ld, rb, bs, ld_b, bs_b;
 };
+
+void set_dense(Item& it) {
+  it.ld = it.ld_b = it.cols;
+  it.rb = it.rows;
+  it.bs = it.bs_b = it.rows * it.cols;
+}
 
 struct Range { uintptr_t lo, hi; bool written; };
 
@@ -185,6 +194,32 @@ muon_status_t check_dims(int64_t rows, int64_t cols, int64_t batch, const char* 
   return MUON_OK;
 }
 
+// The elements a view of `batch` planes occupies, as byte ranges: one range
+// when the view is dense, one per row block when rows follow each other
+// within a block, else one per row.
+void view_ranges(uintptr_t base, size_t es, int64_t rows, int64_t cols, int64_t batch, int64_t ld,
+                 int64_t rb, int64_t bs, int64_t ps, bool written, std::vector<Range>& out) {
+  const int64_t nblk = rows / rb;
+  const bool rows_run = ld == cols;                       // a block is one run
+  const bool blocks_run = rows_run && (nblk == 1 || bs == rb * cols);
+  if (blocks_run && (batch == 1 || ps == rows * cols)) {
+    out.push_back({base, base + uintptr_t(batch * rows * cols) * es, written});
+    return;
+  }
+  for (int64_t e = 0; e < batch; ++e)
+    for (int64_t b = 0; b < nblk; ++b) {
+      const int64_t blk = e * ps + b * bs;
+      if (rows_run) {
+        out.push_back({base + uintptr_t(blk) * es, base + uintptr_t(blk + rb * cols) * es, written});
+      } else {
+        for (int64_t r = 0; r < rb; ++r) {
+          const uintptr_t lo = base + uintptr_t(blk + r * ld) * es;
+          out.push_back({lo, lo + uintptr_t(cols) * es, written});
+        }
+      }
+    }
+}
+
 muon_status_t validate_step(const muon_param_t* params, int64_t n, const muon_hparams_t* hp,
                             std::vector<Item>* items, Msg& msg) {
   muon_status_t st = check_hparams(hp, msg);
@@ -199,29 +234,72 @@ muon_status_t validate_step(const muon_param_t* params, int64_t n, const muon_hp
     if (!p.param || !p.grad || !p.momentum) { msg.set("entry %lld: NULL pointer", (long long)i); return MUON_ERR_INVALID_ARGUMENT; }
     if ((st = check_dims(p.rows, p.cols, p.batch, "entry", i, msg)) != MUON_OK) return st;
     if (!dtype_ok(p.param_dtype) || !dtype_ok(p.grad_dtype)) { msg.set("entry %lld: unknown dtype", (long long)i); return MUON_ERR_INVALID_ARGUMENT; }
-    if (p.ld != 0 && p.ld != p.cols) { msg.set("entry %lld: only dense rows (ld == cols) are supported", (long long)i); return MUON_ERR_UNSUPPORTED; }
     const int64_t plane = p.rows * p.cols;
     if (p.batch > (int64_t(1) << 40) / plane) { msg.set("entry %lld: too many elements", (long long)i); return MUON_ERR_UNSUPPORTED; }
+    // the logical-matrix view (zero fields take their dense defaults)
+    if (p.ld < 0 || p.row_block < 0 || p.block_stride < 0 || p.plane_stride < 0) {
+      msg.set("entry %lld: negative stride", (long long)i);
+      return MUON_ERR_INVALID_ARGUMENT;
+    }
+    if ((p.momentum_dense != 0 && p.momentum_dense != 1) || p.reserved != 0) {
+      msg.set("entry %lld: momentum_dense must be 0 or 1 and reserved 0", (long long)i);
+      return MUON_ERR_INVALID_ARGUMENT;
+    }
+    const int64_t ld = p.ld ? p.ld : p.cols;
+    const int64_t rb = p.row_block ? p.row_block : p.rows;
+    if (ld < p.cols) { msg.set("entry %lld: ld < cols", (long long)i); return MUON_ERR_INVALID_ARGUMENT; }
+    if (rb > p.rows || p.rows % rb) { msg.set("entry %lld: row_block must divide rows", (long long)i); return MUON_ERR_INVALID_ARGUMENT; }
+    const int64_t nblk = p.rows / rb;
+    // strides beyond 2^46 elements are refused before any product is formed
+    constexpr int64_t kMaxStride = int64_t(1) << 46;
+    if (ld > kMaxStride || p.block_stride > kMaxStride || p.plane_stride > kMaxStride) {
+      msg.set("entry %lld: stride too large", (long long)i);
+      return MUON_ERR_UNSUPPORTED;
+    }
+    const int64_t bs = p.block_stride ? p.block_stride : rb * ld;
+    const double span_d = double(nblk - 1) * double(bs) + double(rb - 1) * double(ld) + double(p.cols);
+    if (span_d > double(kMaxStride)) { msg.set("entry %lld: view too large", (long long)i); return MUON_ERR_UNSUPPORTED; }
+    const int64_t span = (nblk - 1) * bs + (rb - 1) * ld + p.cols;  // elements one plane spans
+    if (nblk > 1 && bs < (rb - 1) * ld + p.cols) {
+      msg.set("entry %lld: row blocks overlap (block_stride too small)", (long long)i);
+      return MUON_ERR_INVALID_ARGUMENT;
+    }
+    const int64_t ps = p.plane_stride ? p.plane_stride : nblk * bs;
+    if (p.batch > 1 && ps < span) { msg.set("entry %lld: planes overlap (plane_stride too small)", (long long)i); return MUON_ERR_INVALID_ARGUMENT; }
+    if (double(p.batch - 1) * double(ps) + double(span) > double(int64_t(1) << 48)) {
+      msg.set("entry %lld: view too large", (long long)i);
+      return MUON_ERR_UNSUPPORTED;
+    }
+    const bool mdense = p.momentum_dense != 0;
     const uintptr_t W = reinterpret_cast<uintptr_t>(p.param), G = reinterpret_cast<uintptr_t>(p.grad),
                     M = reinterpret_cast<uintptr_t>(p.momentum);
-    const uint64_t ne = uint64_t(plane) * uint64_t(p.batch);
     if ((W % dtype_size(p.param_dtype)) || (G % dtype_size(p.grad_dtype)) || (M % 4)) {
       msg.set("entry %lld: pointer not aligned to its element size", (long long)i);
       return MUON_ERR_INVALID_ARGUMENT;
     }
-    ranges.push_back({W, W + ne * dtype_size(p.param_dtype), true});
-    ranges.push_back({G, G + ne * dtype_size(p.grad_dtype), false});
-    ranges.push_back({M, M + ne * 4, true});
+    view_ranges(W, dtype_size(p.param_dtype), p.rows, p.cols, p.batch, ld, rb, bs, ps, true, ranges);
+    view_ranges(G, dtype_size(p.grad_dtype), p.rows, p.cols, p.batch, ld, rb, bs, ps, false, ranges);
+    if (mdense) view_ranges(M, 4, p.rows, p.cols, p.batch, p.cols, p.rows, plane, plane, true, ranges);
+    else view_ranges(M, 4, p.rows, p.cols, p.batch, ld, rb, bs, ps, true, ranges);
     if (items) {
       for (int64_t e = 0; e < p.batch; ++e) {
         Item it;
         it.flat = flat++;
         it.rows = p.rows; it.cols = p.cols;
         it.pdt = p.param_dtype; it.gdt = p.grad_dtype;
-        it.W = static_cast<char*>(p.param) + e * plane * dtype_size(p.param_dtype);
-        it.g = static_cast<const char*>(p.grad) + e * plane * dtype_size(p.grad_dtype);
-        it.buf = p.momentum + e * plane;
+        it.W = static_cast<char*>(p.param) + e * ps * int64_t(dtype_size(p.param_dtype));
+        it.g = static_cast<const char*>(p.grad) + e * ps * int64_t(dtype_size(p.grad_dtype));
+        it.buf = p.momentum + (mdense ? e * plane : e * ps);
         it.out = nullptr;
+        it.ld = ld; it.rb = rb; it.bs = bs;
+        it.ld_b = mdense ? p.cols : ld;
+        it.bs_b = mdense ? rb * p.cols : bs;
+        // row blocks that follow each other at the row stride are no blocks
+        if (it.bs == rb * it.ld && it.bs_b == rb * it.ld_b) {
+          it.rb = p.rows;
+          it.bs = p.rows * it.ld;
+          it.bs_b = p.rows * it.ld_b;
+        }
         items->push_back(it);
       }
     }
@@ -266,6 +344,7 @@ muon_status_t validate_orth(const void* const* in, void* const* out, const int64
       it.flat = i; it.rows = rows[i]; it.cols = cols[i];
       it.pdt = dtype; it.gdt = dtype;
       it.W = nullptr; it.g = in[i]; it.buf = nullptr; it.out = out[i];
+      set_dense(it);
       items->push_back(it);
     }
   }
@@ -438,9 +517,17 @@ MatDesc make_desc(const Item& it, double lr, double wd, int scale_mode) {
   d.W = it.W; d.g = it.g; d.buf = it.buf; d.out = it.out;
   d.rows = int32_t(it.rows); d.cols = int32_t(it.cols);
   d.transposed = it.rows > it.cols ? 1 : 0;
+  d.ld = it.ld; d.bstride = it.bs; d.ld_b = it.ld_b; d.bstride_b = it.bs_b;
+  d.rb = int32_t(it.rb);
+  const bool blocks = it.rb < it.rows;
+  d.dense = (it.ld == it.cols && it.ld_b == it.cols && !blocks) ? 1 : 0;
   const auto al16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
-  d.vec_ok = ((it.rows * it.cols) % 8 == 0) && al16(it.g) && (!it.buf || al16(it.buf)) ? 1 : 0;
-  d.vec4_ok = (it.cols % 4 == 0) && al16(it.W ? it.W : it.out) ? 1 : 0;
+  // 8 consecutive elements of g and buf at 16-byte aligned addresses: over
+  // the flat index when dense, else within a row (every row start aligned)
+  const bool rows8 = it.cols % 8 == 0 && it.ld % 8 == 0 && it.ld_b % 8 == 0 &&
+                     (!blocks || (it.bs % 8 == 0 && it.bs_b % 8 == 0));
+  d.vec_ok = (d.dense ? (it.rows * it.cols) % 8 == 0 : rows8) && al16(it.g) && (!it.buf || al16(it.buf)) ? 1 : 0;
+  d.vec4_ok = (it.cols % 4 == 0 && it.ld % 4 == 0 && (!blocks || it.bs % 4 == 0)) && al16(it.W ? it.W : it.out) ? 1 : 0;
   const double scale = scale_mode == 0 ? 0.2 * std::sqrt(double(std::max(it.rows, it.cols))) : 1.0;
   d.upd_scale = float(lr * scale);
   d.decay = float(1.0 - lr * wd);

@@ -19,20 +19,40 @@ constexpr int kNormElemsPerBlock = 16384;
 enum DType : int32_t { DT_F32 = 0, DT_BF16 = 1 };
 
 // One matrix of a chunk, as the kernels see it (device-resident table).
+// The matrix is a logical view of the caller's storage: its row i starts at
+// element (i / rb) * bstride + (i % rb) * ld of W, g and out, and at
+// (i / rb) * bstride_b + (i % rb) * ld_b of buf; the cols elements of a row
+// are contiguous.  A dense matrix has ld = cols, rb = rows.
 struct MatDesc {
-  void* W;              // parameter (muon_step), param dtype, rows x cols
+  void* W;              // parameter (muon_step), param dtype
   const void* g;        // gradient (muon_step) or NS input (orthogonalize)
   float* buf;           // momentum (muon_step), fp32
-  void* out;            // output (orthogonalize), rows x cols
-  int32_t rows, cols;   // the matrix as stored by the caller
+  void* out;            // output (orthogonalize)
+  int32_t rows, cols;   // the logical matrix
   int32_t transposed;   // rows > cols: the iteration runs on the transpose
-  int32_t vec_ok;       // 16-byte aligned pointers and rows*cols % 8 == 0
+  int32_t vec_ok;       // g and buf can be read 8 elements at a time (16-byte aligned)
   float upd_scale;      // lr * RMS-matching scale
   float decay;          // 1 - lr * weight_decay
-  int32_t vec4_ok;      // W (or out) 16-byte aligned and cols % 4 == 0
-  int32_t reserved1;
+  int32_t vec4_ok;      // W (or out) can be accessed 4 elements at a time
+  int32_t dense;        // W, g, buf all dense: element (i, j) at i * cols + j
+  int64_t ld, bstride;  // row and row-block strides of W, g, out (elements)
+  int64_t ld_b, bstride_b;  // the same for buf
+  int32_t rb;           // rows per row block (rows when not interleaved)
+  int32_t reserved[3];
 };
-static_assert(sizeof(MatDesc) == 64, "MatDesc layout");
+static_assert(sizeof(MatDesc) == 112, "MatDesc layout");
+
+// Element offset of row i, column j of the view (W, g, out) and of buf.
+__host__ __device__ inline int64_t view_index(const MatDesc& d, int64_t i, int64_t j) {
+  if (d.rb >= d.rows) return i * d.ld + j;
+  const int64_t q = i / d.rb;
+  return q * d.bstride + (i - q * d.rb) * d.ld + j;
+}
+__host__ __device__ inline int64_t buf_index(const MatDesc& d, int64_t i, int64_t j) {
+  if (d.rb >= d.rows) return i * d.ld_b + j;
+  const int64_t q = i / d.rb;
+  return q * d.bstride_b + (i - q * d.rb) * d.ld_b + j;
+}
 
 // Geometry shared by all matrices of a chunk.
 struct ChunkGeom {

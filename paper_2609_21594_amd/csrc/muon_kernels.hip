@@ -30,6 +30,11 @@ typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
+// The 256 x 256 kernel addresses a tile's 256 rows (operands, the a*X
+// term, the parameter block) by 32-bit offsets from one base, so every row
+// it reads or writes must be shorter than 2^31 / 256 bytes.
+constexpr int64_t kTileMaxRowBytes = (int64_t(1) << 31) / 256;
+
 // ---------------------------------------------------------------------------
 // bfloat16 storage: uint16 bit patterns.  Widening is exact; narrowing is
 // the hardware conversion (v_cvt_pk_bf16_f32): round to nearest, ties to
@@ -103,27 +108,55 @@ __global__ __launch_bounds__(256) void k_partials(const MatDesc* __restrict__ de
     return gv;
   };
 
+  // Element i of the matrix (row-major over the logical view) sits at
+  // gi(i) in g and bi(i) in buf: i itself when the view is dense.
+  const bool dense = md.dense != 0;
+  const bool small = numel < (int64_t(1) << 31);
+  auto rc = [&](int64_t i, int64_t& r, int64_t& c) {
+    if (small) {
+      const uint32_t q = static_cast<uint32_t>(i) / static_cast<uint32_t>(md.cols);
+      r = q;
+      c = i - static_cast<int64_t>(q) * md.cols;
+    } else {
+      r = i / md.cols;
+      c = i - r * md.cols;
+    }
+  };
+  auto gi = [&](int64_t i) -> int64_t {
+    if (dense) return i;
+    int64_t r, c;
+    rc(i, r, c);
+    return view_index(md, r, c);
+  };
+  auto bi = [&](int64_t i) -> int64_t {
+    if (dense) return i;
+    int64_t r, c;
+    rc(i, r, c);
+    return buf_index(md, r, c);
+  };
   if (md.vec_ok) {
-    // 8 consecutive elements per thread and iteration; numel % 8 == 0.
+    // 8 consecutive elements per thread and iteration (numel % 8 == 0; for
+    // a strided view cols % 8 == 0, so the 8 share a row).
     for (int64_t i = start + threadIdx.x * 8; i < end; i += 256 * 8) {
+      const int64_t ig = gi(i), ib = MOM ? bi(i) : 0;
       float gv[8];
       if (sizeof(GT) == 2) {
-        const u32x4_t raw = *reinterpret_cast<const u32x4_t*>(g + i);
+        const u32x4_t raw = *reinterpret_cast<const u32x4_t*>(g + ig);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           gv[2 * q] = __uint_as_float(raw[q] << 16);
           gv[2 * q + 1] = __uint_as_float(raw[q] & 0xffff0000u);
         }
       } else {
-        const float4 a = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(g) + i);
-        const float4 b = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(g) + i + 4);
+        const float4 a = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(g) + ig);
+        const float4 b = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(g) + ig + 4);
         gv[0] = a.x; gv[1] = a.y; gv[2] = a.z; gv[3] = a.w;
         gv[4] = b.x; gv[5] = b.y; gv[6] = b.z; gv[7] = b.w;
       }
       float bv[8] = {0, 0, 0, 0, 0, 0, 0, 0}, bn[8];
       if (MOM) {
-        const float4 a = *reinterpret_cast<const float4*>(buf + i);
-        const float4 b = *reinterpret_cast<const float4*>(buf + i + 4);
+        const float4 a = *reinterpret_cast<const float4*>(buf + ib);
+        const float4 b = *reinterpret_cast<const float4*>(buf + ib + 4);
         bv[0] = a.x; bv[1] = a.y; bv[2] = a.z; bv[3] = a.w;
         bv[4] = b.x; bv[5] = b.y; bv[6] = b.z; bv[7] = b.w;
       }
@@ -133,16 +166,17 @@ __global__ __launch_bounds__(256) void k_partials(const MatDesc* __restrict__ de
         acc = fmaf(u, u, acc);
       }
       if (MOM) {
-        *reinterpret_cast<float4*>(buf + i) = make_float4(bn[0], bn[1], bn[2], bn[3]);
-        *reinterpret_cast<float4*>(buf + i + 4) = make_float4(bn[4], bn[5], bn[6], bn[7]);
+        *reinterpret_cast<float4*>(buf + ib) = make_float4(bn[0], bn[1], bn[2], bn[3]);
+        *reinterpret_cast<float4*>(buf + ib + 4) = make_float4(bn[4], bn[5], bn[6], bn[7]);
       }
     }
   } else {
     for (int64_t i = start + threadIdx.x; i < end; i += 256) {
-      const float gv = to_f32<GT>(g[i]);
+      const int64_t ig = gi(i), ib = MOM ? bi(i) : 0;
+      const float gv = to_f32<GT>(g[ig]);
       float bn = 0.f;
-      const float u = one(gv, MOM ? buf[i] : 0.f, bn);
-      if (MOM) buf[i] = bn;
+      const float u = one(gv, MOM ? buf[ib] : 0.f, bn);
+      if (MOM) buf[ib] = bn;
       acc = fmaf(u, u, acc);
     }
   }
@@ -198,11 +232,10 @@ __global__ __launch_bounds__(256) void k_normalize(const MatDesc* __restrict__ d
     const int ur = ur0 + row, uc = uc0 + col;
     float v = 0.f;
     if (ur < md.rows && uc < md.cols) {
-      const int64_t idx = static_cast<int64_t>(ur) * md.cols + uc;
-      const float gv = to_f32<GT>(g[idx]);
+      const float gv = to_f32<GT>(g[view_index(md, ur, uc)]);
       float u;
       if (MOM) {
-        const float bn = md.buf[idx];  // already updated by k_partials
+        const float bn = md.buf[buf_index(md, ur, uc)];  // already updated by k_partials
         u = sc.nesterov ? fmaf(beta, bn, omb * gv) : bn;
       } else {
         u = gv;
@@ -410,7 +443,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_nt(GemmArgs ga) {
       } else {  // EPI_FINAL
         if (!tr) {
           if (gi < ga.s && gj < ga.l) {
-            const int64_t pidx = static_cast<int64_t>(gi) * md->cols + gj;
+            const int64_t pidx = view_index(*md, gi, gj);
             if (ga.final_kind == 0) {
               const float w = load_as_f32(md->W, pidx, ga.param_dtype);
               store_from_f32(md->W, pidx, ga.param_dtype, fmaf(md->decay, w, -md->upd_scale * v));
@@ -434,7 +467,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_nt(GemmArgs ga) {
     const int gi = gi0 + r, gj = gj0 + c;
     if (EPI == EPI_FINAL) {
       if (gi < ga.s && gj < ga.l) {  // parameter is l x s: element (gj, gi)
-        const int64_t pidx = static_cast<int64_t>(gj) * md->cols + gi;
+        const int64_t pidx = view_index(*md, gj, gi);
         if (ga.final_kind == 0) {
           const float w = load_as_f32(md->W, pidx, ga.param_dtype);
           store_from_f32(md->W, pidx, ga.param_dtype, fmaf(md->decay, w, -md->upd_scale * v));
@@ -1104,7 +1137,8 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   // natural ones (32 rows x 16 bytes) over all banks.
   bool stage_w = false;
   if constexpr (FINAL && FK == 0 && PDT == DT_BF16)
-    stage_w = v4 && md->cols % 8 == 0 && (bm + 1) * BM <= ga.s && (bn + 1) * BN <= ga.l;
+    stage_w = v4 && md->cols % 8 == 0 && md->ld % 8 == 0 && md->rb >= md->rows &&
+              md->ld * 2 < kTileMaxRowBytes && (bm + 1) * BM <= ga.s && (bn + 1) * BN <= ga.l;
   auto wpos = [](int r, int b) {
     const int key = ((r & 3) << 2) | ((r >> 2) & 3);
     return r * 512 + (((b >> 4) ^ key) << 4) + (b & 15);
@@ -1113,13 +1147,14 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   if (stage_t || stage_c || stage_w) __syncthreads();  // every wave is done with the operand slabs
   if (stage_w) {
     static_assert(BM * BN * 2 / 1024 == 16 * NW, "W tile: 16 load instructions per wave");
-    const char* wb = static_cast<const char*>(md->W) + (static_cast<int64_t>(wr0) * md->cols + wc0) * 2;
+    const char* wb = static_cast<const char*>(md->W) + (static_cast<int64_t>(wr0) * md->ld + wc0) * 2;
+    const uint32_t ldw = static_cast<uint32_t>(md->ld) * 2;
     const uint32_t lds0 = lds_offset(smem);
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
       const int row = 2 * (wave * 16 + k) + lane / 32;
       const int c = (lane % 32) ^ (((row & 3) << 2) | ((row >> 2) & 3));
-      load_lds16(wb, static_cast<uint32_t>(row * md->cols * 2 + c * 16), lds0 + (wave * 16 + k) * 1024);
+      load_lds16(wb, static_cast<uint32_t>(row) * ldw + static_cast<uint32_t>(c * 16), lds0 + (wave * 16 + k) * 1024);
     }
   }
   if (e_epi && stage_c) {
@@ -1215,7 +1250,7 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
             } else if (col < ga.l) {
               const int n = min(4, ga.s - row0);
               if (n > 0)
-                apply4<FK, PDT>(md, static_cast<int64_t>(col) * md->cols + row0, v, v4 && n == 4, n);
+                apply4<FK, PDT>(md, view_index(*md, col, row0), v, v4 && n == 4, n);
             }
           } else {             // parameter is s x l: elements (row0 + q4, c0 .. c0 + 3)
             quad_transpose(v);
@@ -1225,7 +1260,7 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
             } else if (row < ga.s) {
               const int n = min(4, ga.l - c0);
               if (n > 0)
-                apply4<FK, PDT>(md, static_cast<int64_t>(row) * md->cols + c0, v, v4 && n == 4, n);
+                apply4<FK, PDT>(md, view_index(*md, row, c0), v, v4 && n == 4, n);
             }
           }
         });
@@ -1238,7 +1273,7 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
     // updated W rows (512 bytes each) -> W, 16 bytes a thread
     for (int idx = threadIdx.x; idx < BM * 32; idx += 64 * NW) {
       const int r = idx >> 5, ch = idx & 31;
-      *reinterpret_cast<u32x4_t*>(static_cast<char*>(md->W) + (static_cast<int64_t>(wr0 + r) * md->cols + wc0) * 2 +
+      *reinterpret_cast<u32x4_t*>(static_cast<char*>(md->W) + (static_cast<int64_t>(wr0 + r) * md->ld + wc0) * 2 +
                                   ch * 16) = *reinterpret_cast<const u32x4_t*>(smem + wpos(r, ch * 16));
     }
     __syncthreads();  // the next tile's loads overwrite the staging area
@@ -1311,11 +1346,12 @@ __global__ __launch_bounds__(256) void k_apply_x0(const MatDesc* __restrict__ de
   const XT* D = (md.transposed ? XTb : X) + m * matX;
   const int ldD = md.transposed ? cg.S : cg.L;
   const float o = to_f32<XT>(D[ur * ldD + uc]);
+  const int64_t w = view_index(md, ur, uc);
   if (final_kind == 0) {
-    const float w = load_as_f32(md.W, i, cg.param_dtype);
-    store_from_f32(md.W, i, cg.param_dtype, fmaf(md.decay, w, -md.upd_scale * o));
+    const float wv = load_as_f32(md.W, w, cg.param_dtype);
+    store_from_f32(md.W, w, cg.param_dtype, fmaf(md.decay, wv, -md.upd_scale * o));
   } else {
-    store_from_f32(md.out, i, cg.param_dtype, o);
+    store_from_f32(md.out, w, cg.param_dtype, o);
   }
 }
 
@@ -1373,10 +1409,6 @@ hipError_t launch_tile(int epi, GemmArgs ga, int nmat, hipStream_t st) {
   return hipGetLastError();
 }
 
-// The 256 x 256 kernel addresses a tile's 256 rows (operands, the a*X
-// term, the parameter block) by 32-bit offsets from one base, so every row
-// it reads or writes must be shorter than 2^31 / 256 bytes.
-constexpr int64_t kTileMaxRowBytes = (int64_t(1) << 31) / 256;
 inline bool tile_rows_fit(int64_t S, int64_t L, int es) {
   return S * es < kTileMaxRowBytes && L * es < kTileMaxRowBytes;
 }

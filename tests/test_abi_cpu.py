@@ -39,14 +39,14 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.muon_abi_version() == 1
+    assert lib.muon_abi_version() == 2
     for code, name in B.STATUS.items():
         assert lib.muon_status_string(code).decode() == name
 
 
 def test_struct_layouts_match_header():
     # sizes the C compiler gives these structs on x86-64
-    assert ctypes.sizeof(B.MuonParam) == 64
+    assert ctypes.sizeof(B.MuonParam) == 96
     assert ctypes.sizeof(B.MuonHParams) == 48
     assert ctypes.sizeof(B.MuonChunkInfo) == 64
 
@@ -95,7 +95,13 @@ def test_validation_accepts_good_request(lib):
     (lambda e: setattr(e, "batch", 0), 1),
     (lambda e: setattr(e, "param_dtype", 7), 1),
     (lambda e: setattr(e, "grad_dtype", -1), 1),
-    (lambda e: setattr(e, "ld", 99), 2),
+    (lambda e: setattr(e, "ld", 15), 1),                      # ld < cols
+    (lambda e: setattr(e, "ld", 64), 1),                      # param row 4 is grad row 0
+    (lambda e: setattr(e, "row_block", 5), 1),                # does not divide rows
+    (lambda e: setattr(e, "row_block", -1), 1),
+    (lambda e: (setattr(e, "row_block", 4), setattr(e, "block_stride", 3 * 16)), 1),  # blocks overlap
+    (lambda e: setattr(e, "momentum_dense", 2), 1),
+    (lambda e: setattr(e, "reserved", 1), 1),
     (lambda e: setattr(e, "momentum", e.momentum + 2), 1),   # misaligned fp32
     (lambda e: setattr(e, "grad", e.param + 16), 1),          # grad overlaps param
     (lambda e: setattr(e, "momentum", e.grad), 1),            # momentum overlaps grad
@@ -120,6 +126,78 @@ def test_validation_allows_shared_gradients(lib):
     es[1].grad = es[0].grad  # two read-only buffers may alias
     st, msg = B.validate_step(es, hp())
     assert st == B.MUON_OK, msg
+
+
+def view(W, G, M, rows, cols, ld=0, rb=0, bs=0, batch=1, ps=0, mdense=0, dt=B.BF16):
+    return B.MuonParam(W, G, M, rows, cols, batch, ld, dt, dt, rb, bs, ps, mdense, 0)
+
+
+def fused_qkv(heads=4, hd=8, d=32, interleaved=True):
+    # one [3*heads*hd, d] bf16 weight (and its grad and fp32 momentum); the
+    # q, k, v matrices are [heads*hd, d] views: per-head interleaved row
+    # blocks, or three contiguous row ranges
+    W, G, M = BASE, BASE + (1 << 30), BASE + (2 << 30)
+    out = []
+    for j in range(3):
+        if interleaved:
+            off = j * hd * d
+            out.append(view(W + 2 * off, G + 2 * off, M + 4 * off, heads * hd, d,
+                            rb=hd, bs=3 * hd * d))
+        else:
+            off = j * heads * hd * d
+            out.append(view(W + 2 * off, G + 2 * off, M + 4 * off, heads * hd, d))
+    return out
+
+
+@pytest.mark.parametrize("interleaved", [True, False])
+def test_views_of_one_fused_weight_are_accepted(lib, interleaved):
+    st, msg = B.validate_step(fused_qkv(interleaved=interleaved), hp())
+    assert st == B.MUON_OK, msg
+
+
+def test_overlapping_views_are_rejected(lib):
+    es = fused_qkv()
+    es[1].param = es[0].param + 2 * 32  # k's head blocks start on q's second row
+    st, msg = B.validate_step(es, hp())
+    assert st == 1 and "overlap" in msg
+
+
+def test_column_halves_of_a_packed_weight(lib):
+    # [E, d, 2f] packed gate|up: two [E, d, f] views with ld = 2f
+    E, d, f = 3, 16, 24
+    W, G, M = BASE, BASE + (1 << 30), BASE + (2 << 30)
+    halves = [view(W + 2 * o, G + 2 * o, M + 4 * o, d, f, ld=2 * f, batch=E, ps=d * 2 * f)
+              for o in (0, f)]
+    st, msg = B.validate_step(halves, hp())
+    assert st == B.MUON_OK, msg
+    halves[1].param -= 2  # one column into the gate half
+    st, msg = B.validate_step(halves, hp())
+    assert st == 1
+    halves[1].param += 2
+    halves[1].plane_stride = d * 2 * f - 1  # planes would overlap each other
+    st, msg = B.validate_step(halves, hp())
+    assert st == 1
+
+
+def test_dense_momentum_for_a_strided_view(lib):
+    # momentum kept per logical matrix (dense) while param and grad are views
+    es = fused_qkv()
+    Mbase = BASE + (3 << 30)
+    for j, e in enumerate(es):
+        e.momentum = Mbase + 4 * j * 32 * 32
+        e.momentum_dense = 1
+    st, msg = B.validate_step(es, hp())
+    assert st == B.MUON_OK, msg
+    es[2].momentum = es[1].momentum + 4  # dense momenta overlap
+    st, _ = B.validate_step(es, hp())
+    assert st == 1
+
+
+def test_views_plan_like_their_dense_copies(lib):
+    st, chunks, ws, order = B.plan_step(fused_qkv(), hp())
+    st2, chunks2, ws2, order2 = B.plan_step(entries([(32, 32)] * 3), hp())
+    assert st == st2 == B.MUON_OK
+    assert chunks == chunks2 and ws == ws2 and order == order2
 
 
 @pytest.mark.parametrize("kw", [dict(ns_steps=-1), dict(ns_steps=65), dict(eps=-1.0),
