@@ -17,7 +17,10 @@
  *   momentum   buf' = beta*buf + (1-beta)*g ;
  *              u = (1-beta)*g + beta*buf' (nesterov) or u = buf'
  *   update     W' = (1 - lr*wd) * W - lr * scale * O,
- *              scale = 0.2*sqrt(max(rows, cols)) (scale_mode 0) or 1 (mode 1)
+ *              scale = 0.2*sqrt(max(rows, cols)) (scale_mode 0, Sec. 2.3),
+ *              1 (mode 1), or sqrt(max(1, rows/cols)) (mode 2, the rule of
+ *              the original Muon method that Sec. 2.3 and Sec. 6.2 keep as a
+ *              configurable legacy stage)
  *   eps        added to the Frobenius norm, outside the square root
  *   square     matrices (rows == cols) are not transposed
  *   ns_coeffs  NULL selects the constant quintic (3.4445, -4.7750, 2.0315).
@@ -104,6 +107,13 @@ typedef struct {
   int32_t momentum_dense;  /* 0: momentum has param's view; 1: momentum is a
                               dense batch x rows x cols array */
   int32_t reserved;        /* must be 0 */
+  /* Per-parameter configuration (Sec. 6.2: step count, coefficients and
+   * scaling are per-parameter stages).  Entries whose tables hold the same
+   * values are batched together; different tables never share a batch. */
+  const float* ns_coeffs;  /* host, ns_steps x 3 {a_k, b_k, c_k}: this entry's
+                              table; NULL: the call's (hparams) table */
+  int32_t ns_steps;        /* rows of ns_coeffs, 0..64 (ignored when NULL) */
+  int32_t scale_mode;      /* 0: the call's scale_mode; 1 + m: scale_mode m */
 } muon_param_t;
 
 typedef struct {
@@ -115,7 +125,8 @@ typedef struct {
   int32_t nesterov;        /* 0 or 1 */
   const float* ns_coeffs;  /* host array K x 3 {a_k, b_k, c_k}, or NULL */
   muon_ns_precision_t ns_precision;
-  int32_t scale_mode;      /* 0: 0.2*sqrt(max(rows, cols)); 1: none */
+  int32_t scale_mode;      /* 0: 0.2*sqrt(max(rows, cols)); 1: none;
+                              2: sqrt(max(1, rows/cols)) */
   int64_t max_chunk_elems; /* batch cap in elements of X; 0 = 2^29 (Sec. 6.6) */
 } muon_hparams_t;
 
@@ -126,6 +137,9 @@ typedef struct {
   int64_t first;           /* index of the chunk's first matrix in plan order */
   int64_t count;           /* matrices in the chunk */
   int32_t param_dtype, grad_dtype;
+  int32_t ns_steps;        /* K of the chunk's coefficient table */
+  int32_t coeff_set;       /* 0: the call's table; k > 0: the k-th distinct
+                              per-entry table, in entry order */
   size_t workspace_bytes;  /* workspace this chunk needs */
 } muon_chunk_info_t;
 
@@ -151,7 +165,8 @@ size_t muon_workspace_bytes(muon_handle_t h);
  *   param    <- (1 - lr*wd)*param - lr*scale*O                 (in place)
  * grad is only read.  param, grad and momentum of all entries must not
  * overlap (two grads may).  Matrices are grouped by (short side, long side,
- * dtypes), chunked at max_chunk_elems, and chunks run largest first.
+ * dtypes, coefficient table), chunked at max_chunk_elems, and chunks run
+ * largest first.
  */
 muon_status_t muon_step(muon_handle_t h, const muon_param_t* params, int64_t n,
                         const muon_hparams_t* hp, void* stream);

@@ -124,7 +124,8 @@ class MuonHParams:
     nesterov: bool = True
     # Per-step (a_k, b_k, c_k); None selects LEGACY_QUINTIC at every step.
     ns_coeffs: Optional[Sequence[Tuple[float, float, float]]] = None
-    # 0: multiply by 0.2*sqrt(max(m, n)) (Sec. 2.3); 1: no rescale.
+    # 0: multiply by 0.2*sqrt(max(m, n)) (Sec. 2.3); 1: no rescale;
+    # 2: sqrt(max(1, m/n)) (the original Muon rule; see rms_scale).
     scale_mode: int = 0
 
     def coefficient_table(self) -> List[Tuple[float, float, float]]:
@@ -199,8 +200,20 @@ def orthogonalize(G: np.ndarray, ns_steps: int = 5,
 
 
 def rms_scale(rows: int, cols: int, scale_mode: int = 0) -> float:
-    """RMS-matching factor 0.2*sqrt(max(m, n)) of Sec. 2.3 (1 when disabled)."""
-    return RMS_MATCH * float(np.sqrt(max(rows, cols))) if scale_mode == 0 else 1.0
+    """Update scale of the m x n matrix.
+
+    0: the RMS-matching factor 0.2*sqrt(max(m, n)) of Sec. 2.3;
+    1: no rescale;
+    2: sqrt(max(1, m/n)), the factor of the original Muon method, which
+       Sec. 2.3 and Sec. 6.2 keep as a configurable legacy stage.
+    """
+    if scale_mode == 0:
+        return RMS_MATCH * float(np.sqrt(max(rows, cols)))
+    if scale_mode == 1:
+        return 1.0
+    if scale_mode == 2:
+        return float(np.sqrt(max(1.0, rows / cols)))
+    raise ValueError("scale_mode must be 0, 1 or 2")
 
 
 def apply_update(W: np.ndarray, O: np.ndarray, lr: float, weight_decay: float,

@@ -35,7 +35,8 @@ class MuonParam(ctypes.Structure):
                 ("param_dtype", ctypes.c_int), ("grad_dtype", ctypes.c_int),
                 ("row_block", ctypes.c_int64), ("block_stride", ctypes.c_int64),
                 ("plane_stride", ctypes.c_int64), ("momentum_dense", ctypes.c_int32),
-                ("reserved", ctypes.c_int32)]
+                ("reserved", ctypes.c_int32), ("ns_coeffs", ctypes.POINTER(ctypes.c_float)),
+                ("ns_steps", ctypes.c_int32), ("scale_mode", ctypes.c_int32)]
 
 
 class MuonHParams(ctypes.Structure):
@@ -50,6 +51,7 @@ class MuonChunkInfo(ctypes.Structure):
     _fields_ = [("s", ctypes.c_int64), ("l", ctypes.c_int64), ("s_pad", ctypes.c_int64),
                 ("l_pad", ctypes.c_int64), ("first", ctypes.c_int64), ("count", ctypes.c_int64),
                 ("param_dtype", ctypes.c_int32), ("grad_dtype", ctypes.c_int32),
+                ("ns_steps", ctypes.c_int32), ("coeff_set", ctypes.c_int32),
                 ("workspace_bytes", ctypes.c_size_t)]
 
 
@@ -179,14 +181,22 @@ def _view(x):
     return t, E, rows, N, ld, rb, bs, ps
 
 
-def params_array(params, grads, moms):
-    """MuonParam[] for lists of logical matrices (see _view).  grad takes
-    the param's view; momentum takes it too, or is a dense
-    [M, N] / [E, M, N] tensor."""
+def params_array(params, grads, moms, entry_coeffs=None, entry_scale_modes=None):
+    """(MuonParam[], keepalive) for lists of logical matrices (see _view).
+    grad takes the param's view; momentum takes it too, or is a dense
+    [M, N] / [E, M, N] tensor.  entry_coeffs[i] (a K x 3 table) and
+    entry_scale_modes[i] override the call's for entry i; None keeps the
+    call's.  Keep the second item alive during the call."""
     import torch
     if not (len(params) == len(grads) == len(moms)):
         raise ValueError("params, grads and momenta must have equal length")
-    arr = (MuonParam * max(1, len(params)))()
+    n = len(params)
+    entry_coeffs = entry_coeffs or [None] * n
+    entry_scale_modes = entry_scale_modes or [None] * n
+    if len(entry_coeffs) != n or len(entry_scale_modes) != n:
+        raise ValueError("per-entry options need one item per entry")
+    arr = (MuonParam * max(1, n))()
+    keep = []
     for i, (W, g, m) in enumerate(zip(params, grads, moms)):
         vw, vg, vm = _view(W), _view(g), _view(m)
         if vw[1:] != vg[1:] or tuple(vw[0].shape) != tuple(vg[0].shape):
@@ -200,9 +210,18 @@ def params_array(params, grads, moms):
             mdense = 1
         else:
             raise ValueError(f"entry {i}: momentum must have the param's view or be dense")
+        ctab, csteps = None, 0
+        if entry_coeffs[i] is not None:
+            flat = [float(v) for r in entry_coeffs[i] for v in r]
+            csteps = len(flat) // 3
+            ctab = (ctypes.c_float * max(1, len(flat)))(*flat)
+            keep.append(ctab)
+        smode = 0 if entry_scale_modes[i] is None else 1 + int(entry_scale_modes[i])
         arr[i] = MuonParam(vw[0].data_ptr(), vg[0].data_ptr(), vm[0].data_ptr(), rows, cols, batch,
-                           ld, _dtype_code(vw[0]), _dtype_code(vg[0]), rb, bs, ps, mdense, 0)
-    return arr
+                           ld, _dtype_code(vw[0]), _dtype_code(vg[0]), rb, bs, ps, mdense, 0,
+                           ctypes.cast(ctab, ctypes.POINTER(ctypes.c_float)) if ctab else None,
+                           csteps, smode)
+    return arr, keep
 
 
 def _stream_ptr(stream) -> int:
@@ -261,13 +280,15 @@ class Muon:
     def workspace_bytes(self) -> int:
         return int(self.lib.muon_workspace_bytes(self.h))
 
-    def step(self, params, grads, moms, stream=None, **hp_kw):
-        """In place: momentum and params updated, grads read (muon_step)."""
-        arr = params_array(params, grads, moms)
+    def step(self, params, grads, moms, stream=None, entry_coeffs=None, entry_scale_modes=None,
+             **hp_kw):
+        """In place: momentum and params updated, grads read (muon_step).
+        entry_coeffs / entry_scale_modes: optional per-entry overrides."""
+        arr, keep_e = params_array(params, grads, moms, entry_coeffs, entry_scale_modes)
         hp, keep = make_hparams(**hp_kw)
         self._check(self.lib.muon_step(self.h, arr, len(params), ctypes.byref(hp),
                                        ctypes.c_void_p(_stream_ptr(stream))))
-        del keep
+        del keep, keep_e
 
     def orthogonalize(self, inputs, outputs, ns_steps=5, ns_coeffs=None, eps=1e-7,
                       ns_precision="bf16", stream=None):

@@ -128,7 +128,22 @@ struct Item {
   int32_t pdt, gdt;
   void* W; const void* g; float* buf; void* out;
   int64_t ld, rb, bs, ld_b, bs_b;
+  int32_t cset;            // coefficient table (index into the call's table list)
+  int32_t scale_mode;      // 0: 0.2 sqrt(max(m, n)); 1: none; 2: sqrt(max(1, m/n))
 };
+
+// The distinct coefficient tables of a call: [0] is the call's own table,
+// then every per-entry table whose values differ from all earlier ones.
+using CoeffTables = std::vector<std::vector<float>>;
+
+std::vector<float> coefficient_table(int K, const float* coeffs);
+
+int32_t table_id(CoeffTables& tables, std::vector<float> t) {
+  for (size_t i = 0; i < tables.size(); ++i)
+    if (tables[i] == t) return int32_t(i);
+  tables.push_back(std::move(t));
+  return int32_t(tables.size() - 1);
+}
 
 void set_dense(Item& it) {
   it.ld = it.ld_b = it.cols;
@@ -174,7 +189,7 @@ muon_status_t check_hparams(const muon_hparams_t* hp, Msg& msg) {
     msg.set("unknown ns_precision %d", int(hp->ns_precision));
     return MUON_ERR_INVALID_ARGUMENT;
   }
-  if (hp->scale_mode != 0 && hp->scale_mode != 1) { msg.set("scale_mode must be 0 or 1"); return MUON_ERR_INVALID_ARGUMENT; }
+  if (hp->scale_mode < 0 || hp->scale_mode > 2) { msg.set("scale_mode must be 0, 1 or 2"); return MUON_ERR_INVALID_ARGUMENT; }
   if (hp->max_chunk_elems < 0) { msg.set("max_chunk_elems must be >= 0"); return MUON_ERR_INVALID_ARGUMENT; }
   if (hp->ns_coeffs)
     for (int i = 0; i < 3 * hp->ns_steps; ++i)
@@ -221,9 +236,13 @@ void view_ranges(uintptr_t base, size_t es, int64_t rows, int64_t cols, int64_t 
 }
 
 muon_status_t validate_step(const muon_param_t* params, int64_t n, const muon_hparams_t* hp,
-                            std::vector<Item>* items, Msg& msg) {
+                            std::vector<Item>* items, CoeffTables* tables, Msg& msg) {
   muon_status_t st = check_hparams(hp, msg);
   if (st != MUON_OK) return st;
+  if (tables) {
+    tables->clear();
+    tables->push_back(coefficient_table(hp->ns_steps, hp->ns_coeffs));
+  }
   if (n < 0) { msg.set("n must be >= 0"); return MUON_ERR_INVALID_ARGUMENT; }
   if (n > 0 && !params) { msg.set("params is NULL"); return MUON_ERR_INVALID_ARGUMENT; }
   std::vector<Range> ranges;
@@ -270,6 +289,26 @@ muon_status_t validate_step(const muon_param_t* params, int64_t n, const muon_hp
       msg.set("entry %lld: view too large", (long long)i);
       return MUON_ERR_UNSUPPORTED;
     }
+    // per-parameter coefficient table and scale
+    if (p.ns_coeffs) {
+      if (p.ns_steps < 0 || p.ns_steps > kMaxSteps) {
+        msg.set("entry %lld: ns_steps must be in [0, %d]", (long long)i, kMaxSteps);
+        return MUON_ERR_INVALID_ARGUMENT;
+      }
+      for (int k = 0; k < 3 * p.ns_steps; ++k)
+        if (!std::isfinite(p.ns_coeffs[k])) {
+          msg.set("entry %lld: ns_coeffs[%d] is not finite", (long long)i, k);
+          return MUON_ERR_INVALID_ARGUMENT;
+        }
+    }
+    if (p.scale_mode < 0 || p.scale_mode > 3) {
+      msg.set("entry %lld: scale_mode must be 0 (the call's) or 1 + a scale_mode", (long long)i);
+      return MUON_ERR_INVALID_ARGUMENT;
+    }
+    int32_t cset = 0;
+    if (tables && p.ns_coeffs)
+      cset = table_id(*tables, std::vector<float>(p.ns_coeffs, p.ns_coeffs + 3 * p.ns_steps));
+    const int32_t smode = p.scale_mode ? p.scale_mode - 1 : hp->scale_mode;
     const bool mdense = p.momentum_dense != 0;
     const uintptr_t W = reinterpret_cast<uintptr_t>(p.param), G = reinterpret_cast<uintptr_t>(p.grad),
                     M = reinterpret_cast<uintptr_t>(p.momentum);
@@ -294,6 +333,8 @@ muon_status_t validate_step(const muon_param_t* params, int64_t n, const muon_hp
         it.ld = ld; it.rb = rb; it.bs = bs;
         it.ld_b = mdense ? p.cols : ld;
         it.bs_b = mdense ? rb * p.cols : bs;
+        it.cset = cset;
+        it.scale_mode = smode;
         // row blocks that follow each other at the row stride are no blocks
         if (it.bs == rb * it.ld && it.bs_b == rb * it.ld_b) {
           it.rb = p.rows;
@@ -345,6 +386,8 @@ muon_status_t validate_orth(const void* const* in, void* const* out, const int64
       it.pdt = dtype; it.gdt = dtype;
       it.W = nullptr; it.g = in[i]; it.buf = nullptr; it.out = out[i];
       set_dense(it);
+      it.cset = 0;
+      it.scale_mode = 1;
       items->push_back(it);
     }
   }
@@ -359,6 +402,7 @@ muon_status_t validate_orth(const void* const* in, void* const* out, const int64
 struct Chunk {
   int64_t s, l, S, L;
   int32_t pdt, gdt;
+  int32_t cset;
   int64_t first, count;
   size_t bytes;
   // byte offsets inside the workspace
@@ -373,22 +417,28 @@ struct Plan {
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
-Plan make_plan(const std::vector<Item>& items, int64_t cap, bool ns_f32) {
+// `steps[c]` is the step count of coefficient table c; the work of a
+// bucket is s^2 l per step (at least one, so K = 0 buckets keep their
+// shape order).
+Plan make_plan(const std::vector<Item>& items, int64_t cap, bool ns_f32, const std::vector<int>& steps) {
   if (cap <= 0) cap = kDefaultChunkElems;
-  using Key = std::tuple<int64_t, int64_t, int32_t, int32_t>;
+  using Key = std::tuple<int64_t, int64_t, int32_t, int32_t, int32_t>;
   std::map<Key, std::vector<int64_t>> buckets;
   std::map<Key, int64_t> first_seen;
   for (size_t i = 0; i < items.size(); ++i) {
     const Item& it = items[i];
-    Key k{std::min(it.rows, it.cols), std::max(it.rows, it.cols), it.pdt, it.gdt};
+    Key k{std::min(it.rows, it.cols), std::max(it.rows, it.cols), it.pdt, it.gdt, it.cset};
     if (!first_seen.count(k)) first_seen[k] = int64_t(i);
     buckets[k].push_back(int64_t(i));
   }
   std::vector<Key> keys;
   for (auto& kv : buckets) keys.push_back(kv.first);
+  auto work = [&](const Key& k) {
+    return double(std::get<0>(k)) * std::get<0>(k) * std::get<1>(k) *
+           std::max(1, steps[size_t(std::get<4>(k))]);
+  };
   std::stable_sort(keys.begin(), keys.end(), [&](const Key& a, const Key& b) {
-    const double wa = double(std::get<0>(a)) * std::get<0>(a) * std::get<1>(a);
-    const double wb = double(std::get<0>(b)) * std::get<0>(b) * std::get<1>(b);
+    const double wa = work(a), wb = work(b);
     if (wa != wb) return wa > wb;
     return first_seen[a] < first_seen[b];
   });
@@ -404,6 +454,7 @@ Plan make_plan(const std::vector<Item>& items, int64_t cap, bool ns_f32) {
       c.S = muon::round_up(s, muon::kPad);
       c.L = muon::round_up(l, muon::kPad);
       c.pdt = std::get<2>(k); c.gdt = std::get<3>(k);
+      c.cset = std::get<4>(k);
       c.first = int64_t(plan.order.size());
       c.count = std::min<int64_t>(per, int64_t(idx.size() - b));
       for (int64_t j = 0; j < c.count; ++j) plan.order.push_back(idx[b + size_t(j)]);
@@ -512,7 +563,7 @@ muon_status_t upload_table(muon_handle_t h, const std::vector<MatDesc>& table, h
   return MUON_OK;
 }
 
-MatDesc make_desc(const Item& it, double lr, double wd, int scale_mode) {
+MatDesc make_desc(const Item& it, double lr, double wd) {
   MatDesc d{};
   d.W = it.W; d.g = it.g; d.buf = it.buf; d.out = it.out;
   d.rows = int32_t(it.rows); d.cols = int32_t(it.cols);
@@ -528,21 +579,23 @@ MatDesc make_desc(const Item& it, double lr, double wd, int scale_mode) {
                      (!blocks || (it.bs % 8 == 0 && it.bs_b % 8 == 0));
   d.vec_ok = (d.dense ? (it.rows * it.cols) % 8 == 0 : rows8) && al16(it.g) && (!it.buf || al16(it.buf)) ? 1 : 0;
   d.vec4_ok = (it.cols % 4 == 0 && it.ld % 4 == 0 && (!blocks || it.bs % 4 == 0)) && al16(it.W ? it.W : it.out) ? 1 : 0;
-  const double scale = scale_mode == 0 ? 0.2 * std::sqrt(double(std::max(it.rows, it.cols))) : 1.0;
+  double scale = 1.0;
+  if (it.scale_mode == 0) scale = 0.2 * std::sqrt(double(std::max(it.rows, it.cols)));
+  else if (it.scale_mode == 2) scale = std::sqrt(std::max(1.0, double(it.rows) / double(it.cols)));
   d.upd_scale = float(lr * scale);
   d.decay = float(1.0 - lr * wd);
   return d;
 }
 
 muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Plan& plan,
-                      double lr, double wd, int scale_mode, const StepScalars& sc, bool ns_f32,
-                      const float* coeffs, int K, hipStream_t stream) {
+                      double lr, double wd, const StepScalars& sc, bool ns_f32,
+                      const CoeffTables& tables, hipStream_t stream) {
   DeviceGuard dg(h->device);
   if (!dg.ok) { set_err(h, "cannot select device %d", h->device); return MUON_ERR_DEVICE; }
   muon_status_t st = ensure_workspace(h, plan.ws_bytes);
   if (st != MUON_OK) return st;
   std::vector<MatDesc> table(plan.order.size());
-  for (size_t p = 0; p < plan.order.size(); ++p) table[p] = make_desc(items[size_t(plan.order[p])], lr, wd, scale_mode);
+  for (size_t p = 0; p < plan.order.size(); ++p) table[p] = make_desc(items[size_t(plan.order[p])], lr, wd);
   if ((st = upload_table(h, table, stream)) != MUON_OK) return st;
   char* ws = static_cast<char*>(h->ws);
   for (const Chunk& c : plan.chunks) {
@@ -558,7 +611,8 @@ muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Pla
     b.A = ws + c.off_A; b.B = ws + c.off_B;
     b.partials = reinterpret_cast<float*>(ws + c.off_part);
     b.rscale = reinterpret_cast<float*>(ws + c.off_r);
-    hipError_t e = muon::run_chunk(g, h->d_desc + c.first, b, sc, coeffs, K, stream,
+    const std::vector<float>& ct = tables[size_t(c.cset)];
+    hipError_t e = muon::run_chunk(g, h->d_desc + c.first, b, sc, ct.data(), int(ct.size() / 3), stream,
                                    h->profiling ? &h->timer : nullptr);
     if (e != hipSuccess) return device_fail(h, "kernel launch", e);
   }
@@ -570,6 +624,12 @@ std::vector<float> coefficient_table(int K, const float* coeffs) {
   for (int k = 0; k < K; ++k)
     for (int j = 0; j < 3; ++j) t[size_t(3 * k + j)] = coeffs ? coeffs[3 * k + j] : kLegacyQuintic[j];
   return t;
+}
+
+std::vector<int> step_counts(const CoeffTables& tables) {
+  std::vector<int> k;
+  for (const auto& t : tables) k.push_back(int(t.size() / 3));
+  return k;
 }
 
 }  // namespace
@@ -673,7 +733,7 @@ muon_status_t muon_validate_step(const muon_param_t* params, int64_t n, const mu
                                  char* msg, size_t msg_len) {
   Msg m{msg, msg_len};
   if (msg && msg_len) msg[0] = '\0';
-  return validate_step(params, n, hp, nullptr, m);
+  return validate_step(params, n, hp, nullptr, nullptr, m);
 }
 
 muon_status_t muon_plan_step(const muon_param_t* params, int64_t n, const muon_hparams_t* hp,
@@ -681,10 +741,11 @@ muon_status_t muon_plan_step(const muon_param_t* params, int64_t n, const muon_h
                              size_t* workspace_bytes, int64_t* order) {
   Msg m{nullptr, 0};
   std::vector<Item> items;
-  muon_status_t st = validate_step(params, n, hp, &items, m);
+  CoeffTables tables;
+  muon_status_t st = validate_step(params, n, hp, &items, &tables, m);
   if (st != MUON_OK) return st;
   if (cap > 0 && !chunks) return MUON_ERR_INVALID_ARGUMENT;
-  const Plan plan = make_plan(items, hp->max_chunk_elems, hp->ns_precision == MUON_NS_F32);
+  const Plan plan = make_plan(items, hp->max_chunk_elems, hp->ns_precision == MUON_NS_F32, step_counts(tables));
   if (n_chunks) *n_chunks = int64_t(plan.chunks.size());
   if (workspace_bytes) *workspace_bytes = plan.ws_bytes;
   for (int64_t i = 0; i < cap && i < int64_t(plan.chunks.size()); ++i) {
@@ -693,6 +754,8 @@ muon_status_t muon_plan_step(const muon_param_t* params, int64_t n, const muon_h
     o.s = c.s; o.l = c.l; o.s_pad = c.S; o.l_pad = c.L;
     o.first = c.first; o.count = c.count;
     o.param_dtype = c.pdt; o.grad_dtype = c.gdt;
+    o.ns_steps = int32_t(tables[size_t(c.cset)].size() / 3);
+    o.coeff_set = c.cset;
     o.workspace_bytes = c.bytes;
   }
   if (order)
@@ -707,11 +770,12 @@ muon_status_t muon_step(muon_handle_t h, const muon_param_t* params, int64_t n,
   char buf[256] = {0};
   Msg m{buf, sizeof buf};
   std::vector<Item> items;
-  muon_status_t st = validate_step(params, n, hp, &items, m);
+  CoeffTables tables;
+  muon_status_t st = validate_step(params, n, hp, &items, &tables, m);
   if (st != MUON_OK) { h->err = buf; return st; }
   if (items.empty()) return MUON_OK;
   const bool f32 = hp->ns_precision == MUON_NS_F32;
-  const Plan plan = make_plan(items, hp->max_chunk_elems, f32);
+  const Plan plan = make_plan(items, hp->max_chunk_elems, f32, step_counts(tables));
   StepScalars sc{};
   sc.beta = hp->beta;
   sc.one_minus_beta = 1.0f - hp->beta;
@@ -719,9 +783,8 @@ muon_status_t muon_step(muon_handle_t h, const muon_param_t* params, int64_t n,
   sc.momentum = 1;
   sc.eps = hp->eps;
   sc.final_kind = 0;
-  const std::vector<float> coeffs = coefficient_table(hp->ns_steps, hp->ns_coeffs);
-  return execute(h, items, plan, hp->lr, hp->weight_decay, hp->scale_mode, sc, f32, coeffs.data(),
-                 hp->ns_steps, static_cast<hipStream_t>(stream));
+  return execute(h, items, plan, hp->lr, hp->weight_decay, sc, f32, tables,
+                 static_cast<hipStream_t>(stream));
 }
 
 muon_status_t ns_orthogonalize_batched(muon_handle_t h, const void* const* in, void* const* out,
@@ -737,14 +800,13 @@ muon_status_t ns_orthogonalize_batched(muon_handle_t h, const void* const* in, v
   if (st != MUON_OK) { h->err = buf; return st; }
   if (items.empty()) return MUON_OK;
   const bool f32 = prec == MUON_NS_F32;
-  const Plan plan = make_plan(items, 0, f32);
+  const CoeffTables tables{coefficient_table(ns_steps, ns_coeffs)};
+  const Plan plan = make_plan(items, 0, f32, step_counts(tables));
   StepScalars sc{};
   sc.momentum = 0;
   sc.eps = eps;
   sc.final_kind = 1;
-  const std::vector<float> coeffs = coefficient_table(ns_steps, ns_coeffs);
-  return execute(h, items, plan, 0.0, 0.0, 1, sc, f32, coeffs.data(), ns_steps,
-                 static_cast<hipStream_t>(stream));
+  return execute(h, items, plan, 0.0, 0.0, sc, f32, tables, static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

@@ -46,9 +46,9 @@ def test_abi_version_and_status_strings(lib):
 
 def test_struct_layouts_match_header():
     # sizes the C compiler gives these structs on x86-64
-    assert ctypes.sizeof(B.MuonParam) == 96
+    assert ctypes.sizeof(B.MuonParam) == 112
     assert ctypes.sizeof(B.MuonHParams) == 48
-    assert ctypes.sizeof(B.MuonChunkInfo) == 64
+    assert ctypes.sizeof(B.MuonChunkInfo) == 72
 
 
 # fake, never dereferenced device addresses for host-only checks
@@ -102,6 +102,8 @@ def test_validation_accepts_good_request(lib):
     (lambda e: (setattr(e, "row_block", 4), setattr(e, "block_stride", 3 * 16)), 1),  # blocks overlap
     (lambda e: setattr(e, "momentum_dense", 2), 1),
     (lambda e: setattr(e, "reserved", 1), 1),
+    (lambda e: setattr(e, "scale_mode", 4), 1),
+    (lambda e: setattr(e, "scale_mode", -1), 1),
     (lambda e: setattr(e, "momentum", e.momentum + 2), 1),   # misaligned fp32
     (lambda e: setattr(e, "grad", e.param + 16), 1),          # grad overlaps param
     (lambda e: setattr(e, "momentum", e.grad), 1),            # momentum overlaps grad
@@ -198,6 +200,52 @@ def test_views_plan_like_their_dense_copies(lib):
     st2, chunks2, ws2, order2 = B.plan_step(entries([(32, 32)] * 3), hp())
     assert st == st2 == B.MUON_OK
     assert chunks == chunks2 and ws == ws2 and order == order2
+
+
+def table(rows):
+    flat = [float(v) for r in rows for v in r]
+    arr = (ctypes.c_float * len(flat))(*flat)
+    table.keep.append(arr)
+    return ctypes.cast(arr, ctypes.POINTER(ctypes.c_float)), len(rows)
+
+
+table.keep = []
+CUBIC = [(1.5, -0.5, 0.0)] * 3
+
+
+def test_per_entry_tables_batch_by_value(lib):
+    # entries 1 and 3 carry equal cubic tables (separate arrays), entry 2
+    # carries the call's own table by value: two batches, {0, 2} and {1, 3}
+    es = entries([(32, 32)] * 4)
+    es[1].ns_coeffs, es[1].ns_steps = table(CUBIC)
+    es[3].ns_coeffs, es[3].ns_steps = table(CUBIC)
+    es[2].ns_coeffs, es[2].ns_steps = table([(3.4445, -4.7750, 2.0315)] * 5)
+    st, chunks, _, order = B.plan_step(es, hp())
+    assert st == B.MUON_OK
+    got = {(c["coeff_set"], c["ns_steps"]): order[c["first"]:c["first"] + c["count"]] for c in chunks}
+    assert got == {(0, 5): [0, 2], (1, 3): [1, 3]}
+
+
+def test_per_entry_table_with_more_steps_runs_first(lib):
+    # same shape, 8 steps against the call's 5: more work, so first
+    es = entries([(64, 64)] * 2)
+    es[1].ns_coeffs, es[1].ns_steps = table([(1.5, -0.5, 0.0)] * 8)
+    st, chunks, _, order = B.plan_step(es, hp())
+    assert st == B.MUON_OK and [c["ns_steps"] for c in chunks] == [8, 5] and order == [1, 0]
+
+
+@pytest.mark.parametrize("steps,rows", [(65, [(1.0, 0.0, 0.0)] * 65), (1, [(1.0, float("nan"), 0.0)])])
+def test_per_entry_table_is_validated(lib, steps, rows):
+    es = entries([(16, 16)])
+    es[0].ns_coeffs, _ = table(rows)
+    es[0].ns_steps = steps
+    st, msg = B.validate_step(es, hp())
+    assert st == 1 and msg
+
+
+def test_call_scale_mode_range(lib):
+    assert B.validate_step(entries([(8, 8)]), hp(scale_mode=2))[0] == B.MUON_OK
+    assert B.validate_step(entries([(8, 8)]), hp(scale_mode=3))[0] == 1
 
 
 @pytest.mark.parametrize("kw", [dict(ns_steps=-1), dict(ns_steps=65), dict(eps=-1.0),

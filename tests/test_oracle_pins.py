@@ -323,6 +323,18 @@ def test_apply_scale_uses_long_side(shape):
     np.testing.assert_allclose((W - r1.W_new) / 0.05, r1.O, rtol=1e-12, atol=1e-15)
 
 
+@pytest.mark.parametrize("shape,factor", [((16, 4), 2.0), ((4, 16), 1.0), ((9, 4), 1.5), ((5, 5), 1.0)])
+def test_apply_original_muon_scale(shape, factor):
+    # scale_mode 2: sqrt(max(1, rows/cols)); the factors are worked by hand
+    rng = np.random.default_rng(14)
+    W, g = rng.standard_normal(shape), rng.standard_normal(shape)
+    hp = ref.MuonHParams(lr=0.05, weight_decay=0.0, scale_mode=2)
+    r = ref.muon_step_matrix(W, g, np.zeros(shape), hp)
+    np.testing.assert_allclose((W - r.W_new) / (0.05 * factor), r.O, rtol=1e-12, atol=1e-15)
+    with pytest.raises(ValueError):
+        ref.rms_scale(4, 4, 3)
+
+
 def test_batched_and_expert_stacks_equal_single_matrices():
     rng = np.random.default_rng(13)
     shapes = [(5, 7), (3, 4, 6), (8, 3)]
