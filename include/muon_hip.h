@@ -183,6 +183,42 @@ muon_status_t ns_orthogonalize_batched(muon_handle_t h, const void* const* in,
                                        int32_t ns_steps, const float* ns_coeffs, float eps,
                                        muon_ns_precision_t prec, void* stream);
 
+/*
+ * AdamW for the parameters Muon does not take: Sec. 6.4 (Fig. "muon-
+ * grouping") sends one-dimensional and scalar parameters to AdamW through a
+ * chained optimizer, with decoupled weight decay.  The paper prints no
+ * formula; this is AdamW with decoupled decay and bias correction, per
+ * element, in fp32:
+ *   m' = beta1*m + (1-beta1)*g          v' = beta2*v + (1-beta2)*g^2
+ *   p' = (1 - lr*wd)*p - lr/(1 - beta1^t) * m' / (sqrt(v'/(1 - beta2^t)) + eps)
+ * for step t (t = 1 on the first call).  Every tensor is taken as `numel`
+ * contiguous elements.  param, exp_avg and exp_avg_sq are updated in place;
+ * grad is only read.  Buffers of different entries must not overlap (grads
+ * may).  Enqueued on `stream` like muon_step, and ordered after the
+ * handle's earlier calls.
+ */
+typedef struct {
+  void* param;             /* in/out: numel, param_dtype */
+  const void* grad;        /* in:     numel, grad_dtype */
+  float* exp_avg;          /* in/out: numel, fp32 (m) */
+  float* exp_avg_sq;       /* in/out: numel, fp32 (v) */
+  int64_t numel;           /* >= 0 */
+  muon_dtype_t param_dtype;
+  muon_dtype_t grad_dtype;
+} muon_adamw_param_t;
+
+typedef struct {
+  float lr;                /* finite */
+  float beta1, beta2;      /* in [0, 1) */
+  float eps;               /* finite, > 0 */
+  float weight_decay;      /* finite */
+  int32_t reserved;        /* must be 0 */
+  int64_t step;            /* t >= 1 */
+} muon_adamw_hparams_t;
+
+muon_status_t muon_adamw_step(muon_handle_t h, const muon_adamw_param_t* params, int64_t n,
+                              const muon_adamw_hparams_t* hp, void* stream);
+
 /* Host-only checks and planning (no device needed).  muon_validate_step
  * returns the status muon_step would return for these arguments before
  * launching anything and writes the reason into msg (may be NULL). */
@@ -209,7 +245,7 @@ muon_status_t muon_plan_step(const muon_param_t* params, int64_t n, const muon_h
  *               written once.
  * Families (in this order): momentum_norm, norm_finalize,
  * normalize_transpose, gram_syrk, poly_syrk, update_gemm, update_apply_gemm,
- * apply_x0.  `reset` != 0 clears the counters after reading. */
+ * apply_x0, adamw.  `reset` != 0 clears the counters after reading. */
 typedef struct {
   const char* name;
   int64_t launches;

@@ -18,7 +18,8 @@ What is computed (paper: HyperParallel-FSDP, arXiv 2609.21594):
 * Sec. 6.3: a fused expert weight [E, M, N] is E independent [M, N] matrices;
   it is never flattened.
 * Sec. 6.4 and Fig. "muon-grouping": the update is applied together with
-  decoupled weight decay.
+  decoupled weight decay; one-dimensional and scalar parameters leave Muon
+  for AdamW through a chained optimizer (adamw_step at the end).
 
 Readings where the paper is silent (each is listed in the design notes):
 
@@ -33,7 +34,11 @@ Readings where the paper is silent (each is listed in the design notes):
 * the default coefficient table is the constant quintic (3.4445, -4.7750,
   2.0315) of the original Muon method the paper cites as its legacy set; the
   paper prints neither that set nor its asymmetric five-step default, so any
-  per-step table can be passed in.
+  per-step table can be passed in;
+* scale_mode 2, sqrt(max(1, m/n)), is the original Muon method's scale,
+  which the paper keeps as a configurable legacy stage without printing it;
+* AdamW (which the paper names but does not define) has exponential moments,
+  bias correction by 1 - beta^t and decoupled decay on the old value.
 
 Every floating-point step runs in fp64.  Inputs are decoded exactly; results
 are rounded once, from fp64, to the storage type (round to nearest, ties to
@@ -263,3 +268,36 @@ def muon_step(params: Sequence[np.ndarray], grads: Sequence[np.ndarray],
             raise ValueError("Muon takes matrices or stacks of matrices only")
     return out
 
+
+
+# ---------------------------------------------------------------------------
+# AdamW for the parameters Muon does not take.  Sec. 6.4 (and the decision
+# flow of Fig. "muon-grouping") sends one-dimensional and scalar parameters to
+# AdamW through a chained optimizer, with decoupled weight decay.  The paper
+# prints no formula, so this is AdamW as commonly defined: exponential
+# moments, bias correction by 1 - beta^t, decoupled decay on the old value.
+# ---------------------------------------------------------------------------
+@dataclass
+class AdamWHParams:
+    lr: float = 1e-3
+    beta1: float = 0.9
+    beta2: float = 0.999
+    eps: float = 1e-8
+    weight_decay: float = 0.0
+
+
+def adamw_step(p, g, m, v, step: int, hp: AdamWHParams):
+    """One AdamW step (t = step >= 1) on arrays of any shape; returns
+    (p', m', v') in fp64:
+        m' = beta1 m + (1 - beta1) g,   v' = beta2 v + (1 - beta2) g^2,
+        p' = (1 - lr wd) p - lr * (m' / (1 - beta1^t)) / (sqrt(v' / (1 - beta2^t)) + eps).
+    """
+    if step < 1:
+        raise ValueError("step must be >= 1")
+    p, g, m, v = (np.asarray(a, dtype=np.float64) for a in (p, g, m, v))
+    m_new = hp.beta1 * m + (1.0 - hp.beta1) * g
+    v_new = hp.beta2 * v + (1.0 - hp.beta2) * g * g
+    m_hat = m_new / (1.0 - hp.beta1 ** step)
+    v_hat = v_new / (1.0 - hp.beta2 ** step)
+    p_new = (1.0 - hp.lr * hp.weight_decay) * p - hp.lr * m_hat / (np.sqrt(v_hat) + hp.eps)
+    return p_new, m_new, v_new

@@ -47,6 +47,19 @@ class MuonHParams(ctypes.Structure):
                 ("scale_mode", ctypes.c_int32), ("max_chunk_elems", ctypes.c_int64)]
 
 
+class AdamWParam(ctypes.Structure):
+    _fields_ = [("param", ctypes.c_void_p), ("grad", ctypes.c_void_p),
+                ("exp_avg", ctypes.c_void_p), ("exp_avg_sq", ctypes.c_void_p),
+                ("numel", ctypes.c_int64), ("param_dtype", ctypes.c_int),
+                ("grad_dtype", ctypes.c_int)]
+
+
+class AdamWHParams(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+                ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float),
+                ("reserved", ctypes.c_int32), ("step", ctypes.c_int64)]
+
+
 class MuonChunkInfo(ctypes.Structure):
     _fields_ = [("s", ctypes.c_int64), ("l", ctypes.c_int64), ("s_pad", ctypes.c_int64),
                 ("l_pad", ctypes.c_int64), ("first", ctypes.c_int64), ("count", ctypes.c_int64),
@@ -64,7 +77,7 @@ class MuonKernelStats(ctypes.Structure):
 EXPORTS = ["muon_create", "muon_destroy", "muon_reserve", "muon_set_workspace_limit",
            "muon_workspace_bytes", "muon_step", "ns_orthogonalize_batched",
            "muon_validate_step", "muon_plan_step", "muon_status_string", "muon_last_error",
-           "muon_abi_version", "muon_profile_enable", "muon_profile_read"]
+           "muon_abi_version", "muon_profile_enable", "muon_profile_read", "muon_adamw_step"]
 
 _lib: Optional[ctypes.CDLL] = None
 
@@ -95,6 +108,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.muon_plan_step.argtypes = [ctypes.POINTER(MuonParam), i64, ctypes.POINTER(MuonHParams),
                                    ctypes.POINTER(MuonChunkInfo), i64, ctypes.POINTER(i64),
                                    ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(i64)]
+    lib.muon_adamw_step.argtypes = [vp, ctypes.POINTER(AdamWParam), i64, ctypes.POINTER(AdamWHParams), vp]
     lib.muon_profile_enable.argtypes = [vp, ctypes.c_int]
     lib.muon_profile_read.argtypes = [vp, ctypes.POINTER(MuonKernelStats), ctypes.c_int,
                                       ctypes.POINTER(ctypes.c_int), ctypes.c_int]
@@ -104,7 +118,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.muon_last_error.restype = ctypes.c_char_p
     for name in ("muon_create", "muon_destroy", "muon_reserve", "muon_set_workspace_limit",
                  "muon_step", "ns_orthogonalize_batched", "muon_validate_step", "muon_plan_step",
-                 "muon_profile_enable", "muon_profile_read"):
+                 "muon_profile_enable", "muon_profile_read", "muon_adamw_step"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -289,6 +303,29 @@ class Muon:
         self._check(self.lib.muon_step(self.h, arr, len(params), ctypes.byref(hp),
                                        ctypes.c_void_p(_stream_ptr(stream))))
         del keep, keep_e
+
+    def adamw_step(self, params, grads, exp_avgs, exp_avg_sqs, step, lr=1e-3, betas=(0.9, 0.999),
+                   eps=1e-8, weight_decay=0.0, stream=None):
+        """AdamW on contiguous tensors of any shape (muon_adamw_step): params
+        and both moments updated in place, grads read; `step` is t >= 1."""
+        n = len(params)
+        if not (len(grads) == len(exp_avgs) == len(exp_avg_sqs) == n):
+            raise ValueError("params, grads and moments must have equal length")
+        arr = (AdamWParam * max(1, n))()
+        for i, (p, g, m, v) in enumerate(zip(params, grads, exp_avgs, exp_avg_sqs)):
+            if not (p.numel() == g.numel() == m.numel() == v.numel()):
+                raise ValueError(f"entry {i}: element counts differ")
+            for t in (p, g, m, v):
+                if not t.is_contiguous():
+                    raise ValueError(f"entry {i}: tensors must be contiguous")
+            if _dtype_code(m) != F32 or _dtype_code(v) != F32:
+                raise TypeError(f"entry {i}: moments must be float32")
+            arr[i] = AdamWParam(p.data_ptr(), g.data_ptr(), m.data_ptr(), v.data_ptr(), p.numel(),
+                                _dtype_code(p), _dtype_code(g))
+        hp = AdamWHParams(float(lr), float(betas[0]), float(betas[1]), float(eps), float(weight_decay),
+                          0, int(step))
+        self._check(self.lib.muon_adamw_step(self.h, arr, n, ctypes.byref(hp),
+                                             ctypes.c_void_p(_stream_ptr(stream))))
 
     def orthogonalize(self, inputs, outputs, ns_steps=5, ns_coeffs=None, eps=1e-7,
                       ns_precision="bf16", stream=None):

@@ -69,6 +69,17 @@ struct EventTimer : muon::LaunchTimer {
   }
 };
 
+// A descriptor table in device memory, filled from pinned staging memory.
+struct DeviceTable {
+  void* dev = nullptr;               // device copy
+  size_t dev_cap = 0;                // bytes
+  void* host = nullptr;              // pinned staging for the upload
+  size_t host_cap = 0;
+  hipEvent_t staged = nullptr;       // the last upload out of `host` has completed
+  bool pending = false;
+  std::vector<char> last;            // content of `dev`
+};
+
 struct muon_handle {
   int device = 0;
   bool profiling = false;
@@ -76,13 +87,14 @@ struct muon_handle {
   void* ws = nullptr;
   size_t ws_bytes = 0;
   size_t ws_limit = 0;               // 0 = no cap
-  MatDesc* d_desc = nullptr;         // device descriptor table
-  size_t desc_cap = 0;               // entries
-  MatDesc* h_stage = nullptr;        // pinned staging for the table upload
-  size_t stage_cap = 0;
-  hipEvent_t stage_done = nullptr;   // last upload out of h_stage has completed
-  bool stage_pending = false;
-  std::vector<MatDesc> last_table;   // content of d_desc
+  DeviceTable mats;                  // MatDesc per matrix (muon_step, orthogonalize)
+  DeviceTable adams;                 // AdamDesc per tensor (muon_adamw_step)
+  // Every call's work uses the workspace and the tables; a call on another
+  // stream than the previous one waits (on the device) for the previous
+  // call's work first.
+  hipEvent_t call_done = nullptr;
+  hipStream_t last_stream = nullptr;
+  bool have_last = false;
   std::string err;
 };
 
@@ -519,48 +531,77 @@ muon_status_t ensure_workspace(muon_handle_t h, size_t bytes) {
   return MUON_OK;
 }
 
-// Puts `table` into h->d_desc on `stream`, skipping the copy when the device
-// table already holds exactly these bytes.
-muon_status_t upload_table(muon_handle_t h, const std::vector<MatDesc>& table, hipStream_t stream) {
-  if (table.size() == h->last_table.size() &&
-      std::memcmp(table.data(), h->last_table.data(), table.size() * sizeof(MatDesc)) == 0)
-    return MUON_OK;
+// Puts `bytes` bytes at `data` into t.dev on `stream`, skipping the copy
+// when the device table already holds exactly these bytes.  The caller has
+// ordered `stream` after every earlier call's work (begin_call).
+muon_status_t upload_table(muon_handle_t h, DeviceTable& t, const void* data, size_t bytes,
+                           hipStream_t stream) {
+  if (bytes == t.last.size() && std::memcmp(data, t.last.data(), bytes) == 0) return MUON_OK;
   hipError_t e;
-  if (table.size() > h->desc_cap) {
-    const size_t cap = std::max(table.size(), size_t(256));
-    if (h->d_desc) {
+  if (bytes > t.dev_cap) {
+    const size_t cap = std::max(bytes, size_t(16384));
+    if (t.dev) {
       if ((e = hipDeviceSynchronize()) != hipSuccess) return device_fail(h, "hipDeviceSynchronize", e);
-      if ((e = hipFree(h->d_desc)) != hipSuccess) return device_fail(h, "hipFree", e);
-      h->d_desc = nullptr; h->desc_cap = 0;
+      if ((e = hipFree(t.dev)) != hipSuccess) return device_fail(h, "hipFree", e);
+      t.dev = nullptr; t.dev_cap = 0; t.last.clear();
     }
-    if ((e = hipMalloc(&h->d_desc, cap * sizeof(MatDesc))) != hipSuccess) {
+    if ((e = hipMalloc(&t.dev, cap)) != hipSuccess) {
       (void)hipGetLastError();
-      set_err(h, "hipMalloc of the descriptor table failed");
+      set_err(h, "hipMalloc of a descriptor table failed");
       return MUON_ERR_OUT_OF_MEMORY;
     }
-    h->desc_cap = cap;
+    t.dev_cap = cap;
   }
-  if (h->stage_pending) {
-    if ((e = hipEventSynchronize(h->stage_done)) != hipSuccess) return device_fail(h, "hipEventSynchronize", e);
-    h->stage_pending = false;
+  if (t.pending) {
+    if ((e = hipEventSynchronize(t.staged)) != hipSuccess) return device_fail(h, "hipEventSynchronize", e);
+    t.pending = false;
   }
-  if (table.size() > h->stage_cap) {
-    if (h->h_stage) { (void)hipHostFree(h->h_stage); h->h_stage = nullptr; h->stage_cap = 0; }
-    const size_t cap = std::max(table.size(), size_t(256));
-    if ((e = hipHostMalloc(reinterpret_cast<void**>(&h->h_stage), cap * sizeof(MatDesc), hipHostMallocDefault)) != hipSuccess) {
+  if (bytes > t.host_cap) {
+    if (t.host) { (void)hipHostFree(t.host); t.host = nullptr; t.host_cap = 0; }
+    const size_t cap = std::max(bytes, size_t(16384));
+    if ((e = hipHostMalloc(&t.host, cap, hipHostMallocDefault)) != hipSuccess) {
       (void)hipGetLastError();
-      set_err(h, "hipHostMalloc of the descriptor staging buffer failed");
+      set_err(h, "hipHostMalloc of a descriptor staging buffer failed");
       return MUON_ERR_OUT_OF_MEMORY;
     }
-    h->stage_cap = cap;
+    t.host_cap = cap;
   }
-  std::memcpy(h->h_stage, table.data(), table.size() * sizeof(MatDesc));
-  if ((e = hipMemcpyAsync(h->d_desc, h->h_stage, table.size() * sizeof(MatDesc), hipMemcpyHostToDevice, stream)) != hipSuccess)
+  std::memcpy(t.host, data, bytes);
+  if ((e = hipMemcpyAsync(t.dev, t.host, bytes, hipMemcpyHostToDevice, stream)) != hipSuccess)
     return device_fail(h, "hipMemcpyAsync", e);
-  if ((e = hipEventRecord(h->stage_done, stream)) != hipSuccess) return device_fail(h, "hipEventRecord", e);
-  h->stage_pending = true;
-  h->last_table = table;
+  if ((e = hipEventRecord(t.staged, stream)) != hipSuccess) return device_fail(h, "hipEventRecord", e);
+  t.pending = true;
+  t.last.assign(static_cast<const char*>(data), static_cast<const char*>(data) + bytes);
   return MUON_OK;
+}
+
+// Orders `stream` after the previous call's work when that ran on another
+// stream (the workspace and the tables are shared by all calls).
+muon_status_t begin_call(muon_handle_t h, hipStream_t stream) {
+  if (h->have_last && stream != h->last_stream) {
+    const hipError_t e = hipStreamWaitEvent(stream, h->call_done, 0);
+    if (e != hipSuccess) return device_fail(h, "hipStreamWaitEvent", e);
+  }
+  return MUON_OK;
+}
+
+muon_status_t end_call(muon_handle_t h, hipStream_t stream) {
+  const hipError_t e = hipEventRecord(h->call_done, stream);
+  if (e != hipSuccess) return device_fail(h, "hipEventRecord", e);
+  h->last_stream = stream;
+  h->have_last = true;
+  return MUON_OK;
+}
+
+bool create_table(DeviceTable& t) {
+  return hipEventCreateWithFlags(&t.staged, hipEventDisableTiming) == hipSuccess;
+}
+
+void destroy_table(DeviceTable& t) {
+  if (t.dev) (void)hipFree(t.dev);
+  if (t.host) (void)hipHostFree(t.host);
+  if (t.staged) (void)hipEventDestroy(t.staged);
+  t = DeviceTable();
 }
 
 MatDesc make_desc(const Item& it, double lr, double wd) {
@@ -594,9 +635,11 @@ muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Pla
   if (!dg.ok) { set_err(h, "cannot select device %d", h->device); return MUON_ERR_DEVICE; }
   muon_status_t st = ensure_workspace(h, plan.ws_bytes);
   if (st != MUON_OK) return st;
+  if ((st = begin_call(h, stream)) != MUON_OK) return st;
   std::vector<MatDesc> table(plan.order.size());
   for (size_t p = 0; p < plan.order.size(); ++p) table[p] = make_desc(items[size_t(plan.order[p])], lr, wd);
-  if ((st = upload_table(h, table, stream)) != MUON_OK) return st;
+  if ((st = upload_table(h, h->mats, table.data(), table.size() * sizeof(MatDesc), stream)) != MUON_OK) return st;
+  const MatDesc* d_desc = static_cast<const MatDesc*>(h->mats.dev);
   char* ws = static_cast<char*>(h->ws);
   for (const Chunk& c : plan.chunks) {
     ChunkGeom g{};
@@ -612,10 +655,49 @@ muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Pla
     b.partials = reinterpret_cast<float*>(ws + c.off_part);
     b.rscale = reinterpret_cast<float*>(ws + c.off_r);
     const std::vector<float>& ct = tables[size_t(c.cset)];
-    hipError_t e = muon::run_chunk(g, h->d_desc + c.first, b, sc, ct.data(), int(ct.size() / 3), stream,
+    hipError_t e = muon::run_chunk(g, d_desc + c.first, b, sc, ct.data(), int(ct.size() / 3), stream,
                                    h->profiling ? &h->timer : nullptr);
     if (e != hipSuccess) return device_fail(h, "kernel launch", e);
   }
+  return end_call(h, stream);
+}
+
+// AdamW: checks, then one launch per (param, grad) dtype pair over the
+// tensors of that pair.
+muon_status_t validate_adamw(const muon_adamw_param_t* params, int64_t n, const muon_adamw_hparams_t* hp,
+                             Msg& msg) {
+  if (!hp) { msg.set("hparams is NULL"); return MUON_ERR_INVALID_ARGUMENT; }
+  if (!std::isfinite(hp->lr) || !std::isfinite(hp->weight_decay) || !std::isfinite(hp->eps) ||
+      !(hp->eps > 0.f)) {
+    msg.set("lr and weight_decay must be finite, eps finite and > 0");
+    return MUON_ERR_INVALID_ARGUMENT;
+  }
+  if (!(hp->beta1 >= 0.f && hp->beta1 < 1.f) || !(hp->beta2 >= 0.f && hp->beta2 < 1.f)) {
+    msg.set("beta1 and beta2 must be in [0, 1)");
+    return MUON_ERR_INVALID_ARGUMENT;
+  }
+  if (hp->step < 1) { msg.set("step must be >= 1"); return MUON_ERR_INVALID_ARGUMENT; }
+  if (hp->reserved != 0) { msg.set("reserved must be 0"); return MUON_ERR_INVALID_ARGUMENT; }
+  if (n < 0) { msg.set("n must be >= 0"); return MUON_ERR_INVALID_ARGUMENT; }
+  if (n > 0 && !params) { msg.set("params is NULL"); return MUON_ERR_INVALID_ARGUMENT; }
+  std::vector<Range> ranges;
+  for (int64_t i = 0; i < n; ++i) {
+    const muon_adamw_param_t& p = params[i];
+    if (p.numel < 0 || p.numel > (int64_t(1) << 40)) { msg.set("entry %lld: numel out of range", (long long)i); return MUON_ERR_INVALID_ARGUMENT; }
+    if (p.numel == 0) continue;
+    if (!p.param || !p.grad || !p.exp_avg || !p.exp_avg_sq) { msg.set("entry %lld: NULL pointer", (long long)i); return MUON_ERR_INVALID_ARGUMENT; }
+    if (!dtype_ok(p.param_dtype) || !dtype_ok(p.grad_dtype)) { msg.set("entry %lld: unknown dtype", (long long)i); return MUON_ERR_INVALID_ARGUMENT; }
+    const uintptr_t P = reinterpret_cast<uintptr_t>(p.param), G = reinterpret_cast<uintptr_t>(p.grad),
+                    M = reinterpret_cast<uintptr_t>(p.exp_avg), V = reinterpret_cast<uintptr_t>(p.exp_avg_sq);
+    const size_t ps = dtype_size(p.param_dtype), gs = dtype_size(p.grad_dtype);
+    if (P % ps || G % gs || M % 4 || V % 4) { msg.set("entry %lld: pointer not aligned to its element size", (long long)i); return MUON_ERR_INVALID_ARGUMENT; }
+    const uintptr_t ne = uintptr_t(p.numel);
+    ranges.push_back({P, P + ne * ps, true});
+    ranges.push_back({G, G + ne * gs, false});
+    ranges.push_back({M, M + ne * 4, true});
+    ranges.push_back({V, V + ne * 4, true});
+  }
+  if (!ranges_disjoint(ranges)) { msg.set("param, grad and moment buffers overlap"); return MUON_ERR_INVALID_ARGUMENT; }
   return MUON_OK;
 }
 
@@ -661,7 +743,11 @@ muon_status_t muon_create(muon_handle_t* out, int device) {
   if (!h) return MUON_ERR_OUT_OF_MEMORY;
   h->device = device;
   DeviceGuard dg(device);
-  if (!dg.ok || hipEventCreateWithFlags(&h->stage_done, hipEventDisableTiming) != hipSuccess) {
+  if (!dg.ok || !create_table(h->mats) || !create_table(h->adams) ||
+      hipEventCreateWithFlags(&h->call_done, hipEventDisableTiming) != hipSuccess) {
+    destroy_table(h->mats);
+    destroy_table(h->adams);
+    if (h->call_done) (void)hipEventDestroy(h->call_done);
     delete h;
     return MUON_ERR_DEVICE;
   }
@@ -676,9 +762,9 @@ muon_status_t muon_destroy(muon_handle_t h) {
     DeviceGuard dg(h->device);
     if (hipDeviceSynchronize() != hipSuccess) st = MUON_ERR_DEVICE;
     if (h->ws) (void)hipFree(h->ws);
-    if (h->d_desc) (void)hipFree(h->d_desc);
-    if (h->h_stage) (void)hipHostFree(h->h_stage);
-    if (h->stage_done) (void)hipEventDestroy(h->stage_done);
+    destroy_table(h->mats);
+    destroy_table(h->adams);
+    if (h->call_done) (void)hipEventDestroy(h->call_done);
     h->timer.destroy();
   }
   delete h;
@@ -710,7 +796,7 @@ muon_status_t muon_profile_read(muon_handle_t h, muon_kernel_stats_t* out, int c
                                 int reset) {
   static const char* const kNames[muon::KK_COUNT] = {
       "momentum_norm", "norm_finalize", "normalize_transpose", "gram_syrk",
-      "poly_syrk", "update_gemm", "update_apply_gemm", "apply_x0"};
+      "poly_syrk", "update_gemm", "update_apply_gemm", "apply_x0", "adamw"};
   if (!h || (cap > 0 && !out)) return MUON_ERR_INVALID_ARGUMENT;
   DeviceGuard dg(h->device);
   const bool ok = h->timer.collect();
@@ -785,6 +871,67 @@ muon_status_t muon_step(muon_handle_t h, const muon_param_t* params, int64_t n,
   sc.final_kind = 0;
   return execute(h, items, plan, hp->lr, hp->weight_decay, sc, f32, tables,
                  static_cast<hipStream_t>(stream));
+}
+
+muon_status_t muon_adamw_step(muon_handle_t h, const muon_adamw_param_t* params, int64_t n,
+                              const muon_adamw_hparams_t* hp, void* stream_) {
+  if (!h) return MUON_ERR_INVALID_ARGUMENT;
+  h->err.clear();
+  char buf[256] = {0};
+  Msg m{buf, sizeof buf};
+  muon_status_t st = validate_adamw(params, n, hp, m);
+  if (st != MUON_OK) { h->err = buf; return st; }
+  const hipStream_t stream = static_cast<hipStream_t>(stream_);
+  // tensors grouped by dtype pair; workgroup ranges per group
+  std::vector<muon::AdamDesc> table;
+  struct Group { int pdt, gdt; size_t first, count; int64_t blocks; double bytes; };
+  std::vector<Group> groups;
+  for (int pdt : {MUON_BF16, MUON_F32})
+    for (int gdt : {MUON_BF16, MUON_F32}) {
+      Group gr{pdt, gdt, table.size(), 0, 0, 0.0};
+      for (int64_t i = 0; i < n; ++i) {
+        const muon_adamw_param_t& p = params[i];
+        if (p.numel == 0 || p.param_dtype != pdt || p.grad_dtype != gdt) continue;
+        muon::AdamDesc d{};
+        d.p = p.param; d.g = p.grad; d.m = p.exp_avg; d.v = p.exp_avg_sq;
+        d.numel = p.numel;
+        d.first_block = gr.blocks;
+        const auto al16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
+        d.vec_ok = p.numel % 8 == 0 && al16(p.param) && al16(p.grad) && al16(p.exp_avg) && al16(p.exp_avg_sq);
+        gr.blocks += (p.numel + muon::kAdamElemsPerBlock - 1) / muon::kAdamElemsPerBlock;
+        gr.bytes += double(p.numel) * (2.0 * dtype_size(pdt) + dtype_size(gdt) + 16.0);
+        table.push_back(d);
+        ++gr.count;
+      }
+      if (gr.count) groups.push_back(gr);
+    }
+  if (table.empty()) return MUON_OK;
+  for (const Group& gr : groups)
+    if (gr.blocks > int64_t(INT32_MAX)) { set_err(h, "too many elements in one dtype group"); return MUON_ERR_UNSUPPORTED; }
+  DeviceGuard dg(h->device);
+  if (!dg.ok) { set_err(h, "cannot select device %d", h->device); return MUON_ERR_DEVICE; }
+  if ((st = begin_call(h, stream)) != MUON_OK) return st;
+  if ((st = upload_table(h, h->adams, table.data(), table.size() * sizeof(muon::AdamDesc), stream)) != MUON_OK)
+    return st;
+  // scalars: bias corrections in double, then fp32
+  const double t = double(hp->step);
+  const double bc1 = 1.0 - std::pow(double(hp->beta1), t), bc2 = 1.0 - std::pow(double(hp->beta2), t);
+  muon::AdamScalars sc{};
+  sc.decay = float(1.0 - double(hp->lr) * double(hp->weight_decay));
+  sc.beta1 = hp->beta1; sc.one_minus_beta1 = float(1.0 - double(hp->beta1));
+  sc.beta2 = hp->beta2; sc.one_minus_beta2 = float(1.0 - double(hp->beta2));
+  sc.step_size = float(double(hp->lr) / bc1);
+  sc.inv_sqrt_bc2 = float(1.0 / std::sqrt(bc2));
+  sc.eps = hp->eps;
+  const muon::AdamDesc* d = static_cast<const muon::AdamDesc*>(h->adams.dev);
+  for (const Group& gr : groups) {
+    const hipError_t e = muon::run_adamw(d + gr.first, int(gr.count), gr.blocks,
+                                         gr.pdt == MUON_BF16 ? muon::DT_BF16 : muon::DT_F32,
+                                         gr.gdt == MUON_BF16 ? muon::DT_BF16 : muon::DT_F32, sc, gr.bytes,
+                                         stream, h->profiling ? &h->timer : nullptr);
+    if (e != hipSuccess) return device_fail(h, "kernel launch", e);
+  }
+  return end_call(h, stream);
 }
 
 muon_status_t ns_orthogonalize_batched(muon_handle_t h, const void* const* in, void* const* out,

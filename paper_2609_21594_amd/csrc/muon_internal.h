@@ -86,7 +86,7 @@ struct StepScalars {
 // Kernel families, for the optional per-launch timing.
 enum KernelKind : int {
   KK_PARTIALS = 0, KK_FINALIZE, KK_NORMALIZE, KK_GRAM, KK_POLY, KK_UPDATE, KK_FINAL,
-  KK_APPLY_X0, KK_COUNT
+  KK_APPLY_X0, KK_ADAMW, KK_COUNT
 };
 
 // Receives a bracket around every launch when timing is enabled.
@@ -100,6 +100,41 @@ inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 inline int64_t norm_blocks(int64_t numel) {
   return (numel + kNormElemsPerBlock - 1) / kNormElemsPerBlock;
 }
+
+// ---------------------------------------------------------------------------
+// AdamW for the parameters Muon does not take (1-D and scalar ones; Sec. 6.4
+// delegates them to AdamW through a chained optimizer).
+// ---------------------------------------------------------------------------
+// Elements one workgroup updates.
+constexpr int kAdamElemsPerBlock = 8192;
+
+// One tensor of an AdamW call (device-resident table).
+struct AdamDesc {
+  void* p;              // parameter, param dtype
+  const void* g;        // gradient, grad dtype
+  float* m;             // first moment, fp32
+  float* v;             // second moment, fp32
+  int64_t numel;
+  int64_t first_block;  // workgroups of the launch before this tensor's
+  int32_t vec_ok;       // 8 elements at a time: numel % 8 == 0 and 16-byte aligned
+  int32_t reserved[3];
+};
+static_assert(sizeof(AdamDesc) == 64, "AdamDesc layout");
+
+// Per-call scalars: p' = p*decay - step_size * m' / (sqrt(v')*inv_sqrt_bc2 + eps),
+// m' = beta1*m + (1-beta1)*g, v' = beta2*v + (1-beta2)*g^2.
+struct AdamScalars {
+  float decay;          // 1 - lr*wd
+  float beta1, one_minus_beta1, beta2, one_minus_beta2;
+  float step_size;      // lr / (1 - beta1^t)
+  float inv_sqrt_bc2;   // 1 / sqrt(1 - beta2^t)
+  float eps;
+};
+
+// Updates n tensors of one (param, grad) dtype pair: `blocks` workgroups.
+hipError_t run_adamw(const AdamDesc* d_desc, int n, int64_t blocks, int param_dtype,
+                     int grad_dtype, const AdamScalars& sc, double bytes, hipStream_t stream,
+                     LaunchTimer* timer);
 
 // Enqueues the whole step for one chunk on `stream`: momentum + partial
 // norms, norm finalisation, normalise + transpose-first + cast, K

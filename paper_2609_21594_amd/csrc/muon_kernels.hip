@@ -1611,4 +1611,104 @@ hipError_t run_chunk(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBuff
              : run_chunk_t<float, uint16_t>(cg, d_desc, wb, sc, coeffs, K, st, timer);
 }
 
+// ---------------------------------------------------------------------------
+// AdamW over many tensors in one launch: workgroup b updates elements
+// [8192 j, 8192 (j + 1)) of the tensor whose range of workgroups holds b
+// (found by binary search over first_block).  HBM-bound: each element reads
+// p, g, m, v and writes p, m, v once; 8 consecutive elements per thread
+// (16-byte accesses) when the tensor allows it.
+// ---------------------------------------------------------------------------
+template <typename PT, typename GT>
+__device__ __forceinline__ void adam_one(float& p, float g, float& m, float& v, const AdamScalars& sc) {
+  m = fmaf(sc.beta1, m, sc.one_minus_beta1 * g);
+  v = fmaf(sc.beta2, v, sc.one_minus_beta2 * (g * g));
+  const float denom = fmaf(sqrtf(v), sc.inv_sqrt_bc2, sc.eps);
+  p = fmaf(p, sc.decay, -sc.step_size * (m / denom));
+}
+
+template <typename T>
+__device__ __forceinline__ void load8(const T* base, int64_t i, float out[8]) {
+  if constexpr (sizeof(T) == 2) {
+    const u32x4_t raw = *reinterpret_cast<const u32x4_t*>(base + i);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      out[2 * q] = __uint_as_float(raw[q] << 16);
+      out[2 * q + 1] = __uint_as_float(raw[q] & 0xffff0000u);
+    }
+  } else {
+    const float4 a = *reinterpret_cast<const float4*>(base + i);
+    const float4 b = *reinterpret_cast<const float4*>(base + i + 4);
+    out[0] = a.x; out[1] = a.y; out[2] = a.z; out[3] = a.w;
+    out[4] = b.x; out[5] = b.y; out[6] = b.z; out[7] = b.w;
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void store8(T* base, int64_t i, const float in[8]) {
+  if constexpr (sizeof(T) == 2) {
+    u32x4_t raw;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) raw[q] = pack_bf16x2(in[2 * q], in[2 * q + 1]);
+    *reinterpret_cast<u32x4_t*>(base + i) = raw;
+  } else {
+    *reinterpret_cast<float4*>(base + i) = make_float4(in[0], in[1], in[2], in[3]);
+    *reinterpret_cast<float4*>(base + i + 4) = make_float4(in[4], in[5], in[6], in[7]);
+  }
+}
+
+template <typename PT, typename GT>
+__global__ __launch_bounds__(256) void k_adamw(const AdamDesc* __restrict__ desc, int n, AdamScalars sc) {
+  const int64_t b = blockIdx.x;
+  int lo = 0, hi = n - 1;  // last tensor with first_block <= b
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (desc[mid].first_block <= b) lo = mid;
+    else hi = mid - 1;
+  }
+  const AdamDesc a = desc[lo];
+  const int64_t start = (b - a.first_block) * kAdamElemsPerBlock;
+  const int64_t end = min(a.numel, start + static_cast<int64_t>(kAdamElemsPerBlock));
+  PT* __restrict__ p = static_cast<PT*>(a.p);
+  const GT* __restrict__ g = static_cast<const GT*>(a.g);
+  float* __restrict__ m = a.m;
+  float* __restrict__ v = a.v;
+  if (a.vec_ok) {
+    for (int64_t i = start + threadIdx.x * 8; i < end; i += 256 * 8) {
+      float pv[8], gv[8], mv[8], vv[8];
+      load8(p, i, pv);
+      load8(g, i, gv);
+      load8(m, i, mv);
+      load8(v, i, vv);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) adam_one<PT, GT>(pv[q], gv[q], mv[q], vv[q], sc);
+      store8(p, i, pv);
+      store8(m, i, mv);
+      store8(v, i, vv);
+    }
+  } else {
+    for (int64_t i = start + threadIdx.x; i < end; i += 256) {
+      float pv = to_f32<PT>(p[i]), mv = m[i], vv = v[i];
+      adam_one<PT, GT>(pv, to_f32<GT>(g[i]), mv, vv, sc);
+      p[i] = from_f32<PT>(pv);
+      m[i] = mv;
+      v[i] = vv;
+    }
+  }
+}
+
+hipError_t run_adamw(const AdamDesc* d_desc, int n, int64_t blocks, int param_dtype, int grad_dtype,
+                     const AdamScalars& sc, double bytes, hipStream_t st, LaunchTimer* timer) {
+  if (n <= 0 || blocks <= 0) return hipSuccess;
+  Timed tm(timer, KK_ADAMW, st);
+  const dim3 grid(static_cast<unsigned>(blocks)), block(256);
+  const bool pb = param_dtype == DT_BF16, gb = grad_dtype == DT_BF16;
+  if (pb && gb) hipLaunchKernelGGL((k_adamw<uint16_t, uint16_t>), grid, block, 0, st, d_desc, n, sc);
+  else if (pb) hipLaunchKernelGGL((k_adamw<uint16_t, float>), grid, block, 0, st, d_desc, n, sc);
+  else if (gb) hipLaunchKernelGGL((k_adamw<float, uint16_t>), grid, block, 0, st, d_desc, n, sc);
+  else hipLaunchKernelGGL((k_adamw<float, float>), grid, block, 0, st, d_desc, n, sc);
+  const hipError_t e = hipGetLastError();
+  if (e == hipSuccess) tm.done(0, 0, bytes);
+  return e;
+}
+
 }  // namespace muon
