@@ -17,6 +17,13 @@ the product it computes) per launch over its mean launch duration, both from
 HIP events the library records around each launch on its own stream.
 cpu_baseline: the fp64 CPU oracle on a bounded sample of the same workload
 (one matrix of each shape bucket), extrapolated to the workload's mix.
+
+Side measurements on workload 3 (not part of `value`):
+views: the same step with every layer's q, k and v taken as zero-copy,
+  head-interleaved views of one fused QKV weight (and its gradient and
+  momentum), as a model adapter would hand them over;
+adamw: the chained AdamW over the parameters a 7B-like model leaves to it
+  (embedding and output head 2 x 32000 x 4096, 65 norm weights of 4096).
 """
 from __future__ import annotations
 
@@ -120,6 +127,73 @@ def cpu_baseline(wl, inputs):
             "sample": (f"fp64 NumPy oracle, one full {'orthogonalisation' if wl.orthogonalize_only else 'Muon step'} on one matrix per shape bucket "
                        f"({'; '.join(sampled)}), extrapolated by bucket counts to all "
                        f"{len(wl.matrices)} matrices; {cores} BLAS threads on {cpu}")}
+
+
+def views_step(muon, W, G, B, wl, hp, steps, warmup):
+    """ms per step of workload 3 with q, k, v as head-interleaved views of a
+    fused [3*4096, 4096] QKV weight per layer (32 heads of 128 rows, ordered
+    q_h, k_h, v_h per head), its gradient and momentum."""
+    import torch
+    from paper_2609_21594_amd.binding import RowBlocks
+    H, hd = 32, 128
+    names = [m.name for m in wl.matrices]
+    Wv, Gv, Bv, keep = [], [], [], []
+    for layer in sorted({n.split(".")[0] for n in names}, key=lambda x: int(x[1:])):
+        idx = [names.index(f"{layer}.{p}") for p in ("q", "k", "v")]
+        fused = []
+        for T in (W, G, B):
+            F = torch.empty((H, 3, hd, T[idx[0]].shape[1]), dtype=T[idx[0]].dtype, device="cuda")
+            for j, i in enumerate(idx):
+                F[:, j] = T[i].view(H, hd, -1)
+            fused.append(F)
+        keep.append(fused)
+        for j in range(3):
+            for lst, F in zip((Wv, Gv, Bv), fused):
+                lst.append(RowBlocks(F[:, j]))
+        for p in ("o", "gate", "up", "down"):
+            i = names.index(f"{layer}.{p}")
+            Wv.append(W[i]); Gv.append(G[i]); Bv.append(B[i])
+    for _ in range(warmup):
+        muon.step(Wv, Gv, Bv, **hp)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        muon.step(Wv, Gv, Bv, **hp)
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / steps
+
+
+def adamw_bench(muon, steps, warmup):
+    """The chained AdamW over a 7B-like model's AdamW parameters:
+    embedding and output head (2 x 32000 x 4096) and 65 norm weights of
+    4096; bf16 parameters and gradients, fp32 moments; seeded normal
+    values.  Rate = algorithmic bytes (22 per element) over kernel time."""
+    import torch
+    sizes = [32000 * 4096] * 2 + [4096] * 65
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(2609)
+    P = [(0.02 * torch.randn(n, generator=gen, device="cuda")).to(torch.bfloat16) for n in sizes]
+    Gr = [(1e-3 * torch.randn(n, generator=gen, device="cuda")).to(torch.bfloat16) for n in sizes]
+    M = [torch.zeros(n, device="cuda") for n in sizes]
+    V = [torch.zeros(n, device="cuda") for n in sizes]
+    kw = dict(lr=3e-4, betas=(0.9, 0.95), eps=1e-8, weight_decay=0.1)
+    for t in range(1, warmup + 1):
+        muon.adamw_step(P, Gr, M, V, t, **kw)
+    torch.cuda.synchronize()
+    muon.profile(True)
+    muon.profile_read(reset=True)
+    t0 = time.perf_counter()
+    for t in range(warmup + 1, warmup + steps + 1):
+        muon.adamw_step(P, Gr, M, V, t, **kw)
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t0) * 1e3 / steps
+    st = muon.profile_read(reset=True)["adamw"]
+    muon.profile(False)
+    n = sum(sizes)
+    gbs = st["bytes"] / (st["total_ms"] * 1e-3) / 1e9
+    return {"workload": "7B-like AdamW set: 2 x 32000x4096 + 65 x 4096, bf16 params/grads, fp32 moments",
+            "elements": n, "ms_per_step": wall_ms, "kernel_ms": st["total_ms"] / steps,
+            "bytes_per_elem": 22, "gbs": gbs, "frac_hbm": gbs / PEAK_HBM_GBS}
 
 
 def reference_gemm(wl):
@@ -295,6 +369,13 @@ def main():
         "kernels": kernels,
         "input_generation_s": gen_s,
     }
+    if wl.index == 3:
+        vms = views_step(muon, W, G, B, wl, hp, args.steps, args.warmup)
+        out["views"] = {"workload": "same, q/k/v as head-interleaved views of fused QKV weights",
+                        "ms_per_step": vms, "vs_dense": vms / ms}
+        del W, G, B
+        torch.cuda.empty_cache()
+        out["adamw"] = adamw_bench(muon, args.steps, args.warmup)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, inputs)
     muon.close()
