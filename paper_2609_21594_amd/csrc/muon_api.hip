@@ -620,6 +620,7 @@ MatDesc make_desc(const Item& it, double lr, double wd) {
                      (!blocks || (it.bs % 8 == 0 && it.bs_b % 8 == 0));
   d.vec_ok = (d.dense ? (it.rows * it.cols) % 8 == 0 : rows8) && al16(it.g) && (!it.buf || al16(it.buf)) ? 1 : 0;
   d.vec4_ok = (it.cols % 4 == 0 && it.ld % 4 == 0 && (!blocks || it.bs % 4 == 0)) && al16(it.W ? it.W : it.out) ? 1 : 0;
+  d.row8_ok = rows8 && al16(it.g) && (!it.buf || al16(it.buf)) ? 1 : 0;
   double scale = 1.0;
   if (it.scale_mode == 0) scale = 0.2 * std::sqrt(double(std::max(it.rows, it.cols)));
   else if (it.scale_mode == 2) scale = std::sqrt(std::max(1.0, double(it.rows) / double(it.cols)));

@@ -38,7 +38,8 @@ struct MatDesc {
   int64_t ld, bstride;  // row and row-block strides of W, g, out (elements)
   int64_t ld_b, bstride_b;  // the same for buf
   int32_t rb;           // rows per row block (rows when not interleaved)
-  int32_t reserved[3];
+  int32_t row8_ok;      // every row of g (and buf) starts 16-byte aligned and cols % 8 == 0
+  int32_t reserved[2];
 };
 static_assert(sizeof(MatDesc) == 112, "MatDesc layout");
 

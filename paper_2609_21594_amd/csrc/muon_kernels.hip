@@ -68,6 +68,38 @@ __device__ __forceinline__ void store_from_f32(void* p, int64_t i, int dt, float
   else static_cast<float*>(p)[i] = v;
 }
 
+// 8 consecutive elements at base + i (16-byte aligned) as fp32, and back
+// (bf16 rounded to nearest even).
+template <typename T>
+__device__ __forceinline__ void load8(const T* base, int64_t i, float out[8]) {
+  if constexpr (sizeof(T) == 2) {
+    const u32x4_t raw = *reinterpret_cast<const u32x4_t*>(base + i);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      out[2 * q] = __uint_as_float(raw[q] << 16);
+      out[2 * q + 1] = __uint_as_float(raw[q] & 0xffff0000u);
+    }
+  } else {
+    const float4 a = *reinterpret_cast<const float4*>(base + i);
+    const float4 b = *reinterpret_cast<const float4*>(base + i + 4);
+    out[0] = a.x; out[1] = a.y; out[2] = a.z; out[3] = a.w;
+    out[4] = b.x; out[5] = b.y; out[6] = b.z; out[7] = b.w;
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void store8(T* base, int64_t i, const float in[8]) {
+  if constexpr (sizeof(T) == 2) {
+    u32x4_t raw;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) raw[q] = pack_bf16x2(in[2 * q], in[2 * q + 1]);
+    *reinterpret_cast<u32x4_t*>(base + i) = raw;
+  } else {
+    *reinterpret_cast<float4*>(base + i) = make_float4(in[0], in[1], in[2], in[3]);
+    *reinterpret_cast<float4*>(base + i + 4) = make_float4(in[4], in[5], in[6], in[7]);
+  }
+}
+
 // Fixed-order sum over a 256-thread block: butterfly within each 64-lane
 // wavefront, then the four wave sums in wave order.  Deterministic.
 __device__ __forceinline__ float block_sum_256(float v, float* red4) {
@@ -197,10 +229,12 @@ __global__ __launch_bounds__(256) void k_finalize(const float* __restrict__ part
 
 // ---------------------------------------------------------------------------
 // X0 = r*u with transpose-first.  A workgroup owns a 64x64 tile of the
-// padded X extent (S x L); it reads the matching tile of u row by row
-// (coalesced), writes it unchanged into whichever of X / X^T has u's layout,
-// and transposes it through LDS into the other.  Zero outside the matrix.
-// grid = (L/64, S/64, matrices).
+// padded X extent (S x L).  It reads the matching tile of u row-wise, 8
+// consecutive elements per access (16-byte loads of g and buf where the rows
+// allow it, element by element at ragged edges), writes it unchanged into
+// whichever of X / X^T has u's layout (16-byte stores), and transposes it
+// through LDS into the other (16-byte stores of 8 elements of one column).
+// Zero outside the matrix.  grid = (L/64, S/64, matrices).
 // ---------------------------------------------------------------------------
 template <typename GT, typename XT, bool MOM>
 __global__ __launch_bounds__(256) void k_normalize(const MatDesc* __restrict__ desc,
@@ -226,31 +260,45 @@ __global__ __launch_bounds__(256) void k_normalize(const MatDesc* __restrict__ d
   const float r = rscale[m];
   const GT* __restrict__ g = static_cast<const GT*>(md.g);
   const float beta = sc.beta, omb = sc.one_minus_beta;
-  const int col = threadIdx.x & 63;
-#pragma unroll 4
-  for (int row = threadIdx.x >> 6; row < 64; row += 4) {
+  auto u_of = [&](float gv, float bn) { return MOM ? (sc.nesterov ? fmaf(beta, bn, omb * gv) : bn) : gv; };
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int c = threadIdx.x + 256 * k;          // chunk: row c / 8, columns 8 (c % 8) ..
+    const int row = c >> 3, col = (c & 7) * 8;
     const int ur = ur0 + row, uc = uc0 + col;
-    float v = 0.f;
-    if (ur < md.rows && uc < md.cols) {
-      const float gv = to_f32<GT>(g[view_index(md, ur, uc)]);
-      float u;
-      if (MOM) {
-        const float bn = md.buf[buf_index(md, ur, uc)];  // already updated by k_partials
-        u = sc.nesterov ? fmaf(beta, bn, omb * gv) : bn;
-      } else {
-        u = gv;
+    float v[8];
+    if (md.row8_ok && ur < md.rows && uc + 8 <= md.cols) {
+      float gv[8], bv[8];
+      load8(g, view_index(md, ur, uc), gv);
+      if (MOM) load8(md.buf, buf_index(md, ur, uc), bv);  // already updated by k_partials
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = u_of(gv[q], MOM ? bv[q] : 0.f) * r;
+    } else {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        v[q] = 0.f;
+        if (ur < md.rows && uc + q < md.cols) {
+          const float gv = to_f32<GT>(g[view_index(md, ur, uc + q)]);
+          v[q] = u_of(gv, MOM ? md.buf[buf_index(md, ur, uc + q)] : 0.f) * r;
+        }
       }
-      v = u * r;
     }
-    const XT xv = from_f32<XT>(v);
-    if (D) D[static_cast<int64_t>(ur) * ldD + uc] = xv;
-    tile[row * LDT + col] = xv;
+    if (D) store8(D, static_cast<int64_t>(ur) * ldD + uc, v);
+    if (Tb) {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) tile[row * LDT + col + q] = from_f32<XT>(v[q]);
+    }
   }
   if (!Tb) return;  // uniform over the block
   __syncthreads();
-#pragma unroll 4
-  for (int trow = threadIdx.x >> 6; trow < 64; trow += 4) {
-    Tb[static_cast<int64_t>(uc0 + trow) * ldT + ur0 + col] = tile[col * LDT + trow];
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int c = threadIdx.x + 256 * k;          // row c / 8 of the transpose, 8 (c % 8) ..
+    const int trow = c >> 3, r8 = (c & 7) * 8;
+    float v[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[q] = to_f32<XT>(tile[(r8 + q) * LDT + trow]);
+    store8(Tb, static_cast<int64_t>(uc0 + trow) * ldT + ur0 + r8, v);
   }
 }
 
@@ -1624,36 +1672,6 @@ __device__ __forceinline__ void adam_one(float& p, float g, float& m, float& v, 
   v = fmaf(sc.beta2, v, sc.one_minus_beta2 * (g * g));
   const float denom = fmaf(sqrtf(v), sc.inv_sqrt_bc2, sc.eps);
   p = fmaf(p, sc.decay, -sc.step_size * (m / denom));
-}
-
-template <typename T>
-__device__ __forceinline__ void load8(const T* base, int64_t i, float out[8]) {
-  if constexpr (sizeof(T) == 2) {
-    const u32x4_t raw = *reinterpret_cast<const u32x4_t*>(base + i);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      out[2 * q] = __uint_as_float(raw[q] << 16);
-      out[2 * q + 1] = __uint_as_float(raw[q] & 0xffff0000u);
-    }
-  } else {
-    const float4 a = *reinterpret_cast<const float4*>(base + i);
-    const float4 b = *reinterpret_cast<const float4*>(base + i + 4);
-    out[0] = a.x; out[1] = a.y; out[2] = a.z; out[3] = a.w;
-    out[4] = b.x; out[5] = b.y; out[6] = b.z; out[7] = b.w;
-  }
-}
-
-template <typename T>
-__device__ __forceinline__ void store8(T* base, int64_t i, const float in[8]) {
-  if constexpr (sizeof(T) == 2) {
-    u32x4_t raw;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) raw[q] = pack_bf16x2(in[2 * q], in[2 * q + 1]);
-    *reinterpret_cast<u32x4_t*>(base + i) = raw;
-  } else {
-    *reinterpret_cast<float4*>(base + i) = make_float4(in[0], in[1], in[2], in[3]);
-    *reinterpret_cast<float4*>(base + i + 4) = make_float4(in[4], in[5], in[6], in[7]);
-  }
 }
 
 template <typename PT, typename GT>
