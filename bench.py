@@ -57,6 +57,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-side", action="store_true",
+                    help="skip the views and AdamW side measurements (counter runs)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this size (HBM counter calibration)")
     ap.add_argument("--reference-gemm", action="store_true",
@@ -369,7 +371,7 @@ def main():
         "kernels": kernels,
         "input_generation_s": gen_s,
     }
-    if wl.index == 3:
+    if wl.index == 3 and not args.no_side:
         vms = views_step(muon, W, G, B, wl, hp, args.steps, args.warmup)
         out["views"] = {"workload": "same, q/k/v as head-interleaved views of fused QKV weights",
                         "ms_per_step": vms, "vs_dense": vms / ms}
