@@ -149,6 +149,16 @@ typedef struct {
 muon_status_t muon_create(muon_handle_t* out, int device);
 muon_status_t muon_destroy(muon_handle_t h);
 
+/* Chunks of one call that leave compute units idle (their symmetric
+ * products fill the last round of tiles less than 90%) run on a second
+ * stream owned by the handle, beside the chunks on `stream`; the call forks
+ * from and joins back into `stream` through events, so its work is still
+ * ordered on `stream` as a whole.  Such a call uses up to twice the
+ * workspace muon_plan_step reports (never beyond the workspace limit: then
+ * it runs on `stream` alone).  Results are bitwise the same either way.
+ * streams: 2 (the default) or 1 (everything on the caller's stream). */
+muon_status_t muon_set_streams(muon_handle_t h, int streams);
+
 /* Grows the workspace to at least `bytes` now (hipMalloc synchronises, so do
  * this before timing).  Fails with MUON_ERR_OUT_OF_MEMORY above the limit. */
 muon_status_t muon_reserve(muon_handle_t h, size_t bytes);

@@ -77,7 +77,8 @@ class MuonKernelStats(ctypes.Structure):
 EXPORTS = ["muon_create", "muon_destroy", "muon_reserve", "muon_set_workspace_limit",
            "muon_workspace_bytes", "muon_step", "ns_orthogonalize_batched",
            "muon_validate_step", "muon_plan_step", "muon_status_string", "muon_last_error",
-           "muon_abi_version", "muon_profile_enable", "muon_profile_read", "muon_adamw_step"]
+           "muon_abi_version", "muon_profile_enable", "muon_profile_read", "muon_adamw_step",
+           "muon_set_streams"]
 
 _lib: Optional[ctypes.CDLL] = None
 
@@ -110,6 +111,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                    ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(i64)]
     lib.muon_adamw_step.argtypes = [vp, ctypes.POINTER(AdamWParam), i64, ctypes.POINTER(AdamWHParams), vp]
     lib.muon_profile_enable.argtypes = [vp, ctypes.c_int]
+    lib.muon_set_streams.argtypes = [vp, ctypes.c_int]
     lib.muon_profile_read.argtypes = [vp, ctypes.POINTER(MuonKernelStats), ctypes.c_int,
                                       ctypes.POINTER(ctypes.c_int), ctypes.c_int]
     lib.muon_status_string.argtypes = [ctypes.c_int]
@@ -118,7 +120,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.muon_last_error.restype = ctypes.c_char_p
     for name in ("muon_create", "muon_destroy", "muon_reserve", "muon_set_workspace_limit",
                  "muon_step", "ns_orthogonalize_batched", "muon_validate_step", "muon_plan_step",
-                 "muon_profile_enable", "muon_profile_read", "muon_adamw_step"):
+                 "muon_profile_enable", "muon_profile_read", "muon_adamw_step", "muon_set_streams"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -274,6 +276,10 @@ class Muon:
 
     def reserve(self, nbytes: int):
         self._check(self.lib.muon_reserve(self.h, int(nbytes)))
+
+    def set_streams(self, n: int):
+        """2 (default): chunks that leave CUs idle run on a second stream; 1: off."""
+        self._check(self.lib.muon_set_streams(self.h, int(n)))
 
     def set_workspace_limit(self, nbytes: int):
         self._check(self.lib.muon_set_workspace_limit(self.h, int(nbytes)))

@@ -95,6 +95,12 @@ struct muon_handle {
   hipEvent_t call_done = nullptr;
   hipStream_t last_stream = nullptr;
   bool have_last = false;
+  // Chunk concurrency (muon_set_streams): chunks that leave CUs idle run on
+  // a second stream with their own workspace slot, forked from and joined
+  // back into the caller's stream through events.
+  int nstreams = 2;
+  hipStream_t side = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
   std::string err;
 };
 
@@ -634,15 +640,51 @@ muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Pla
                       const CoeffTables& tables, hipStream_t stream) {
   DeviceGuard dg(h->device);
   if (!dg.ok) { set_err(h, "cannot select device %d", h->device); return MUON_ERR_DEVICE; }
-  muon_status_t st = ensure_workspace(h, plan.ws_bytes);
+  // Which chunks run on the second stream: those whose Gram launch leaves
+  // CUs idle in its last round (occupancy below 0.9) alternate between the
+  // streams, so one chunk's idle CUs take the other's work; chunks that fill
+  // every round stay on the caller's stream (two such kernels side by side
+  // share the XCDs' L2 less well: measured slower).  The second slot of
+  // workspace is used only when it fits under the workspace limit.
+  std::vector<char> on_side(plan.chunks.size(), 0);
+  bool two = false;
+  if (h->nstreams > 1 && h->side && plan.chunks.size() > 1) {
+    int cus = 256;
+    (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device);
+    int low = 0;
+    for (size_t ci = 0; ci < plan.chunks.size(); ++ci) {
+      const Chunk& c = plan.chunks[ci];
+      const bool tile = !ns_f32 && c.S % 256 == 0;
+      const int64_t t = tile ? c.S / 256 : c.S / 128;
+      const int64_t tiles = t * (t + 1) / 2 * c.count, slots = int64_t(tile ? cus : 2 * cus);
+      const double occ = double(tiles) / double(((tiles + slots - 1) / slots) * slots);
+      if (occ < 0.9) on_side[ci] = (low++ % 2 == 0);
+      two = two || on_side[ci];
+    }
+  }
+  const size_t slot = align256(plan.ws_bytes);
+  if (two && h->ws_limit && 2 * slot > h->ws_limit) {
+    two = false;
+    std::fill(on_side.begin(), on_side.end(), 0);
+  }
+  muon_status_t st = ensure_workspace(h, two ? 2 * slot : plan.ws_bytes);
   if (st != MUON_OK) return st;
   if ((st = begin_call(h, stream)) != MUON_OK) return st;
   std::vector<MatDesc> table(plan.order.size());
   for (size_t p = 0; p < plan.order.size(); ++p) table[p] = make_desc(items[size_t(plan.order[p])], lr, wd);
   if ((st = upload_table(h, h->mats, table.data(), table.size() * sizeof(MatDesc), stream)) != MUON_OK) return st;
   const MatDesc* d_desc = static_cast<const MatDesc*>(h->mats.dev);
-  char* ws = static_cast<char*>(h->ws);
-  for (const Chunk& c : plan.chunks) {
+  if (two) {
+    hipError_t e = hipEventRecord(h->fork, stream);
+    if (e == hipSuccess) e = hipStreamWaitEvent(h->side, h->fork, 0);
+    if (e != hipSuccess) return device_fail(h, "fork", e);
+  }
+  hipError_t launch_err = hipSuccess;
+  for (size_t ci = 0; ci < plan.chunks.size() && launch_err == hipSuccess; ++ci) {
+    const Chunk& c = plan.chunks[ci];
+    const bool odd = on_side[ci] != 0;
+    char* ws = static_cast<char*>(h->ws) + (odd ? slot : 0);
+    const hipStream_t cs = odd ? h->side : stream;
     ChunkGeom g{};
     g.s = int32_t(c.s); g.l = int32_t(c.l); g.S = int32_t(c.S); g.L = int32_t(c.L);
     g.nmat = int32_t(c.count);
@@ -656,10 +698,15 @@ muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Pla
     b.partials = reinterpret_cast<float*>(ws + c.off_part);
     b.rscale = reinterpret_cast<float*>(ws + c.off_r);
     const std::vector<float>& ct = tables[size_t(c.cset)];
-    hipError_t e = muon::run_chunk(g, d_desc + c.first, b, sc, ct.data(), int(ct.size() / 3), stream,
-                                   h->profiling ? &h->timer : nullptr);
-    if (e != hipSuccess) return device_fail(h, "kernel launch", e);
+    launch_err = muon::run_chunk(g, d_desc + c.first, b, sc, ct.data(), int(ct.size() / 3), cs,
+                                 h->profiling ? &h->timer : nullptr);
   }
+  if (two) {  // joined even after a failed launch, so later calls stay ordered
+    hipError_t e = hipEventRecord(h->join, h->side);
+    if (e == hipSuccess) e = hipStreamWaitEvent(stream, h->join, 0);
+    if (e != hipSuccess && launch_err == hipSuccess) return device_fail(h, "join", e);
+  }
+  if (launch_err != hipSuccess) return device_fail(h, "kernel launch", launch_err);
   return end_call(h, stream);
 }
 
@@ -744,11 +791,27 @@ muon_status_t muon_create(muon_handle_t* out, int device) {
   if (!h) return MUON_ERR_OUT_OF_MEMORY;
   h->device = device;
   DeviceGuard dg(device);
+  auto drop_side = [h]() {
+    if (h->side) (void)hipStreamDestroy(h->side);
+    if (h->fork) (void)hipEventDestroy(h->fork);
+    if (h->join) (void)hipEventDestroy(h->join);
+    h->side = nullptr; h->fork = h->join = nullptr;
+    h->nstreams = 1;
+  };
+  // the second stream has the default priority, like every stream here
+  if (dg.ok &&
+      (hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking) != hipSuccess ||
+       hipEventCreateWithFlags(&h->fork, hipEventDisableTiming) != hipSuccess ||
+       hipEventCreateWithFlags(&h->join, hipEventDisableTiming) != hipSuccess)) {
+    (void)hipGetLastError();
+    drop_side();  // run on the caller's stream alone
+  }
   if (!dg.ok || !create_table(h->mats) || !create_table(h->adams) ||
       hipEventCreateWithFlags(&h->call_done, hipEventDisableTiming) != hipSuccess) {
     destroy_table(h->mats);
     destroy_table(h->adams);
     if (h->call_done) (void)hipEventDestroy(h->call_done);
+    drop_side();
     delete h;
     return MUON_ERR_DEVICE;
   }
@@ -766,10 +829,23 @@ muon_status_t muon_destroy(muon_handle_t h) {
     destroy_table(h->mats);
     destroy_table(h->adams);
     if (h->call_done) (void)hipEventDestroy(h->call_done);
+    if (h->side) (void)hipStreamDestroy(h->side);
+    if (h->fork) (void)hipEventDestroy(h->fork);
+    if (h->join) (void)hipEventDestroy(h->join);
     h->timer.destroy();
   }
   delete h;
   return st;
+}
+
+muon_status_t muon_set_streams(muon_handle_t h, int streams) {
+  if (!h || (streams != 1 && streams != 2)) return MUON_ERR_INVALID_ARGUMENT;
+  if (streams == 2 && !h->side) {
+    h->err = "the second stream could not be created";
+    return MUON_ERR_DEVICE;
+  }
+  h->nstreams = streams;
+  return MUON_OK;
 }
 
 muon_status_t muon_reserve(muon_handle_t h, size_t bytes) {

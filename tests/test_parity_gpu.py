@@ -399,6 +399,40 @@ def test_non_default_stream(muon):
     np.testing.assert_array_equal(to_bits(dW[0]), base[0][0])
 
 
+def test_second_stream_gives_the_same_bits(muon):
+    # every bucket here fills few tiles, so its chunks alternate between the
+    # caller's stream and the handle's second one; on a non-default caller
+    # stream too, and with a workspace limit that leaves room for one slot
+    # only (everything then runs on the caller's stream)
+    import torch
+    from paper_2609_21594_amd import binding as B
+    shapes = [(512, 1024)] * 3 + [(768, 768)] + [(256, 256)] * 2 + [(200, 300)]
+    muon.set_streams(1)
+    try:
+        base = _step_bits(muon, shapes, key=27)
+    finally:
+        muon.set_streams(2)
+    two = _step_bits(muon, shapes, key=27)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        other = _step_bits(muon, shapes, key=27, stream=s)
+    W = [to_dev(gen(sh, 0.02, "bf16", 27, i, 0), "bf16") for i, sh in enumerate(shapes)]
+    arr, keep = B.params_array(W, W, [torch.zeros(sh, device="cuda") for sh in shapes])
+    hp, keep2 = B.make_hparams()
+    _, _, one_slot, _ = B.plan_step(list(arr)[:len(shapes)], hp)
+    lim = B.Muon(0)
+    try:
+        lim.set_workspace_limit(one_slot)
+        limited = _step_bits(lim, shapes, key=27)
+    finally:
+        lim.close()
+    for run in (two, other, limited):
+        for x, y in zip(base[0] + base[1], run[0] + run[1]):
+            np.testing.assert_array_equal(x, y)
+    with pytest.raises(B.MuonError):
+        muon.set_streams(3)
+
+
 def test_errors_leave_buffers_untouched(muon):
     import torch
     from paper_2609_21594_amd.binding import Muon, MuonError
