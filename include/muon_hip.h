@@ -253,8 +253,10 @@ muon_status_t muon_plan_step(const muon_param_t* params, int64_t n, const muon_h
  *               only for the symmetric products),
  *   bytes       minimal HBM traffic: each operand read once, each output
  *               written once.
- * Families (in this order): momentum_norm, norm_finalize,
- * normalize_transpose, gram_syrk, poly_syrk, update_gemm, update_apply_gemm,
+ * Families (in this order): momentum_norm (momentum, norm partials and the
+ * unscaled X0 in one pass), norm_finalize, rescale (X0 = r*u for matrices
+ * whose r is too large or small to be applied in the first products),
+ * gram_syrk, poly_syrk, update_gemm, update_apply_gemm,
  * apply_x0, adamw.  `reset` != 0 clears the counters after reading. */
 typedef struct {
   const char* name;

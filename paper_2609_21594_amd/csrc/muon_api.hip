@@ -478,7 +478,7 @@ Plan make_plan(const std::vector<Item>& items, int64_t cap, bool ns_f32, const s
       for (int64_t j = 0; j < c.count; ++j) plan.order.push_back(idx[b + size_t(j)]);
       const size_t xb = align256(size_t(c.count) * size_t(c.S) * size_t(c.L) * es);
       const size_t ab = align256(size_t(c.count) * size_t(c.S) * size_t(c.S) * es);
-      const size_t pb = align256(size_t(c.count) * size_t(muon::norm_blocks(s * l)) * 4);
+      const size_t pb = align256(size_t(c.count) * size_t(muon::norm_tiles(c.S, c.L)) * 4);
       size_t off = 0;
       c.off_X[0] = off; off += xb;
       c.off_X[1] = off; off += xb;
@@ -487,7 +487,7 @@ Plan make_plan(const std::vector<Item>& items, int64_t cap, bool ns_f32, const s
       c.off_A = off; off += ab;
       c.off_B = off; off += ab;
       c.off_part = off; off += pb;
-      c.off_r = off; off += align256(size_t(c.count) * 4);
+      c.off_r = off; off += align256(size_t(c.count) * 8);  // rscale, then xscale
       c.bytes = off;
       plan.ws_bytes = std::max(plan.ws_bytes, off);
       plan.chunks.push_back(c);
@@ -697,6 +697,7 @@ muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Pla
     b.A = ws + c.off_A; b.B = ws + c.off_B;
     b.partials = reinterpret_cast<float*>(ws + c.off_part);
     b.rscale = reinterpret_cast<float*>(ws + c.off_r);
+    b.xscale = b.rscale + c.count;
     const std::vector<float>& ct = tables[size_t(c.cset)];
     launch_err = muon::run_chunk(g, d_desc + c.first, b, sc, ct.data(), int(ct.size() / 3), cs,
                                  h->profiling ? &h->timer : nullptr);
@@ -872,7 +873,7 @@ muon_status_t muon_profile_enable(muon_handle_t h, int enable) {
 muon_status_t muon_profile_read(muon_handle_t h, muon_kernel_stats_t* out, int cap, int* n,
                                 int reset) {
   static const char* const kNames[muon::KK_COUNT] = {
-      "momentum_norm", "norm_finalize", "normalize_transpose", "gram_syrk",
+      "momentum_norm", "norm_finalize", "rescale", "gram_syrk",
       "poly_syrk", "update_gemm", "update_apply_gemm", "apply_x0", "adamw"};
   if (!h || (cap > 0 && !out)) return MUON_ERR_INVALID_ARGUMENT;
   DeviceGuard dg(h->device);

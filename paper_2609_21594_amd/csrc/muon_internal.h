@@ -13,8 +13,6 @@ namespace muon {
 constexpr int kPad = 128;
 // GEMM macro tile (rows and columns of one workgroup's output tile).
 constexpr int kTile = 128;
-// Elements reduced by one workgroup of the momentum / norm kernel.
-constexpr int kNormElemsPerBlock = 16384;
 
 enum DType : int32_t { DT_F32 = 0, DT_BF16 = 1 };
 
@@ -72,8 +70,10 @@ struct ChunkBuffers {
   void* XT[2];          // L x S, row stride S
   void* A;              // S x S
   void* B;              // S x S
-  float* partials;      // nmat x nblk
-  float* rscale;        // nmat: 1 / (||u||_F + eps)
+  float* partials;      // nmat x norm_tiles(S, L)
+  float* rscale;        // nmat: r = 1 / (||u||_F + eps)
+  float* xscale;        // nmat: the scale the first Newton-Schulz step applies
+                        // to X: r, or 1 where X already holds r*u
 };
 
 struct StepScalars {
@@ -98,9 +98,8 @@ struct LaunchTimer {
 };
 
 inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
-inline int64_t norm_blocks(int64_t numel) {
-  return (numel + kNormElemsPerBlock - 1) / kNormElemsPerBlock;
-}
+// Norm partial sums per matrix: one per 64x64 tile of the padded extent.
+inline int64_t norm_tiles(int64_t S, int64_t L) { return (S / 64) * (L / 64); }
 
 // ---------------------------------------------------------------------------
 // AdamW for the parameters Muon does not take (1-D and scalar ones; Sec. 6.4

@@ -1,9 +1,11 @@
 // gfx950 (CDNA4) kernels of the batched Muon step.
 //
 // Per chunk of same-shape matrices (Sec. 6.6 shape fusion):
-//   k_partials   momentum update in place + per-block sums of u^2   (HBM-bound)
+//   k_prologue   momentum update in place, per-tile sums of u^2, and X~ = u
+//                (unscaled), transpose-first, cast; writes X~ and X~^T (HBM-bound)
 //   k_finalize   r = 1 / (||u||_F + eps) per matrix (fixed-order sum)
-//   k_normalize  X0 = r*u, transpose-first, cast; writes X0 and X0^T (HBM-bound)
+//   k_rescale    X0 = r*u for the rare matrices whose r the first products
+//                cannot apply (see k_finalize); others exit at once
 //   k_gemm_nt    the three contractions of Eq. (1) on MFMA:
 //                  A  = X X^T          (Gram, upper tiles only, mirrored)
 //                  B  = b A + c A A    (A is symmetric, so A A = A A^T)
@@ -113,184 +115,58 @@ __device__ __forceinline__ float block_sum_256(float v, float* red4) {
 }
 
 // ---------------------------------------------------------------------------
-// Momentum update (in place) and partial sums of u^2; or, without momentum,
-// partial sums of G^2.  One workgroup reduces kNormElemsPerBlock elements of
-// one matrix; grid = (blocks per matrix, matrices).
+// Prologue, one pass over g and the momentum.  X0 = u / (||u|| + eps) needs
+// the norm of all of u before any element of X0 can be formed; rather than
+// reading g and the momentum a second time, this pass writes X~ = u unscaled
+// (cast to the NS dtype) and the first Newton-Schulz step applies r = 1 /
+// (||u|| + eps) to its products: A0 = r^2 (X~ X~^T), X1 = r (a X~ + B0 X~).
+//
+// A workgroup owns a 64x64 tile of the padded X extent (S x L).  It reads the
+// matching tile of u's inputs row-wise, 8 consecutive elements per access
+// (16-byte loads where the rows allow it, element by element at ragged
+// edges), updates the momentum in place, writes X~ into whichever of X / X^T
+// has u's layout (16-byte stores) and, through LDS, into the other (16-byte
+// stores of 8 elements of one column), and stores its tile's sum of u^2 (a
+// fixed-order reduction).  Zero outside the matrix.
+// grid = (L/64, S/64, matrices).
 // ---------------------------------------------------------------------------
-template <typename GT, bool MOM>
-__global__ __launch_bounds__(256) void k_partials(const MatDesc* __restrict__ desc, int nblk,
-                                                  StepScalars sc, float* __restrict__ partials) {
-  __shared__ float red4[4];
-  const int m = blockIdx.y;
-  const MatDesc md = desc[m];
-  const int64_t numel = static_cast<int64_t>(md.rows) * md.cols;
-  const int64_t start = static_cast<int64_t>(blockIdx.x) * kNormElemsPerBlock;
-  const int64_t end = min(numel, start + static_cast<int64_t>(kNormElemsPerBlock));
-  const GT* __restrict__ g = static_cast<const GT*>(md.g);
-  float* __restrict__ buf = md.buf;
-  const float beta = sc.beta, omb = sc.one_minus_beta;
-  float acc = 0.f;
+template <typename XT>
+struct TileStage {
+  static constexpr int LDT = sizeof(XT) == 2 ? 66 : 65;  // LDS row stride (odd word stride)
+};
 
-  auto one = [&](float gv, float bv, float& bn_out) -> float {
-    if (MOM) {
-      const float bn = fmaf(beta, bv, omb * gv);
-      bn_out = bn;
-      return sc.nesterov ? fmaf(beta, bn, omb * gv) : bn;
-    }
-    return gv;
-  };
+// Tile (i0, j0) of X (origin in X coordinates) of matrix m: the same tile of
+// u, its two destinations and their row strides.
+template <typename XT>
+struct TileDst {
+  int ur0, uc0;
+  XT* D;       // u's own layout (X when u is s x l, X^T when l x s), or null
+  int ldD;
+  XT* Tb;      // the transpose, through LDS, or null
+  int ldT;
+};
 
-  // Element i of the matrix (row-major over the logical view) sits at
-  // gi(i) in g and bi(i) in buf: i itself when the view is dense.
-  const bool dense = md.dense != 0;
-  const bool small = numel < (int64_t(1) << 31);
-  auto rc = [&](int64_t i, int64_t& r, int64_t& c) {
-    if (small) {
-      const uint32_t q = static_cast<uint32_t>(i) / static_cast<uint32_t>(md.cols);
-      r = q;
-      c = i - static_cast<int64_t>(q) * md.cols;
-    } else {
-      r = i / md.cols;
-      c = i - r * md.cols;
-    }
-  };
-  auto gi = [&](int64_t i) -> int64_t {
-    if (dense) return i;
-    int64_t r, c;
-    rc(i, r, c);
-    return view_index(md, r, c);
-  };
-  auto bi = [&](int64_t i) -> int64_t {
-    if (dense) return i;
-    int64_t r, c;
-    rc(i, r, c);
-    return buf_index(md, r, c);
-  };
-  if (md.vec_ok) {
-    // 8 consecutive elements per thread and iteration (numel % 8 == 0; for
-    // a strided view cols % 8 == 0, so the 8 share a row).
-    for (int64_t i = start + threadIdx.x * 8; i < end; i += 256 * 8) {
-      const int64_t ig = gi(i), ib = MOM ? bi(i) : 0;
-      float gv[8];
-      if (sizeof(GT) == 2) {
-        const u32x4_t raw = *reinterpret_cast<const u32x4_t*>(g + ig);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          gv[2 * q] = __uint_as_float(raw[q] << 16);
-          gv[2 * q + 1] = __uint_as_float(raw[q] & 0xffff0000u);
-        }
-      } else {
-        const float4 a = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(g) + ig);
-        const float4 b = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(g) + ig + 4);
-        gv[0] = a.x; gv[1] = a.y; gv[2] = a.z; gv[3] = a.w;
-        gv[4] = b.x; gv[5] = b.y; gv[6] = b.z; gv[7] = b.w;
-      }
-      float bv[8] = {0, 0, 0, 0, 0, 0, 0, 0}, bn[8];
-      if (MOM) {
-        const float4 a = *reinterpret_cast<const float4*>(buf + ib);
-        const float4 b = *reinterpret_cast<const float4*>(buf + ib + 4);
-        bv[0] = a.x; bv[1] = a.y; bv[2] = a.z; bv[3] = a.w;
-        bv[4] = b.x; bv[5] = b.y; bv[6] = b.z; bv[7] = b.w;
-      }
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const float u = one(gv[q], bv[q], bn[q]);
-        acc = fmaf(u, u, acc);
-      }
-      if (MOM) {
-        *reinterpret_cast<float4*>(buf + ib) = make_float4(bn[0], bn[1], bn[2], bn[3]);
-        *reinterpret_cast<float4*>(buf + ib + 4) = make_float4(bn[4], bn[5], bn[6], bn[7]);
-      }
-    }
-  } else {
-    for (int64_t i = start + threadIdx.x; i < end; i += 256) {
-      const int64_t ig = gi(i), ib = MOM ? bi(i) : 0;
-      const float gv = to_f32<GT>(g[ig]);
-      float bn = 0.f;
-      const float u = one(gv, MOM ? buf[ib] : 0.f, bn);
-      if (MOM) buf[ib] = bn;
-      acc = fmaf(u, u, acc);
-    }
-  }
-  const float s = block_sum_256(acc, red4);
-  if (threadIdx.x == 0) partials[static_cast<int64_t>(m) * nblk + blockIdx.x] = s;
-}
-
-// r = 1 / (sqrt(sum of partials) + eps), one workgroup per matrix.
-__global__ __launch_bounds__(256) void k_finalize(const float* __restrict__ partials, int nblk,
-                                                  float eps, float* __restrict__ rscale) {
-  __shared__ float red4[4];
-  const int m = blockIdx.x;
-  float acc = 0.f;
-  for (int i = threadIdx.x; i < nblk; i += 256) acc += partials[static_cast<int64_t>(m) * nblk + i];
-  const float s = block_sum_256(acc, red4);
-  if (threadIdx.x == 0) rscale[m] = 1.0f / (sqrtf(s) + eps);
-}
-
-// ---------------------------------------------------------------------------
-// X0 = r*u with transpose-first.  A workgroup owns a 64x64 tile of the
-// padded X extent (S x L).  It reads the matching tile of u row-wise, 8
-// consecutive elements per access (16-byte loads of g and buf where the rows
-// allow it, element by element at ragged edges), writes it unchanged into
-// whichever of X / X^T has u's layout (16-byte stores), and transposes it
-// through LDS into the other (16-byte stores of 8 elements of one column).
-// Zero outside the matrix.  grid = (L/64, S/64, matrices).
-// ---------------------------------------------------------------------------
-template <typename GT, typename XT, bool MOM>
-__global__ __launch_bounds__(256) void k_normalize(const MatDesc* __restrict__ desc,
-                                                   const float* __restrict__ rscale,
-                                                   StepScalars sc, ChunkGeom cg, XT* __restrict__ X,
-                                                   XT* __restrict__ XTb) {
-  constexpr int LDT = sizeof(XT) == 2 ? 66 : 65;  // LDS row stride (odd word stride)
-  __shared__ XT tile[64 * LDT];
-  const int m = blockIdx.z;
-  const MatDesc md = desc[m];
+template <typename XT>
+__device__ __forceinline__ TileDst<XT> tile_dst(const MatDesc& md, const ChunkGeom& cg, int m, int i0, int j0,
+                                                XT* X, XT* XTb) {
   const bool tr = md.transposed != 0;
-  const int i0 = blockIdx.y * 64, j0 = blockIdx.x * 64;  // tile origin in X coordinates
-  const int ur0 = tr ? j0 : i0, uc0 = tr ? i0 : j0;       // same tile in u coordinates
   const int64_t matX = static_cast<int64_t>(cg.S) * cg.L;
-  // X0 (S x L) is always written; X0^T only when XTb is given.  u's own
-  // layout is X0 when u is s x l and X0^T when it is l x s (transposed).
   XT* Xm = X + m * matX;
   XT* XTm = XTb ? XTb + m * matX : nullptr;
-  XT* D = tr ? XTm : Xm;            // u's own layout (coalesced from the input)
-  const int ldD = tr ? cg.S : cg.L;
-  XT* Tb = tr ? Xm : XTm;           // the transpose, through LDS
-  const int ldT = tr ? cg.L : cg.S;
-  const float r = rscale[m];
-  const GT* __restrict__ g = static_cast<const GT*>(md.g);
-  const float beta = sc.beta, omb = sc.one_minus_beta;
-  auto u_of = [&](float gv, float bn) { return MOM ? (sc.nesterov ? fmaf(beta, bn, omb * gv) : bn) : gv; };
-#pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int c = threadIdx.x + 256 * k;          // chunk: row c / 8, columns 8 (c % 8) ..
-    const int row = c >> 3, col = (c & 7) * 8;
-    const int ur = ur0 + row, uc = uc0 + col;
-    float v[8];
-    if (md.row8_ok && ur < md.rows && uc + 8 <= md.cols) {
-      float gv[8], bv[8];
-      load8(g, view_index(md, ur, uc), gv);
-      if (MOM) load8(md.buf, buf_index(md, ur, uc), bv);  // already updated by k_partials
-#pragma unroll
-      for (int q = 0; q < 8; ++q) v[q] = u_of(gv[q], MOM ? bv[q] : 0.f) * r;
-    } else {
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        v[q] = 0.f;
-        if (ur < md.rows && uc + q < md.cols) {
-          const float gv = to_f32<GT>(g[view_index(md, ur, uc + q)]);
-          v[q] = u_of(gv, MOM ? md.buf[buf_index(md, ur, uc + q)] : 0.f) * r;
-        }
-      }
-    }
-    if (D) store8(D, static_cast<int64_t>(ur) * ldD + uc, v);
-    if (Tb) {
-#pragma unroll
-      for (int q = 0; q < 8; ++q) tile[row * LDT + col + q] = from_f32<XT>(v[q]);
-    }
-  }
-  if (!Tb) return;  // uniform over the block
-  __syncthreads();
+  TileDst<XT> t;
+  t.ur0 = tr ? j0 : i0;
+  t.uc0 = tr ? i0 : j0;
+  t.D = tr ? XTm : Xm;
+  t.ldD = tr ? cg.S : cg.L;
+  t.Tb = tr ? Xm : XTm;
+  t.ldT = tr ? cg.L : cg.S;
+  return t;
+}
+
+// Phase 2 of a tile: rows of the transpose out of LDS, 16 bytes a thread.
+template <typename XT>
+__device__ __forceinline__ void write_transposed(const XT* tile, const TileDst<XT>& t) {
+  constexpr int LDT = TileStage<XT>::LDT;
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
     const int c = threadIdx.x + 256 * k;          // row c / 8 of the transpose, 8 (c % 8) ..
@@ -298,7 +174,137 @@ __global__ __launch_bounds__(256) void k_normalize(const MatDesc* __restrict__ d
     float v[8];
 #pragma unroll
     for (int q = 0; q < 8; ++q) v[q] = to_f32<XT>(tile[(r8 + q) * LDT + trow]);
-    store8(Tb, static_cast<int64_t>(uc0 + trow) * ldT + ur0 + r8, v);
+    store8(t.Tb, static_cast<int64_t>(t.uc0 + trow) * t.ldT + t.ur0 + r8, v);
+  }
+}
+
+// One tile of the prologue (UPDATE_MOM: advance the momentum and write it
+// back; otherwise the momentum has been advanced already).  Returns this
+// thread's sum of u^2.  out = scale * u.
+template <typename GT, typename XT, bool MOM, bool UPDATE_MOM>
+__device__ __forceinline__ float prologue_tile(const MatDesc& md, const StepScalars& sc, const TileDst<XT>& t,
+                                               float scale, XT* tile) {
+  constexpr int LDT = TileStage<XT>::LDT;
+  const GT* __restrict__ g = static_cast<const GT*>(md.g);
+  const float beta = sc.beta, omb = sc.one_minus_beta;
+  float acc = 0.f;
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int c = threadIdx.x + 256 * k;          // chunk: row c / 8, columns 8 (c % 8) ..
+    const int row = c >> 3, col = (c & 7) * 8;
+    const int ur = t.ur0 + row, uc = t.uc0 + col;
+    float v[8];
+    if (md.row8_ok && ur < md.rows && uc + 8 <= md.cols) {
+      float gv[8], bv[8];
+      load8(g, view_index(md, ur, uc), gv);
+      if (MOM) {
+        const int64_t ib = buf_index(md, ur, uc);
+        load8(md.buf, ib, bv);
+        if (UPDATE_MOM) {
+#pragma unroll
+          for (int q = 0; q < 8; ++q) bv[q] = fmaf(beta, bv[q], omb * gv[q]);
+          store8(md.buf, ib, bv);
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] = sc.nesterov ? fmaf(beta, bv[q], omb * gv[q]) : bv[q];
+      } else {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] = gv[q];
+      }
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        acc = fmaf(v[q], v[q], acc);
+        v[q] *= scale;
+      }
+    } else {  // padding stays exactly zero, whatever the scale
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        v[q] = 0.f;
+        if (ur < md.rows && uc + q < md.cols) {
+          const float gv = to_f32<GT>(g[view_index(md, ur, uc + q)]);
+          if (MOM) {
+            const int64_t ib = buf_index(md, ur, uc + q);
+            float bn = md.buf[ib];
+            if (UPDATE_MOM) {
+              bn = fmaf(beta, bn, omb * gv);
+              md.buf[ib] = bn;
+            }
+            v[q] = sc.nesterov ? fmaf(beta, bn, omb * gv) : bn;
+          } else {
+            v[q] = gv;
+          }
+          acc = fmaf(v[q], v[q], acc);
+          v[q] *= scale;
+        }
+      }
+    }
+    if (t.D) store8(t.D, static_cast<int64_t>(ur) * t.ldD + uc, v);
+    if (t.Tb) {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) tile[row * LDT + col + q] = from_f32<XT>(v[q]);
+    }
+  }
+  return acc;
+}
+
+template <typename GT, typename XT, bool MOM>
+__global__ __launch_bounds__(256) void k_prologue(const MatDesc* __restrict__ desc, StepScalars sc, ChunkGeom cg,
+                                                  XT* __restrict__ X, XT* __restrict__ XTb,
+                                                  float* __restrict__ partials) {
+  __shared__ XT tile[64 * TileStage<XT>::LDT];
+  __shared__ float red4[4];
+  const int m = blockIdx.z;
+  const MatDesc md = desc[m];
+  const TileDst<XT> t = tile_dst(md, cg, m, blockIdx.y * 64, blockIdx.x * 64, X, XTb);
+  const float acc = prologue_tile<GT, XT, MOM, true>(md, sc, t, 1.f, tile);
+  const float s = block_sum_256(acc, red4);  // (its barrier also publishes the LDS tile)
+  if (threadIdx.x == 0)
+    partials[static_cast<int64_t>(m) * (gridDim.x * gridDim.y) + blockIdx.y * gridDim.x + blockIdx.x] = s;
+  if (!t.Tb) return;  // uniform over the block
+  __syncthreads();
+  write_transposed(tile, t);
+}
+
+// r = 1 / (sqrt(sum of partials) + eps), one workgroup per matrix, and the
+// scale the first products apply: r itself while X~ X~^T stays well inside
+// the fp32 range (||u|| between 2^-40 and 2^40), else 1 (k_rescale then
+// writes r*u into X instead).
+__global__ __launch_bounds__(256) void k_finalize(const float* __restrict__ partials, int nparts, float eps,
+                                                  float* __restrict__ rscale, float* __restrict__ xscale) {
+  __shared__ float red4[4];
+  const int m = blockIdx.x;
+  float acc = 0.f;
+  for (int i = threadIdx.x; i < nparts; i += 256) acc += partials[static_cast<int64_t>(m) * nparts + i];
+  const float s = block_sum_256(acc, red4);
+  if (threadIdx.x == 0) {
+    const float r = 1.0f / (sqrtf(s) + eps);
+    rscale[m] = r;
+    xscale[m] = (r >= 0x1p-40f && r <= 0x1p40f) ? r : 1.0f;  // NaN fails both tests
+  }
+}
+
+// X0 = r*u, written over X~, for the matrices whose scale k_finalize left at
+// 1 (a norm outside the range above, zero with eps = 0, or NaN); every other
+// matrix's workgroups return at once.  The momentum is already advanced.
+// grid = (workgroups per matrix, matrices); each loops over its tiles.
+template <typename GT, typename XT, bool MOM>
+__global__ __launch_bounds__(256) void k_rescale(const MatDesc* __restrict__ desc, const float* __restrict__ rscale,
+                                                 const float* __restrict__ xscale, StepScalars sc, ChunkGeom cg,
+                                                 XT* __restrict__ X, XT* __restrict__ XTb) {
+  __shared__ XT tile[64 * TileStage<XT>::LDT];
+  const int m = blockIdx.y;
+  const float r = rscale[m];
+  if (r == xscale[m]) return;  // uniform over the block
+  const MatDesc md = desc[m];
+  const int tx = cg.L / 64, ntiles = tx * (cg.S / 64);
+  for (int tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
+    const TileDst<XT> t = tile_dst(md, cg, m, (tt / tx) * 64, (tt % tx) * 64, X, XTb);
+    (void)prologue_tile<GT, XT, MOM, false>(md, sc, t, r, tile);
+    if (t.Tb) {  // uniform over the block
+      __syncthreads();
+      write_transposed(tile, t);
+      __syncthreads();  // the next tile overwrites the LDS tile
+    }
   }
 }
 
@@ -346,6 +352,9 @@ struct GemmArgs {
   // instead of being read again in the epilogue.  The update products
   // always add their a*X term that way on this kernel.
   int32_t e_loop;
+  // First Newton-Schulz step: X holds X~ = u unscaled, and the product is
+  // scaled per matrix by xscale (the Gram product by its square); null after.
+  const float* xscale;
 };
 
 constexpr int kRowBytes = 144;                   // 128 data + 16 pad per LDS row
@@ -449,6 +458,14 @@ __global__ __launch_bounds__(256, 2) void k_gemm_nt(GemmArgs ga) {
   }
 
   // ---- epilogue: accumulators -> LDS fp32 tile ------------------------------
+  // On the first step the products are of X~ = u: the Gram tile is scaled
+  // by r^2, the update's product and its a*X term by r.
+  float s_acc = 1.f, s_e = 1.f;
+  if (ga.xscale && EPI != EPI_POLY) {
+    const float r = ga.xscale[mat];
+    s_acc = EPI == EPI_GRAM ? r * r : r;
+    s_e = r;
+  }
   float* ft = reinterpret_cast<float*>(smem);
 #pragma unroll
   for (int i = 0; i < 2; ++i)
@@ -458,7 +475,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_nt(GemmArgs ga) {
       for (int r = 0; r < 16; ++r) {
         const int row = wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
         const int col = wn * 64 + j * 32 + (lane & 31);
-        ft[row * kFStride + col] = acc[i][j][r];
+        ft[row * kFStride + col] = acc[i][j][r] * s_acc;
       }
   __syncthreads();
 
@@ -483,7 +500,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_nt(GemmArgs ga) {
       if (!diag) ft[r * kFStride + c] = to_f32<T>(o);  // for the mirror store
     } else {
       const float e = to_f32<T>(*reinterpret_cast<const T*>(ga.E + mat * ga.e_mat + static_cast<int64_t>(gi) * ga.lde + gj * static_cast<int>(sizeof(T))));
-      v = fmaf(ga.alpha, e, ft[r * kFStride + c]);
+      v = fmaf(ga.alpha * s_e, e, ft[r * kFStride + c]);
       if (EPI == EPI_UPDATE) {
         const T o = from_f32<T>(v);
         *reinterpret_cast<T*>(ga.C + mat * ga.c_mat + static_cast<int64_t>(gi) * ga.ldc + gj * static_cast<int>(sizeof(T))) = o;
@@ -1126,6 +1143,16 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   const bool stage_t = !QTR && ga.CT != nullptr;
   const bool stage_c = !FINAL && !stage_t;
   const bool e_epi = EPI == EPI_POLY && !epoly;  // the term is read in the epilogue
+  // The factor the accumulators leave with: c for a polynomial that added
+  // (b/c) A in the main loop; on the first step, whose X holds u unscaled,
+  // r^2 for the Gram product and r for the update products.
+  float osc = 1.f;
+  if (EPI == EPI_POLY) {
+    osc = epoly ? ga.beta : 1.f;
+  } else if (ga.xscale) {
+    const float r = ga.xscale[mat];
+    osc = EPI == EPI_GRAM ? r * r : r;
+  }
 
   // Diagonal tiles of the symmetric products are written exactly symmetric:
   // the value computed for (row, col) with row <= col also goes to (col, row).
@@ -1141,7 +1168,7 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
           float v[4];
           if (!e_epi) {
 #pragma unroll
-            for (int q = 0; q < 4; ++q) v[q] = EPI == EPI_POLY ? ga.beta * acc[i][j][4 * g + q] : acc[i][j][4 * g + q];
+            for (int q = 0; q < 4; ++q) v[q] = osc * acc[i][j][4 * g + q];
           } else {
             float e[4];
             unpack_bf16x4(*reinterpret_cast<const uint2*>(ET + static_cast<int64_t>(col) * ga.ldet + row0 * 2), e);
@@ -1260,7 +1287,7 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
           const int c0 = col - q4;                     // direct layout: columns c0 .. c0 + 3
           float v[4];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) v[q] = acc[i][j][4 * g + q];
+          for (int q = 0; q < 4; ++q) v[q] = acc[i][j][4 * g + q] * (e_epi ? 1.f : osc);
           if (!FINAL || tr) {  // natural layout
             if (e_epi) {
               float e[4];
@@ -1269,9 +1296,6 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
               unpack_bf16x4(quad_transpose_bf16(ed), e);
 #pragma unroll
               for (int q = 0; q < 4; ++q) v[q] = fmaf(ga.alpha, e[q], ga.beta * v[q]);
-            } else if (EPI == EPI_POLY) {
-#pragma unroll
-              for (int q = 0; q < 4; ++q) v[q] *= ga.beta;
             }
             if (!FINAL && diag) {  // stage_c: (row, col) and (col, row) for row <= col
               const int cl = col - bn * BN;
@@ -1383,7 +1407,7 @@ void k_gemm_tile(GemmArgs ga) {
 template <typename XT>
 __global__ __launch_bounds__(256) void k_apply_x0(const MatDesc* __restrict__ desc, ChunkGeom cg,
                                                   const XT* __restrict__ X, const XT* __restrict__ XTb,
-                                                  int final_kind) {
+                                                  const float* __restrict__ xscale, int final_kind) {
   const int m = blockIdx.y;
   const MatDesc md = desc[m];
   const int64_t numel = static_cast<int64_t>(md.rows) * md.cols;
@@ -1393,7 +1417,7 @@ __global__ __launch_bounds__(256) void k_apply_x0(const MatDesc* __restrict__ de
   const int64_t matX = static_cast<int64_t>(cg.S) * cg.L;
   const XT* D = (md.transposed ? XTb : X) + m * matX;
   const int ldD = md.transposed ? cg.S : cg.L;
-  const float o = to_f32<XT>(D[ur * ldD + uc]);
+  const float o = to_f32<XT>(D[ur * ldD + uc]) * xscale[m];  // X0 = r X~ (or X0 itself, scale 1)
   const int64_t w = view_index(md, ur, uc);
   if (final_kind == 0) {
     const float wv = load_as_f32(md.W, w, cg.param_dtype);
@@ -1503,7 +1527,7 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
   const int64_t numel = static_cast<int64_t>(cg.s) * cg.l;
   const double ne = double(numel);
   const double s = cg.s, l = cg.l;
-  const int nblk = static_cast<int>(norm_blocks(numel));
+  const int nparts = static_cast<int>(norm_tiles(cg.S, cg.L));
   const double gsz = sizeof(GT), xsz = sizeof(XT);
   const double psz = cg.param_dtype == DT_BF16 ? 2.0 : 4.0;
   // bf16 with S and L multiples of 256: the update products run on the
@@ -1513,32 +1537,36 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
                    tile_rows_fit(cg.S, cg.L, sizeof(XT));
   XT* const xt0 = qtr ? nullptr : static_cast<XT*>(wb.XT[0]);
   hipError_t e;
+  XT* const x0 = static_cast<XT*>(wb.X[0]);
   {
     Timed tm(timer, KK_PARTIALS, st);
+    const dim3 grid(cg.L / 64, cg.S / 64, nmat);
     if (sc.momentum)
-      hipLaunchKernelGGL((k_partials<GT, true>), dim3(nblk, nmat), dim3(256), 0, st, d_desc, nblk, sc, wb.partials);
+      hipLaunchKernelGGL((k_prologue<GT, XT, true>), grid, dim3(256), 0, st, d_desc, sc, cg, x0, xt0, wb.partials);
     else
-      hipLaunchKernelGGL((k_partials<GT, false>), dim3(nblk, nmat), dim3(256), 0, st, d_desc, nblk, sc, wb.partials);
+      hipLaunchKernelGGL((k_prologue<GT, XT, false>), grid, dim3(256), 0, st, d_desc, sc, cg, x0, xt0, wb.partials);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    tm.done(0, 0, nm * ne * (gsz + (sc.momentum ? 8.0 : 0.0)) + nm * nblk * 4.0);
+    // reads g (and the momentum), writes the momentum and X~ (and X~^T)
+    tm.done(0, 0, nm * ne * (gsz + (sc.momentum ? 8.0 : 0.0) + (qtr ? 1.0 : 2.0) * xsz) + nm * nparts * 4.0);
   }
   {
     Timed tm(timer, KK_FINALIZE, st);
-    hipLaunchKernelGGL(k_finalize, dim3(nmat), dim3(256), 0, st, wb.partials, nblk, sc.eps, wb.rscale);
+    hipLaunchKernelGGL(k_finalize, dim3(nmat), dim3(256), 0, st, wb.partials, nparts, sc.eps, wb.rscale,
+                       wb.xscale);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    tm.done(0, 0, nm * nblk * 4.0 + nm * 4.0);
+    tm.done(0, 0, nm * nparts * 4.0 + nm * 8.0);
   }
   {
     Timed tm(timer, KK_NORMALIZE, st);
-    const dim3 ngrid(cg.L / 64, cg.S / 64, nmat);
+    const dim3 grid(64, nmat);
     if (sc.momentum)
-      hipLaunchKernelGGL((k_normalize<GT, XT, true>), ngrid, dim3(256), 0, st, d_desc, wb.rscale, sc, cg,
-                         static_cast<XT*>(wb.X[0]), xt0);
+      hipLaunchKernelGGL((k_rescale<GT, XT, true>), grid, dim3(256), 0, st, d_desc, wb.rscale, wb.xscale, sc, cg,
+                         x0, xt0);
     else
-      hipLaunchKernelGGL((k_normalize<GT, XT, false>), ngrid, dim3(256), 0, st, d_desc, wb.rscale, sc, cg,
-                         static_cast<XT*>(wb.X[0]), xt0);
+      hipLaunchKernelGGL((k_rescale<GT, XT, false>), grid, dim3(256), 0, st, d_desc, wb.rscale, wb.xscale, sc,
+                         cg, x0, xt0);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    tm.done(0, 0, nm * ne * (gsz + (sc.momentum ? 4.0 : 0.0) + (qtr ? 1.0 : 2.0) * xsz));
+    tm.done(0, 0, nm * 8.0);  // nothing else unless a norm is out of range
   }
 
   if (K == 0) {
@@ -1546,7 +1574,7 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
     const int64_t blocks = (numel + 255) / 256;
     hipLaunchKernelGGL((k_apply_x0<XT>), dim3(static_cast<unsigned>(blocks), nmat), dim3(256), 0, st,
                        d_desc, cg, static_cast<const XT*>(wb.X[0]), static_cast<const XT*>(wb.XT[0]),
-                       sc.final_kind);
+                       wb.xscale, sc.final_kind);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     tm.done(0, 0, nm * ne * (xsz + (sc.final_kind == 0 ? 2.0 * psz : psz)));
     return hipSuccess;
@@ -1581,6 +1609,7 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
     g.k_slabs = cg.L * es / 128;
     g.tiles_m = ts; g.tiles_n = ts; g.syrk = 1; g.tiles_per_mat = ts * (ts + 1) / 2;
     g.C = static_cast<char*>(wb.A); g.c_mat = matA; g.ldc = cg.S * es;
+    g.xscale = k == 0 ? wb.xscale : nullptr;  // A0 = r^2 X~ X~^T
     // Under qtr every consumer of A and B runs on the 256 x 256 kernel and
     // reads them as upper-triangle tiles (mode 1): no mirrored tile is
     // written.  Otherwise the lower triangle is written as the mirror.
@@ -1592,6 +1621,7 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
     }
     // B = b A + c A A^T: M = N = K = S.
     GemmArgs p = g;
+    p.xscale = nullptr;
     p.P = static_cast<const char*>(wb.A); p.p_mat = matA; p.ldp = cg.S * es;
     p.Q = p.P; p.q_mat = matA; p.ldq = p.ldp;
     p.k_slabs = cg.S * es / 128;
@@ -1621,6 +1651,7 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
     u.E = X; u.e_mat = matX; u.lde = cg.L * es;
     u.alpha = a;
     u.s = cg.s; u.l = cg.l;
+    u.xscale = k == 0 ? wb.xscale : nullptr;  // X1 = r (a X~ + B0 X~)
     const double uf = nm * 2 * s * s * l, ufx = nm * 2 * Sp * Sp * Lp;
     if (k + 1 < K) {
       u.C = static_cast<char*>(wb.X[cur ^ 1]); u.c_mat = matX; u.ldc = cg.L * es;

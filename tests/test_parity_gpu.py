@@ -247,6 +247,35 @@ def test_tiny_and_scaled_inputs(muon):
         assert rel(to_host(o), want) <= 1e-4
 
 
+@pytest.mark.parametrize("prec", ["f32", "bf16"])
+def test_norms_outside_the_folded_range(muon, prec):
+    # The first Newton-Schulz step applies r = 1/(||u|| + eps) to products of
+    # u itself while r lies in [2^-40, 2^40]; beyond that X0 = r*u is written
+    # out first.  Power-of-two scales keep the inputs exact in both dtypes:
+    # ||u|| ~ 2^-44 and 2^56 here.  eps = 0 makes the result scale-invariant.
+    import torch
+    base = gen((48, 80), 1.0, "f32", 28, 0)
+    if prec == "bf16":
+        base = decode(synth.f32_to_bf16_bits(base), "bf16").astype(np.float32)
+    want = ref.orthogonalize(base.astype(np.float64), 5, eps=0.0)
+    scales = (1.0, 2.0 ** -50, 2.0 ** 50)
+    dt = torch.float32 if prec == "f32" else torch.bfloat16
+    ins = [torch.from_numpy(base * np.float32(sc)).to(dt).cuda() for sc in scales]
+    outs = [torch.empty_like(t) for t in ins]
+    muon.orthogonalize(ins, outs, ns_precision=prec, eps=0.0)
+    torch.cuda.synchronize()
+    for sc, o in zip(scales, outs):
+        assert rel(to_host(o), want) <= TOL[prec], sc
+    # the same through muon_step: zero momentum, beta = 0, no decay, lr = 1
+    # and no rescale, so W' = W - O
+    Ws = [torch.zeros(48, 80, dtype=dt, device="cuda") for _ in scales]
+    Ms = [torch.zeros(48, 80, dtype=torch.float32, device="cuda") for _ in scales]
+    muon.step(Ws, ins, Ms, lr=1.0, beta=0.0, weight_decay=0.0, eps=0.0, ns_precision=prec, scale_mode=1)
+    torch.cuda.synchronize()
+    for sc, w in zip(scales, Ws):
+        assert rel(-to_host(w), want) <= TOL[prec], sc
+
+
 def test_orthogonal_input_closed_form(muon):
     import torch
     Q, _ = np.linalg.qr(rng(9).standard_normal((256, 256)))
