@@ -6,12 +6,16 @@
 //   k_finalize   r = 1 / (||u||_F + eps) per matrix (fixed-order sum)
 //   k_rescale    X0 = r*u for the rare matrices whose r the first products
 //                cannot apply (see k_finalize); others exit at once
-//   k_gemm_nt    the three contractions of Eq. (1) on MFMA:
-//                  A  = X X^T          (Gram, upper tiles only, mirrored)
+//   k_gemm_tile  the three contractions of Eq. (1) on MFMA, 256 x 256 tiles
+//                (bf16; S and L multiples of 256):
+//                  A  = X X^T          (Gram, upper-triangle tiles only)
 //                  B  = b A + c A A    (A is symmetric, so A A = A A^T)
-//                  X' = a X + B X      (reads X^T as the K-contiguous operand)
-//                the last step's epilogue applies the update to W directly.
-//   k_apply      update from X0 when K = 0.
+//                  X' = a X + B X      (X read K-major by transposing LDS reads)
+//                the last step's epilogue applies the update to W directly;
+//   k_gemm_nt    the same on 128 x 128 tiles (fp32 NS and other extents;
+//                writes mirrored A and B and reads X^T);
+//   k_apply_x0   the update from X0 when K = 0;
+//   k_adamw      AdamW for the parameters Muon does not take.
 //
 // All workspace buffers are zero-padded to multiples of 128 in both extents,
 // so the contraction kernels never test bounds; zero padding is preserved by
