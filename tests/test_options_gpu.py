@@ -44,8 +44,8 @@ def device(W, g, m):
     return [to_dev(a, "bf16") for a in W], [to_dev(a, "bf16") for a in g], [to_dev(a, "f32") for a in m]
 
 
-@pytest.mark.parametrize("shapes", [[(512, 1024), (1024, 512), (512, 1024)],
-                                    [(200, 300), (300, 200), (200, 300)]])
+@pytest.mark.parametrize("shapes", [[(512, 1024), (1024, 512), (512, 1024), (1024, 512)],
+                                    [(200, 300), (300, 200), (200, 300), (300, 200)]])
 def test_per_entry_options_match_uniform_calls_and_oracle(muon, shapes):
     import torch
     # lr large enough that the update stands well above the bf16 rounding of
@@ -53,8 +53,9 @@ def test_per_entry_options_match_uniform_calls_and_oracle(muon, shapes):
     hpk = dict(lr=0.2, beta=0.95, weight_decay=0.01, ns_precision="bf16")
     W, g, m = inputs(shapes, (len(shapes), shapes[0][0]))
     # entry 0: the call's table and scale; entry 1: the cubic table and the
-    # original Muon scale; entry 2: an 8-step table
-    opts = [(None, None), (CUBIC3, 2), (MIXED8, None)]
+    # original Muon scale; entry 2: an 8-step table; entry 3: no steps
+    # (O = X0) without any rescale
+    opts = [(None, None), (CUBIC3, 2), (MIXED8, None), ([], 1)]  # the last: K = 0
     Wd, gd, md = device(W, g, m)
     muon.step(Wd, gd, md, entry_coeffs=[o[0] for o in opts], entry_scale_modes=[o[1] for o in opts],
               **hpk)
@@ -62,7 +63,7 @@ def test_per_entry_options_match_uniform_calls_and_oracle(muon, shapes):
         Wu, gu, mu = device([W[i]], [g[i]], [m[i]])
         kw = dict(hpk)
         if coeffs is not None:
-            kw.update(ns_coeffs=coeffs, ns_steps=len(coeffs))
+            kw.update(ns_coeffs=coeffs if coeffs else None, ns_steps=len(coeffs))
         if smode is not None:
             kw.update(scale_mode=smode)
         muon.step(Wu, gu, mu, **kw)
@@ -70,7 +71,7 @@ def test_per_entry_options_match_uniform_calls_and_oracle(muon, shapes):
         assert np.array_equal(to_bits(Wd[i]), to_bits(Wu[0])), i
         assert np.array_equal(to_bits(md[i]), to_bits(mu[0])), i
         hp = ref.MuonHParams(lr=0.2, beta=0.95, weight_decay=0.01,
-                             ns_steps=len(coeffs) if coeffs else 5, ns_coeffs=coeffs,
+                             ns_steps=len(coeffs) if coeffs is not None else 5, ns_coeffs=coeffs,
                              scale_mode=smode or 0)
         W0 = decode(W[i], "bf16")
         r = ref.muon_step_matrix(W0, decode(g[i], "bf16"), np.asarray(m[i], np.float64), hp)

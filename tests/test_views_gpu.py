@@ -102,6 +102,36 @@ def test_gate_up_halves_of_packed_expert_weights(muon, pdt, E, d, f):
     oracle_check(Wd[0][e], Wn[e, :, :f], gn[e, :, :f], mn[e, :, :f], Md[0][e], pdt)
 
 
+@pytest.mark.parametrize("prec,steps", [("f32", 5), ("bf16", 0), ("f32", 0)])
+def test_views_on_the_other_paths(muon, prec, steps):
+    # fp32 Newton-Schulz (the 128 x 128 kernel's last-step epilogue writes
+    # through the view) and K = 0 (the update from X0 alone), on interleaved
+    # row blocks and a column range, against dense copies bit for bit
+    import torch
+    from paper_2609_21594_amd.binding import RowBlocks
+    H, hd, d = 3, 64, 192
+    Wn, gn, mn = physical((3 * H * hd, d), "bf16", (4, steps))
+    Wp, Gp, Mp = to_dev(Wn, "bf16"), to_dev(gn, "bf16"), to_dev(mn, "f32")
+    W0 = Wp.clone()
+    blocks = lambda T: RowBlocks(T.view(H, 3, hd, d)[:, 1])
+    dense_b = lambda T: T.view(H, 3, hd, d)[:, 1].reshape(H * hd, d).clone()
+    cols = lambda T: T[2 * hd:3 * hd, 8:8 + 96]  # head 0's v rows, a column range
+    Wd = [dense_b(Wp), cols(Wp).contiguous()]
+    Gd = [dense_b(Gp), cols(Gp).contiguous()]
+    Md = [dense_b(Mp), cols(Mp).contiguous()]
+    kw = dict(ns_precision=prec, ns_steps=steps, **HP)
+    muon.step([blocks(Wp), cols(Wp)], [blocks(Gp), cols(Gp)], [blocks(Mp), cols(Mp)], **kw)
+    muon.step(Wd, Gd, Md, **kw)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_bits(dense_b(Wp)), to_bits(Wd[0]))
+    assert np.array_equal(to_bits(cols(Wp).contiguous()), to_bits(Wd[1]))
+    assert np.array_equal(to_bits(dense_b(Mp)), to_bits(Md[0]))
+    assert np.array_equal(to_bits(cols(Mp).contiguous()), to_bits(Md[1]))
+    # untouched: the q heads
+    q = W0.view(H, 3, hd, d)[:, 0].contiguous()
+    assert np.array_equal(to_bits(Wp.view(H, 3, hd, d)[:, 0].contiguous()), to_bits(q))
+
+
 def test_unaligned_column_range(muon):
     # a column range starting 3 elements into each row: no 16-byte vector
     # access applies; compared with the oracle, and the columns around it
