@@ -125,7 +125,8 @@ __device__ __forceinline__ float block_sum_256(float v, float* red4) {
 // (cast to the NS dtype) and the first Newton-Schulz step applies r = 1 /
 // (||u|| + eps) to its products: A0 = r^2 (X~ X~^T), X1 = r (a X~ + B0 X~).
 //
-// A workgroup owns a 64x64 tile of the padded X extent (S x L).  It reads the
+// A workgroup owns a 64x64 tile of the padded X extent (S x L), or a 32x128
+// one when u is s x l and no X^T is kept (see tile_of).  It reads the
 // matching tile of u's inputs row-wise, 8 consecutive elements per access
 // (16-byte loads where the rows allow it, element by element at ragged
 // edges), updates the momentum in place, writes X~ into whichever of X / X^T
@@ -149,6 +150,26 @@ struct TileDst {
   XT* Tb;      // the transpose, through LDS, or null
   int ldT;
 };
+
+// Tile tt (row-major over the (S/64) x (L/64) grid) of matrix m.  A matrix
+// with no transpose to write takes 32 x 128 tiles instead (the same count
+// and the same 4096 elements each), whose 256-byte row pieces read and
+// write more contiguously; `wide` says which.
+template <typename XT>
+__device__ __forceinline__ TileDst<XT> tile_dst(const MatDesc& md, const ChunkGeom& cg, int m, int i0, int j0,
+                                                XT* X, XT* XTb);
+
+template <typename XT>
+__device__ __forceinline__ TileDst<XT> tile_of(const MatDesc& md, const ChunkGeom& cg, int m, int tt, XT* X,
+                                               XT* XTb, bool& wide) {
+  wide = md.transposed == 0 && XTb == nullptr;
+  if (wide) {
+    const int tx = cg.L / 128;
+    return tile_dst(md, cg, m, (tt / tx) * 32, (tt % tx) * 128, X, XTb);
+  }
+  const int tx = cg.L / 64;
+  return tile_dst(md, cg, m, (tt / tx) * 64, (tt % tx) * 64, X, XTb);
+}
 
 template <typename XT>
 __device__ __forceinline__ TileDst<XT> tile_dst(const MatDesc& md, const ChunkGeom& cg, int m, int i0, int j0,
@@ -185,17 +206,18 @@ __device__ __forceinline__ void write_transposed(const XT* tile, const TileDst<X
 // One tile of the prologue (UPDATE_MOM: advance the momentum and write it
 // back; otherwise the momentum has been advanced already).  Returns this
 // thread's sum of u^2.  out = scale * u.
-template <typename GT, typename XT, bool MOM, bool UPDATE_MOM>
+template <typename GT, typename XT, bool MOM, bool UPDATE_MOM, bool WIDE>
 __device__ __forceinline__ float prologue_tile(const MatDesc& md, const StepScalars& sc, const TileDst<XT>& t,
                                                float scale, XT* tile) {
   constexpr int LDT = TileStage<XT>::LDT;
+  constexpr int CPR = WIDE ? 16 : 8;              // 8-element chunks per tile row
   const GT* __restrict__ g = static_cast<const GT*>(md.g);
   const float beta = sc.beta, omb = sc.one_minus_beta;
   float acc = 0.f;
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
-    const int c = threadIdx.x + 256 * k;          // chunk: row c / 8, columns 8 (c % 8) ..
-    const int row = c >> 3, col = (c & 7) * 8;
+    const int c = threadIdx.x + 256 * k;          // chunk: row c / CPR, columns 8 (c % CPR) ..
+    const int row = c / CPR, col = (c % CPR) * 8;
     const int ur = t.ur0 + row, uc = t.uc0 + col;
     float v[8];
     if (md.row8_ok && ur < md.rows && uc + 8 <= md.cols) {
@@ -243,7 +265,7 @@ __device__ __forceinline__ float prologue_tile(const MatDesc& md, const StepScal
       }
     }
     if (t.D) store8(t.D, static_cast<int64_t>(ur) * t.ldD + uc, v);
-    if (t.Tb) {
+    if (!WIDE && t.Tb) {
 #pragma unroll
       for (int q = 0; q < 8; ++q) tile[row * LDT + col + q] = from_f32<XT>(v[q]);
     }
@@ -259,8 +281,10 @@ __global__ __launch_bounds__(256) void k_prologue(const MatDesc* __restrict__ de
   __shared__ float red4[4];
   const int m = blockIdx.z;
   const MatDesc md = desc[m];
-  const TileDst<XT> t = tile_dst(md, cg, m, blockIdx.y * 64, blockIdx.x * 64, X, XTb);
-  const float acc = prologue_tile<GT, XT, MOM, true>(md, sc, t, 1.f, tile);
+  bool wide;
+  const TileDst<XT> t = tile_of(md, cg, m, blockIdx.y * gridDim.x + blockIdx.x, X, XTb, wide);
+  const float acc = wide ? prologue_tile<GT, XT, MOM, true, true>(md, sc, t, 1.f, tile)
+                         : prologue_tile<GT, XT, MOM, true, false>(md, sc, t, 1.f, tile);
   const float s = block_sum_256(acc, red4);  // (its barrier also publishes the LDS tile)
   if (threadIdx.x == 0)
     partials[static_cast<int64_t>(m) * (gridDim.x * gridDim.y) + blockIdx.y * gridDim.x + blockIdx.x] = s;
@@ -300,10 +324,12 @@ __global__ __launch_bounds__(256) void k_rescale(const MatDesc* __restrict__ des
   const float r = rscale[m];
   if (r == xscale[m]) return;  // uniform over the block
   const MatDesc md = desc[m];
-  const int tx = cg.L / 64, ntiles = tx * (cg.S / 64);
+  const int ntiles = (cg.L / 64) * (cg.S / 64);
   for (int tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
-    const TileDst<XT> t = tile_dst(md, cg, m, (tt / tx) * 64, (tt % tx) * 64, X, XTb);
-    (void)prologue_tile<GT, XT, MOM, false>(md, sc, t, r, tile);
+    bool wide;
+    const TileDst<XT> t = tile_of(md, cg, m, tt, X, XTb, wide);
+    if (wide) (void)prologue_tile<GT, XT, MOM, false, true>(md, sc, t, r, tile);
+    else (void)prologue_tile<GT, XT, MOM, false, false>(md, sc, t, r, tile);
     if (t.Tb) {  // uniform over the block
       __syncthreads();
       write_transposed(tile, t);
