@@ -296,14 +296,31 @@ __global__ __launch_bounds__(256) void k_prologue(const MatDesc* __restrict__ de
 // r = 1 / (sqrt(sum of partials) + eps), one workgroup per matrix, and the
 // scale the first products apply: r itself while X~ X~^T stays well inside
 // the fp32 range (||u|| between 2^-40 and 2^40), else 1 (k_rescale then
-// writes r*u into X instead).
-__global__ __launch_bounds__(256) void k_finalize(const float* __restrict__ partials, int nparts, float eps,
-                                                  float* __restrict__ rscale, float* __restrict__ xscale) {
-  __shared__ float red4[4];
+// writes r*u into X instead).  1024 threads each sum every 1024th partial
+// into four accumulators (independent loads in flight; an 8192 x 28672
+// matrix has 57344 partials), combined in a fixed order.
+__global__ __launch_bounds__(1024) void k_finalize(const float* __restrict__ partials, int nparts, float eps,
+                                                   float* __restrict__ rscale, float* __restrict__ xscale) {
+  __shared__ float red16[16];
   const int m = blockIdx.x;
-  float acc = 0.f;
-  for (int i = threadIdx.x; i < nparts; i += 256) acc += partials[static_cast<int64_t>(m) * nparts + i];
-  const float s = block_sum_256(acc, red4);
+  const float* p = partials + static_cast<int64_t>(m) * nparts;
+  float a[4] = {0.f, 0.f, 0.f, 0.f};
+  int i = threadIdx.x;
+  for (; i + 3 * 1024 < nparts; i += 4 * 1024) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) a[q] += p[i + q * 1024];
+  }
+  if (i < nparts) a[0] += p[i];
+  if (i + 1024 < nparts) a[1] += p[i + 1024];
+  if (i + 2048 < nparts) a[2] += p[i + 2048];
+  float v = (a[0] + a[1]) + (a[2] + a[3]);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  if ((threadIdx.x & 63) == 0) red16[threadIdx.x >> 6] = v;
+  __syncthreads();
+  float s = 0.f;
+#pragma unroll
+  for (int w = 0; w < 16; ++w) s += red16[w];
   if (threadIdx.x == 0) {
     const float r = 1.0f / (sqrtf(s) + eps);
     rscale[m] = r;
@@ -1581,7 +1598,7 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
   }
   {
     Timed tm(timer, KK_FINALIZE, st);
-    hipLaunchKernelGGL(k_finalize, dim3(nmat), dim3(256), 0, st, wb.partials, nparts, sc.eps, wb.rscale,
+    hipLaunchKernelGGL(k_finalize, dim3(nmat), dim3(1024), 0, st, wb.partials, nparts, sc.eps, wb.rscale,
                        wb.xscale);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     tm.done(0, 0, nm * nparts * 4.0 + nm * 8.0);
