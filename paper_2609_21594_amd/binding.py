@@ -186,14 +186,18 @@ def _view(x):
     else:
         raise ValueError("Muon takes matrices [M, N] or stacks [E, M, N]")
     rows = nb * rb
+    # The ABI reads a zero stride as "dense default", so a stride that is
+    # really zero or negative (an expanded or broadcast tensor) must never
+    # reach it: rows, blocks or planes that overlap are refused here.
+    if (rb > 1 and ld < N) or (nb > 1 and bs <= 0) or (E > 1 and ps <= 0):
+        raise ValueError("a logical matrix's rows, blocks and planes must not overlap "
+                         "(expanded or broadcast tensors are not views Muon can update)")
     if rb == 1:
-        ld = 0
+        ld = N
     if nb == 1:
         rb, bs = 0, 0
     if E == 1:
         ps = 0
-    if ld == 0 or (ld == N and rb == 0):
-        ld = N
     return t, E, rows, N, ld, rb, bs, ps
 
 
