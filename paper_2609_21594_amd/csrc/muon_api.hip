@@ -169,24 +169,68 @@ void set_dense(Item& it) {
   it.bs = it.bs_b = it.rows * it.cols;
 }
 
-struct Range { uintptr_t lo, hi; bool written; };
+// A run of `count` equal byte intervals [lo + k*stride, lo + k*stride + len),
+// k = 0..count-1, with stride >= len when count > 1 (the intervals of a run
+// never overlap each other).  A buffer a call touches is a few runs: one
+// interval when dense, one run over all its rows when rows, blocks and
+// planes continue one stride (a column range of a contiguous tensor).
+struct Run {
+  uintptr_t lo, stride, len;
+  int64_t count;
+  bool written;
+  uintptr_t hi() const { return lo + uintptr_t(count - 1) * stride + len; }  // end of the hull
+};
 
-// Written ranges may not overlap anything; read-only ranges may overlap each
-// other.  Exact in-place pairs (orthogonalize in[i] == out[i]) are passed in
-// merged as one written range.
-bool ranges_disjoint(std::vector<Range>& rs) {
-  std::sort(rs.begin(), rs.end(), [](const Range& a, const Range& b) { return a.lo < b.lo; });
-  uintptr_t max_any = 0, max_written = 0;
-  bool first = true;
-  for (const Range& r : rs) {
-    if (r.hi <= r.lo) continue;
-    if (!first) {
-      if (r.written && r.lo < max_any) return false;
-      if (!r.written && r.lo < max_written) return false;
-    }
-    first = false;
-    max_any = std::max(max_any, r.hi);
-    if (r.written) max_written = std::max(max_written, r.hi);
+int64_t floor_div(int64_t x, int64_t s) { return x >= 0 ? x / s : -((-x + s - 1) / s); }
+
+// Does [x, x + len) meet an interval of run t?  The first interval of t that
+// ends after x is the only candidate.
+bool interval_meets(uintptr_t x, uintptr_t len, const Run& t) {
+  if (x < t.lo + t.len) return t.lo < x + len;
+  if (t.count == 1) return false;
+  const int64_t j = int64_t((x - t.lo - t.len) / t.stride) + 1;
+  return j < t.count && t.lo + uintptr_t(j) * t.stride < x + len;
+}
+
+// Exact intersection test of two runs whose hulls overlap.
+bool runs_meet(const Run& a, const Run& b) {
+  if (a.count == 1) return interval_meets(a.lo, a.len, b);
+  if (b.count == 1) return interval_meets(b.lo, b.len, a);
+  if (a.stride == b.stride) {
+    // a_i meets b_j iff -b.len < D + (j - i)*s < a.len with D = b.lo - a.lo;
+    // every q = j - i in [1 - a.count, b.count - 1] is reachable.
+    const int64_t s = int64_t(a.stride), D = int64_t(b.lo) - int64_t(a.lo);
+    const int64_t q_lo = std::max(floor_div(-int64_t(b.len) - D, s) + 1, 1 - a.count);
+    const int64_t q_hi = std::min(-floor_div(D - int64_t(a.len), s) - 1, b.count - 1);
+    return q_lo <= q_hi;
+  }
+  // different strides: walk the intervals of the run with fewer of them that
+  // lie inside the other's hull
+  const Run& w = a.count <= b.count ? a : b;
+  const Run& o = a.count <= b.count ? b : a;
+  const int64_t k0 = o.lo < w.lo + w.len ? 0 : int64_t((o.lo - w.lo - w.len) / w.stride) + 1;
+  for (int64_t k = k0; k < w.count; ++k) {
+    const uintptr_t x = w.lo + uintptr_t(k) * w.stride;
+    if (x >= o.hi()) break;
+    if (interval_meets(x, w.len, o)) return true;
+  }
+  return false;
+}
+
+// Written runs may not meet anything; read-only runs may meet each other.
+// Exact in-place pairs (orthogonalize in[i] == out[i]) are passed in merged
+// as one written run.  Runs are swept in order of their start; only runs
+// whose hulls overlap are compared.
+bool runs_disjoint(std::vector<Run>& rs) {
+  std::sort(rs.begin(), rs.end(), [](const Run& a, const Run& b) { return a.lo < b.lo; });
+  std::vector<const Run*> open;  // earlier runs whose hull reaches past the current start
+  for (const Run& r : rs) {
+    if (r.len == 0 || r.count == 0) continue;
+    open.erase(std::remove_if(open.begin(), open.end(), [&](const Run* o) { return o->hi() <= r.lo; }),
+               open.end());
+    for (const Run* o : open)
+      if ((o->written || r.written) && runs_meet(*o, r)) return false;
+    open.push_back(&r);
   }
   return true;
 }
@@ -227,30 +271,45 @@ muon_status_t check_dims(int64_t rows, int64_t cols, int64_t batch, const char* 
   return MUON_OK;
 }
 
-// The elements a view of `batch` planes occupies, as byte ranges: one range
-// when the view is dense, one per row block when rows follow each other
-// within a block, else one per row.
-void view_ranges(uintptr_t base, size_t es, int64_t rows, int64_t cols, int64_t batch, int64_t ld,
-                 int64_t rb, int64_t bs, int64_t ps, bool written, std::vector<Range>& out) {
-  const int64_t nblk = rows / rb;
-  const bool rows_run = ld == cols;                       // a block is one run
-  const bool blocks_run = rows_run && (nblk == 1 || bs == rb * cols);
-  if (blocks_run && (batch == 1 || ps == rows * cols)) {
-    out.push_back({base, base + uintptr_t(batch * rows * cols) * es, written});
-    return;
-  }
-  for (int64_t e = 0; e < batch; ++e)
-    for (int64_t b = 0; b < nblk; ++b) {
-      const int64_t blk = e * ps + b * bs;
-      if (rows_run) {
-        out.push_back({base + uintptr_t(blk) * es, base + uintptr_t(blk + rb * cols) * es, written});
-      } else {
-        for (int64_t r = 0; r < rb; ++r) {
-          const uintptr_t lo = base + uintptr_t(blk + r * ld) * es;
-          out.push_back({lo, lo + uintptr_t(cols) * es, written});
-        }
-      }
+// The bytes a view of `batch` planes occupies, as runs.  Row i of plane e
+// starts at element e*ps + (i / rb)*bs + (i % rb)*ld; validation has already
+// ensured that rows, blocks and planes follow each other without overlap.
+// Levels (row, block, plane) merge inward while they are contiguous or
+// continue the stride inside them; the innermost level left is the run, and
+// one run is emitted per index of the levels outside it.
+void view_runs(uintptr_t base, size_t es, int64_t rows, int64_t cols, int64_t batch, int64_t ld,
+               int64_t rb, int64_t bs, int64_t ps, bool written, std::vector<Run>& out) {
+  struct Level { int64_t stride, count; };
+  const Level all[3] = {{ld, rb}, {bs, rows / rb}, {ps, batch}};
+  Level lv[3];
+  int n = 0;
+  for (const Level& l : all)
+    if (l.count > 1) lv[n++] = l;
+  int64_t len = cols;
+  for (bool merged = true; merged;) {
+    merged = false;
+    if (n > 0 && lv[0].stride == len) {  // contiguous: one longer interval
+      len *= lv[0].count;
+      std::copy(lv + 1, lv + n, lv);
+      --n;
+      merged = true;
+      continue;
     }
+    for (int i = 0; i + 1 < n && !merged; ++i)
+      if (lv[i + 1].stride == lv[i].stride * lv[i].count) {  // continues the stride inside it
+        lv[i].count *= lv[i + 1].count;
+        std::copy(lv + i + 2, lv + n, lv + i + 1);
+        --n;
+        merged = true;
+      }
+  }
+  const int64_t stride = n > 0 ? lv[0].stride : len, count = n > 0 ? lv[0].count : 1;
+  const int64_t c1 = n > 1 ? lv[1].count : 1, s1 = n > 1 ? lv[1].stride : 0;
+  const int64_t c2 = n > 2 ? lv[2].count : 1, s2 = n > 2 ? lv[2].stride : 0;
+  for (int64_t p = 0; p < c2; ++p)
+    for (int64_t q = 0; q < c1; ++q)
+      out.push_back({base + uintptr_t(p * s2 + q * s1) * es, uintptr_t(stride) * es, uintptr_t(len) * es,
+                     count, written});
 }
 
 muon_status_t validate_step(const muon_param_t* params, int64_t n, const muon_hparams_t* hp,
@@ -263,8 +322,8 @@ muon_status_t validate_step(const muon_param_t* params, int64_t n, const muon_hp
   }
   if (n < 0) { msg.set("n must be >= 0"); return MUON_ERR_INVALID_ARGUMENT; }
   if (n > 0 && !params) { msg.set("params is NULL"); return MUON_ERR_INVALID_ARGUMENT; }
-  std::vector<Range> ranges;
-  ranges.reserve(3 * n);
+  std::vector<Run> runs;
+  runs.reserve(3 * n);
   int64_t flat = 0;
   for (int64_t i = 0; i < n; ++i) {
     const muon_param_t& p = params[i];
@@ -334,10 +393,10 @@ muon_status_t validate_step(const muon_param_t* params, int64_t n, const muon_hp
       msg.set("entry %lld: pointer not aligned to its element size", (long long)i);
       return MUON_ERR_INVALID_ARGUMENT;
     }
-    view_ranges(W, dtype_size(p.param_dtype), p.rows, p.cols, p.batch, ld, rb, bs, ps, true, ranges);
-    view_ranges(G, dtype_size(p.grad_dtype), p.rows, p.cols, p.batch, ld, rb, bs, ps, false, ranges);
-    if (mdense) view_ranges(M, 4, p.rows, p.cols, p.batch, p.cols, p.rows, plane, plane, true, ranges);
-    else view_ranges(M, 4, p.rows, p.cols, p.batch, ld, rb, bs, ps, true, ranges);
+    view_runs(W, dtype_size(p.param_dtype), p.rows, p.cols, p.batch, ld, rb, bs, ps, true, runs);
+    view_runs(G, dtype_size(p.grad_dtype), p.rows, p.cols, p.batch, ld, rb, bs, ps, false, runs);
+    if (mdense) view_runs(M, 4, p.rows, p.cols, p.batch, p.cols, p.rows, plane, plane, true, runs);
+    else view_runs(M, 4, p.rows, p.cols, p.batch, ld, rb, bs, ps, true, runs);
     if (items) {
       for (int64_t e = 0; e < p.batch; ++e) {
         Item it;
@@ -363,7 +422,7 @@ muon_status_t validate_step(const muon_param_t* params, int64_t n, const muon_hp
       }
     }
   }
-  if (!ranges_disjoint(ranges)) {
+  if (!runs_disjoint(runs)) {
     msg.set("param, grad and momentum buffers overlap");
     return MUON_ERR_INVALID_ARGUMENT;
   }
@@ -383,7 +442,7 @@ muon_status_t validate_orth(const void* const* in, void* const* out, const int64
   if (coeffs)
     for (int i = 0; i < 3 * ns_steps; ++i)
       if (!std::isfinite(coeffs[i])) { msg.set("ns_coeffs[%d] is not finite", i); return MUON_ERR_INVALID_ARGUMENT; }
-  std::vector<Range> ranges;
+  std::vector<Run> runs;
   const size_t es = dtype_size(dtype);
   muon_status_t st;
   for (int64_t i = 0; i < n; ++i) {
@@ -393,10 +452,10 @@ muon_status_t validate_orth(const void* const* in, void* const* out, const int64
     if (a % es || b % es) { msg.set("matrix %lld: pointer not aligned to its element size", (long long)i); return MUON_ERR_INVALID_ARGUMENT; }
     const uintptr_t bytes = uintptr_t(rows[i]) * uintptr_t(cols[i]) * es;
     if (a == b) {
-      ranges.push_back({a, a + bytes, true});
+      runs.push_back({a, bytes, bytes, 1, true});
     } else {
-      ranges.push_back({a, a + bytes, false});
-      ranges.push_back({b, b + bytes, true});
+      runs.push_back({a, bytes, bytes, 1, false});
+      runs.push_back({b, bytes, bytes, 1, true});
     }
     if (items) {
       Item it;
@@ -409,7 +468,7 @@ muon_status_t validate_orth(const void* const* in, void* const* out, const int64
       items->push_back(it);
     }
   }
-  if (!ranges_disjoint(ranges)) { msg.set("an output overlaps another buffer"); return MUON_ERR_INVALID_ARGUMENT; }
+  if (!runs_disjoint(runs)) { msg.set("an output overlaps another buffer"); return MUON_ERR_INVALID_ARGUMENT; }
   return MUON_OK;
 }
 
@@ -729,7 +788,7 @@ muon_status_t validate_adamw(const muon_adamw_param_t* params, int64_t n, const 
   if (hp->reserved != 0) { msg.set("reserved must be 0"); return MUON_ERR_INVALID_ARGUMENT; }
   if (n < 0) { msg.set("n must be >= 0"); return MUON_ERR_INVALID_ARGUMENT; }
   if (n > 0 && !params) { msg.set("params is NULL"); return MUON_ERR_INVALID_ARGUMENT; }
-  std::vector<Range> ranges;
+  std::vector<Run> runs;
   for (int64_t i = 0; i < n; ++i) {
     const muon_adamw_param_t& p = params[i];
     if (p.numel < 0 || p.numel > (int64_t(1) << 40)) { msg.set("entry %lld: numel out of range", (long long)i); return MUON_ERR_INVALID_ARGUMENT; }
@@ -741,12 +800,12 @@ muon_status_t validate_adamw(const muon_adamw_param_t* params, int64_t n, const 
     const size_t ps = dtype_size(p.param_dtype), gs = dtype_size(p.grad_dtype);
     if (P % ps || G % gs || M % 4 || V % 4) { msg.set("entry %lld: pointer not aligned to its element size", (long long)i); return MUON_ERR_INVALID_ARGUMENT; }
     const uintptr_t ne = uintptr_t(p.numel);
-    ranges.push_back({P, P + ne * ps, true});
-    ranges.push_back({G, G + ne * gs, false});
-    ranges.push_back({M, M + ne * 4, true});
-    ranges.push_back({V, V + ne * 4, true});
+    runs.push_back({P, ne * ps, ne * ps, 1, true});
+    runs.push_back({G, ne * gs, ne * gs, 1, false});
+    runs.push_back({M, ne * 4, ne * 4, 1, true});
+    runs.push_back({V, ne * 4, ne * 4, 1, true});
   }
-  if (!ranges_disjoint(ranges)) { msg.set("param, grad and moment buffers overlap"); return MUON_ERR_INVALID_ARGUMENT; }
+  if (!runs_disjoint(runs)) { msg.set("param, grad and moment buffers overlap"); return MUON_ERR_INVALID_ARGUMENT; }
   return MUON_OK;
 }
 

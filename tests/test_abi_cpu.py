@@ -202,6 +202,106 @@ def test_views_plan_like_their_dense_copies(lib):
     assert chunks == chunks2 and ws == ws2 and order == order2
 
 
+def touched(e):
+    """Every byte interval an entry touches, row by row, with whether it is
+    written: the view's definition written out, with no merging."""
+    rb = e.row_block or e.rows
+    ld = e.ld or e.cols
+    bs = e.block_stride or rb * ld
+    ps = e.plane_stride or (e.rows // rb) * bs
+    out = []
+    for base, size, written, dense in ((e.param, 2 if e.param_dtype == B.BF16 else 4, True, False),
+                                       (e.grad, 2 if e.grad_dtype == B.BF16 else 4, False, False),
+                                       (e.momentum, 4, True, bool(e.momentum_dense))):
+        for p in range(e.batch):
+            for i in range(e.rows):
+                off = (p * e.rows + i) * e.cols if dense else p * ps + (i // rb) * bs + (i % rb) * ld
+                out.append((base + off * size, base + (off + e.cols) * size, written))
+    return out
+
+
+def brute_overlap(es):
+    import numpy as np
+    iv = [t for e in es for t in touched(e)]
+    lo = np.array([t[0] - BASE for t in iv], dtype=np.int64)
+    hi = np.array([t[1] - BASE for t in iv], dtype=np.int64)
+    w = np.array([t[2] for t in iv])
+    meet = (lo[:, None] < hi[None, :]) & (lo[None, :] < hi[:, None]) & (w[:, None] | w[None, :])
+    np.fill_diagonal(meet, False)
+    return bool(meet.any())
+
+
+def random_view(rng, window):
+    rb, nblk, cols = (int(v) for v in rng.integers(1, [4, 4, 5]))
+    ld = cols + int(rng.integers(0, 4))
+    bs = (rb - 1) * ld + cols + int(rng.integers(0, 4)) if nblk > 1 else 0
+    batch = int(rng.integers(1, 4))
+    span = (nblk - 1) * (bs or rb * ld) + (rb - 1) * ld + cols
+    ps = span + int(rng.integers(0, 4)) if batch > 1 else 0
+    pdt, gdt = (int(v) for v in rng.choice([B.BF16, B.F32], 2))
+    sz = lambda dt: 2 if dt == B.BF16 else 4
+    W = BASE + sz(pdt) * int(rng.integers(0, window))
+    G = BASE + sz(gdt) * int(rng.integers(0, window))
+    M = BASE + 4 * int(rng.integers(0, window // 2))
+    return B.MuonParam(W, G, M, rb * nblk, cols, batch, ld, pdt, gdt, rb, bs, ps,
+                       int(rng.integers(0, 2)), 0)
+
+
+def test_overlap_check_matches_brute_force(lib):
+    # random views (column ranges, row blocks, planes, dense momenta, mixed
+    # element sizes) packed into a small address window, so that exact
+    # overlaps, interleavings and near misses all occur; the library's
+    # verdict must equal the pairwise check over every row's bytes
+    import numpy as np
+    rng = np.random.Generator(np.random.PCG64(20260912))
+    seen = {True: 0, False: 0}
+    for case in range(600):
+        window = [64, 256, 2048][case % 3]
+        es = [random_view(rng, window) for _ in range(int(rng.integers(1, 4)))]
+        st, msg = B.validate_step(es, hp())
+        want = brute_overlap(es)
+        assert st in (B.MUON_OK, 1), (case, msg)
+        assert (st == 1 and "overlap" in msg) == want, (case, st, msg)
+        seen[want] += 1
+    assert min(seen.values()) >= 100, seen
+
+
+def test_interleaved_strided_views(lib):
+    # same row stride, interleaved: a view of column pairs every 4 columns
+    # and one shifted by 2 do not meet, shifted by 1 they do; a dense buffer
+    # laid over one of the gaps meets nothing only if it fits in the gap
+    E, rows = 2, 5
+    W, G, M = BASE, BASE + (1 << 30), BASE + (2 << 30)
+    mk = lambda o: view(W + 2 * o, G + 2 * o, M + 4 * o, rows, 2, ld=4, batch=E, ps=rows * 4)
+    st, msg = B.validate_step([mk(0), mk(2)], hp())
+    assert st == B.MUON_OK, msg
+    st, _ = B.validate_step([mk(0), mk(1)], hp())
+    assert st == 1
+    gap = view(W + 2 * 2, BASE + (3 << 30), BASE + (4 << 30), 1, 2)  # param in row 0's gap
+    st, msg = B.validate_step([mk(0), gap], hp())
+    assert st == B.MUON_OK, msg
+    gap = view(W + 2 * 2, BASE + (3 << 30), BASE + (4 << 30), 1, 3)  # one element too wide
+    st, _ = B.validate_step([mk(0), gap], hp())
+    assert st == 1
+
+
+def test_overlap_check_is_fast_for_large_expert_views(lib):
+    # packed gate|up halves of 128 experts of 7168 x 2x2048: 917504 rows per
+    # half; the check must not enumerate rows
+    import time
+    E, d, f = 128, 7168, 2048
+    W, G, M = BASE, BASE + (1 << 36), BASE + (2 << 36)
+    halves = [view(W + 2 * o, G + 2 * o, M + 4 * o, d, f, ld=2 * f, batch=E, ps=d * 2 * f)
+              for o in (0, f)]
+    t0 = time.perf_counter()
+    st, msg = B.validate_step(halves, hp())
+    assert st == B.MUON_OK, msg
+    halves[1].momentum -= 4
+    st, _ = B.validate_step(halves, hp())
+    assert st == 1
+    assert time.perf_counter() - t0 < 0.5
+
+
 def table(rows):
     flat = [float(v) for r in rows for v in r]
     arr = (ctypes.c_float * len(flat))(*flat)
