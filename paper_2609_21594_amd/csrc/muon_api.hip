@@ -484,6 +484,7 @@ struct Chunk {
   size_t bytes;
   // byte offsets inside the workspace
   size_t off_X[2], off_XT[2], off_A, off_B, off_part, off_r;
+  bool keeps_xt;  // X^T buffers present (see chunk_keeps_xt)
 };
 
 struct Plan {
@@ -538,11 +539,14 @@ Plan make_plan(const std::vector<Item>& items, int64_t cap, bool ns_f32, const s
       const size_t xb = align256(size_t(c.count) * size_t(c.S) * size_t(c.L) * es);
       const size_t ab = align256(size_t(c.count) * size_t(c.S) * size_t(c.S) * es);
       const size_t pb = align256(size_t(c.count) * size_t(muon::norm_tiles(c.S, c.L)) * 4);
+      c.keeps_xt = muon::chunk_keeps_xt(c.S, c.L, ns_f32, steps[size_t(c.cset)]);
       size_t off = 0;
       c.off_X[0] = off; off += xb;
       c.off_X[1] = off; off += xb;
-      c.off_XT[0] = off; off += xb;
-      c.off_XT[1] = off; off += xb;
+      if (c.keeps_xt) {
+        c.off_XT[0] = off; off += xb;
+        c.off_XT[1] = off; off += xb;
+      }
       c.off_A = off; off += ab;
       c.off_B = off; off += ab;
       c.off_part = off; off += pb;
@@ -721,12 +725,17 @@ muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Pla
       two = two || on_side[ci];
     }
   }
-  const size_t slot = align256(plan.ws_bytes);
-  if (two && h->ws_limit && 2 * slot > h->ws_limit) {
+  // each slot sized for the chunks that run on its stream
+  size_t main_bytes = 0, side_bytes = 0;
+  for (size_t ci = 0; ci < plan.chunks.size(); ++ci)
+    (on_side[ci] ? side_bytes : main_bytes) = std::max(on_side[ci] ? side_bytes : main_bytes,
+                                                       plan.chunks[ci].bytes);
+  const size_t slot = align256(main_bytes);
+  if (two && h->ws_limit && slot + side_bytes > h->ws_limit) {
     two = false;
     std::fill(on_side.begin(), on_side.end(), 0);
   }
-  muon_status_t st = ensure_workspace(h, two ? 2 * slot : plan.ws_bytes);
+  muon_status_t st = ensure_workspace(h, two ? slot + side_bytes : plan.ws_bytes);
   if (st != MUON_OK) return st;
   if ((st = begin_call(h, stream)) != MUON_OK) return st;
   std::vector<MatDesc> table(plan.order.size());
@@ -752,7 +761,8 @@ muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Pla
     g.param_dtype = c.pdt == MUON_BF16 ? muon::DT_BF16 : muon::DT_F32;
     ChunkBuffers b{};
     b.X[0] = ws + c.off_X[0]; b.X[1] = ws + c.off_X[1];
-    b.XT[0] = ws + c.off_XT[0]; b.XT[1] = ws + c.off_XT[1];
+    b.XT[0] = c.keeps_xt ? ws + c.off_XT[0] : nullptr;
+    b.XT[1] = c.keeps_xt ? ws + c.off_XT[1] : nullptr;
     b.A = ws + c.off_A; b.B = ws + c.off_B;
     b.partials = reinterpret_cast<float*>(ws + c.off_part);
     b.rscale = reinterpret_cast<float*>(ws + c.off_r);

@@ -101,6 +101,21 @@ inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 // Norm partial sums per matrix: one per 64x64 tile of the padded extent.
 inline int64_t norm_tiles(int64_t S, int64_t L) { return (S / 64) * (L / 64); }
 
+// The 256 x 256 kernel addresses a tile's 256 rows (operands, the a*X
+// term, the parameter block) by 32-bit offsets from one base, so every row
+// it reads or writes must be shorter than 2^31 / 256 bytes.
+constexpr int64_t kTileMaxRowBytes = (int64_t(1) << 31) / 256;
+inline bool tile_rows_fit(int64_t S, int64_t L, int es) {
+  return S * es < kTileMaxRowBytes && L * es < kTileMaxRowBytes;
+}
+// A chunk keeps X^T (two more X-sized workspace buffers) unless its update
+// products run on the 256 x 256 kernel, which reads X itself through
+// transposing LDS reads: bf16 Newton-Schulz, S and L multiples of 256, at
+// least one step, rows within that kernel's offsets.
+inline bool chunk_keeps_xt(int64_t S, int64_t L, bool ns_f32, int K) {
+  return ns_f32 || S % 256 != 0 || L % 256 != 0 || K == 0 || !tile_rows_fit(S, L, 2);
+}
+
 // ---------------------------------------------------------------------------
 // AdamW for the parameters Muon does not take (1-D and scalar ones; Sec. 6.4
 // delegates them to AdamW through a chained optimizer).

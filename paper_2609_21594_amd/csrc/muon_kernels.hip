@@ -36,11 +36,6 @@ typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
-// The 256 x 256 kernel addresses a tile's 256 rows (operands, the a*X
-// term, the parameter block) by 32-bit offsets from one base, so every row
-// it reads or writes must be shorter than 2^31 / 256 bytes.
-constexpr int64_t kTileMaxRowBytes = (int64_t(1) << 31) / 256;
-
 // ---------------------------------------------------------------------------
 // bfloat16 storage: uint16 bit patterns.  Widening is exact; narrowing is
 // the hardware conversion (v_cvt_pk_bf16_f32): round to nearest, ties to
@@ -1528,10 +1523,6 @@ hipError_t launch_tile(int epi, GemmArgs ga, int nmat, hipStream_t st) {
   return hipGetLastError();
 }
 
-inline bool tile_rows_fit(int64_t S, int64_t L, int es) {
-  return S * es < kTileMaxRowBytes && L * es < kTileMaxRowBytes;
-}
-
 // The 256 x 256 kernel runs the bf16 products whose padded extents are
 // multiples of 256 (and whose rows fit its offsets): the symmetric ones when
 // S is, the update ones (which read X through transposing LDS reads) when S
@@ -1580,8 +1571,7 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
   // bf16 with S and L multiples of 256: the update products run on the
   // 256 x 256 kernel and read X through transposing LDS reads, so no X^T is
   // kept (K = 0 applies X0 from whichever layout matches the parameter).
-  const bool qtr = sizeof(XT) == 2 && cg.S % 256 == 0 && cg.L % 256 == 0 && K > 0 &&
-                   tile_rows_fit(cg.S, cg.L, sizeof(XT));
+  const bool qtr = !chunk_keeps_xt(cg.S, cg.L, sizeof(XT) == 4, K);
   XT* const xt0 = qtr ? nullptr : static_cast<XT*>(wb.XT[0]);
   hipError_t e;
   XT* const x0 = static_cast<XT*>(wb.X[0]);

@@ -418,6 +418,24 @@ def test_plan_padding_and_workspace_bytes(lib):
     assert ws32 == 6 * 2 * xb + 512
 
 
+def test_plan_keeps_no_transpose_where_the_tile_kernel_reads_x(lib):
+    # bf16 with padded extents that are multiples of 256 and at least one
+    # step: the update products read X itself, so only 2 X buffers; with
+    # K = 0, fp32 Newton-Schulz or extents off the 256 grid, 4
+    def ws(shape, **kw):
+        st, (c,), total, _ = B.plan_step(entries([shape]), hp(**kw))
+        assert st == 0 and total == c["workspace_bytes"]
+        return total
+    s, l = 512, 1280
+    xb, ab = s * l * 2, s * s * 2
+    tail = 768 + 256  # norm partials (8 x 20 (or 22) floats); 1/(norm+eps) and the first scale
+    assert ws((s, l)) == 2 * xb + 2 * ab + tail
+    assert ws((l, s)) == 2 * xb + 2 * ab + tail  # transposed to 512 x 1280 first
+    assert ws((s, l), ns_steps=0) == 4 * xb + 2 * ab + tail
+    assert ws((s, l), ns_precision="f32") == 8 * xb + 4 * ab + tail
+    assert ws((s, 1300)) == 4 * (s * 1408 * 2) + 2 * ab + tail
+
+
 def test_plan_separates_dtypes(lib):
     a = entries([(64, 64)], pdt=B.F32, gdt=B.F32)
     b, _ = entry(BASE + (1 << 30), 64, 64)
