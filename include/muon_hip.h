@@ -145,7 +145,12 @@ typedef struct {
 
 /* Handle: owns the workspace and the device descriptor tables of one device.
  * muon_create makes `device` current while it runs and restores the caller's
- * device before it returns. */
+ * device before it returns.  muon_destroy waits on the host for the work of
+ * every call made on the handle (and nothing else on the device), then frees
+ * what the handle owns; growing the workspace or a descriptor table waits
+ * the same way.  Each call records an event at its end, also when it fails
+ * after enqueueing work, and a call on another stream than the previous one
+ * waits for that event on the device first. */
 muon_status_t muon_create(muon_handle_t* out, int device);
 muon_status_t muon_destroy(muon_handle_t h);
 
@@ -153,9 +158,10 @@ muon_status_t muon_destroy(muon_handle_t h);
  * products fill the last round of tiles less than 90%) run on a second
  * stream owned by the handle, beside the chunks on `stream`; the call forks
  * from and joins back into `stream` through events, so its work is still
- * ordered on `stream` as a whole.  Such a call uses up to twice the
- * workspace muon_plan_step reports (never beyond the workspace limit: then
- * it runs on `stream` alone).  Results are bitwise the same either way.
+ * ordered on `stream` as a whole.  Such a call uses a second workspace slot
+ * sized for the chunks it places there, up to twice what muon_plan_step
+ * reports (never beyond the workspace limit: then it runs on `stream`
+ * alone).  Results are bitwise the same either way.
  * streams: 2 (the default) or 1 (everything on the caller's stream). */
 muon_status_t muon_set_streams(muon_handle_t h, int streams);
 

@@ -574,6 +574,16 @@ muon_status_t device_fail(muon_handle_t h, const char* what, hipError_t e) {
   return MUON_ERR_DEVICE;
 }
 
+// Blocks until every call made on the handle has finished on the device.
+// Each call records call_done at its end on its stream, after waiting for
+// the previous call's call_done when it runs on another stream, so the last
+// one covers all of them; unrelated work on the device is not waited for.
+muon_status_t wait_idle(muon_handle_t h) {
+  if (!h->have_last) return MUON_OK;
+  const hipError_t e = hipEventSynchronize(h->call_done);
+  return e == hipSuccess ? MUON_OK : device_fail(h, "hipEventSynchronize", e);
+}
+
 muon_status_t ensure_workspace(muon_handle_t h, size_t bytes) {
   if (bytes <= h->ws_bytes) return MUON_OK;
   if (h->ws_limit && bytes > h->ws_limit) {
@@ -582,8 +592,9 @@ muon_status_t ensure_workspace(muon_handle_t h, size_t bytes) {
   }
   hipError_t e;
   if (h->ws) {
-    // earlier work may still use the old workspace
-    if ((e = hipDeviceSynchronize()) != hipSuccess) return device_fail(h, "hipDeviceSynchronize", e);
+    // earlier calls' work may still use the old workspace
+    const muon_status_t st = wait_idle(h);
+    if (st != MUON_OK) return st;
     if ((e = hipFree(h->ws)) != hipSuccess) return device_fail(h, "hipFree", e);
     h->ws = nullptr;
     h->ws_bytes = 0;
@@ -610,7 +621,8 @@ muon_status_t upload_table(muon_handle_t h, DeviceTable& t, const void* data, si
   if (bytes > t.dev_cap) {
     const size_t cap = std::max(bytes, size_t(16384));
     if (t.dev) {
-      if ((e = hipDeviceSynchronize()) != hipSuccess) return device_fail(h, "hipDeviceSynchronize", e);
+      const muon_status_t st = wait_idle(h);  // earlier calls may still read the old table
+      if (st != MUON_OK) return st;
       if ((e = hipFree(t.dev)) != hipSuccess) return device_fail(h, "hipFree", e);
       t.dev = nullptr; t.dev_cap = 0; t.last.clear();
     }
@@ -738,14 +750,18 @@ muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Pla
   muon_status_t st = ensure_workspace(h, two ? slot + side_bytes : plan.ws_bytes);
   if (st != MUON_OK) return st;
   if ((st = begin_call(h, stream)) != MUON_OK) return st;
+  // From here every exit records call_done, so that later calls wait for
+  // whatever this one managed to enqueue.
+  const auto fail = [&](muon_status_t s) { (void)end_call(h, stream); return s; };
   std::vector<MatDesc> table(plan.order.size());
   for (size_t p = 0; p < plan.order.size(); ++p) table[p] = make_desc(items[size_t(plan.order[p])], lr, wd);
-  if ((st = upload_table(h, h->mats, table.data(), table.size() * sizeof(MatDesc), stream)) != MUON_OK) return st;
+  if ((st = upload_table(h, h->mats, table.data(), table.size() * sizeof(MatDesc), stream)) != MUON_OK)
+    return fail(st);
   const MatDesc* d_desc = static_cast<const MatDesc*>(h->mats.dev);
   if (two) {
     hipError_t e = hipEventRecord(h->fork, stream);
     if (e == hipSuccess) e = hipStreamWaitEvent(h->side, h->fork, 0);
-    if (e != hipSuccess) return device_fail(h, "fork", e);
+    if (e != hipSuccess) return fail(device_fail(h, "fork", e));
   }
   hipError_t launch_err = hipSuccess;
   for (size_t ci = 0; ci < plan.chunks.size() && launch_err == hipSuccess; ++ci) {
@@ -774,9 +790,12 @@ muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Pla
   if (two) {  // joined even after a failed launch, so later calls stay ordered
     hipError_t e = hipEventRecord(h->join, h->side);
     if (e == hipSuccess) e = hipStreamWaitEvent(stream, h->join, 0);
-    if (e != hipSuccess && launch_err == hipSuccess) return device_fail(h, "join", e);
+    if (e != hipSuccess) {
+      (void)hipStreamSynchronize(h->side);  // not joined: wait on the host instead
+      if (launch_err == hipSuccess) return fail(device_fail(h, "join", e));
+    }
   }
-  if (launch_err != hipSuccess) return device_fail(h, "kernel launch", launch_err);
+  if (launch_err != hipSuccess) return fail(device_fail(h, "kernel launch", launch_err));
   return end_call(h, stream);
 }
 
@@ -894,7 +913,9 @@ muon_status_t muon_destroy(muon_handle_t h) {
   muon_status_t st = MUON_OK;
   {
     DeviceGuard dg(h->device);
-    if (hipDeviceSynchronize() != hipSuccess) st = MUON_ERR_DEVICE;
+    if (wait_idle(h) != MUON_OK) st = MUON_ERR_DEVICE;
+    for (DeviceTable* t : {&h->mats, &h->adams})  // staging copies still in flight
+      if (t->pending && hipEventSynchronize(t->staged) != hipSuccess) st = MUON_ERR_DEVICE;
     if (h->ws) (void)hipFree(h->ws);
     destroy_table(h->mats);
     destroy_table(h->adams);
@@ -1058,8 +1079,10 @@ muon_status_t muon_adamw_step(muon_handle_t h, const muon_adamw_param_t* params,
   DeviceGuard dg(h->device);
   if (!dg.ok) { set_err(h, "cannot select device %d", h->device); return MUON_ERR_DEVICE; }
   if ((st = begin_call(h, stream)) != MUON_OK) return st;
+  // every exit from here records call_done (see execute)
+  const auto fail = [&](muon_status_t s) { (void)end_call(h, stream); return s; };
   if ((st = upload_table(h, h->adams, table.data(), table.size() * sizeof(muon::AdamDesc), stream)) != MUON_OK)
-    return st;
+    return fail(st);
   // scalars: bias corrections in double, then fp32
   const double t = double(hp->step);
   const double bc1 = 1.0 - std::pow(double(hp->beta1), t), bc2 = 1.0 - std::pow(double(hp->beta2), t);
@@ -1076,7 +1099,7 @@ muon_status_t muon_adamw_step(muon_handle_t h, const muon_adamw_param_t* params,
                                          gr.pdt == MUON_BF16 ? muon::DT_BF16 : muon::DT_F32,
                                          gr.gdt == MUON_BF16 ? muon::DT_BF16 : muon::DT_F32, sc, gr.bytes,
                                          stream, h->profiling ? &h->timer : nullptr);
-    if (e != hipSuccess) return device_fail(h, "kernel launch", e);
+    if (e != hipSuccess) return fail(device_fail(h, "kernel launch", e));
   }
   return end_call(h, stream);
 }

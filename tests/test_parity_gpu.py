@@ -462,6 +462,46 @@ def test_second_stream_gives_the_same_bits(muon):
         muon.set_streams(3)
 
 
+def test_workspace_growth_between_calls_on_two_streams():
+    # one handle and no host synchronisation between its calls: a small call
+    # on a side stream, a larger one on the current stream (the workspace
+    # grows: the handle waits for its own earlier call before freeing the old
+    # one), and the small one again on the side stream; each result equals
+    # the same call made alone on a fresh handle
+    import torch
+    from paper_2609_21594_amd.binding import Muon
+    require_gpu()
+    small = [(256, 512), (512, 256)]
+    large = [(1024, 2048), (2048, 1024), (768, 768)]
+    calls = [(small, 41), (large, 42), (small, 43)]
+    want = []
+    for shapes, key in calls:
+        ref_h = Muon(0)
+        try:
+            want.append(_step_bits(ref_h, shapes, key=key))
+        finally:
+            ref_h.close()
+    args = [([to_dev(gen(s, 0.02, "bf16", key, i, 0), "bf16") for i, s in enumerate(shapes)],
+             [to_dev(gen(s, 1e-3, "bf16", key, i, 1), "bf16") for i, s in enumerate(shapes)],
+             [to_dev(gen(s, 1e-3, "f32", key, i, 2), "f32") for i, s in enumerate(shapes)])
+            for shapes, key in calls]
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    h = Muon(0)
+    try:
+        sizes = []
+        for (W, g, m), st in zip(args, (side, None, side)):
+            h.step(W, g, m, ns_precision="bf16", stream=st)
+            sizes.append(h.workspace_bytes)
+        torch.cuda.synchronize()
+    finally:
+        h.close()
+    assert sizes[1] > sizes[0] and sizes[2] == sizes[1]
+    for (W, g, m), (wW, wm) in zip(args, want):
+        for x, y in zip([to_bits(t) for t in W] + [to_bits(t) for t in m], wW + wm):
+            np.testing.assert_array_equal(x, y)
+
+
 def test_errors_leave_buffers_untouched(muon):
     import torch
     from paper_2609_21594_amd.binding import Muon, MuonError
