@@ -37,7 +37,13 @@
  *     caller passes must stay alive until that work has completed.
  *   - Every argument is checked before the first launch: a call that returns
  *     an error other than MUON_ERR_DEVICE changed nothing.  Values inside the
- *     tensors are never checked; NaN and Inf propagate.
+ *     tensors are never checked; NaN and Inf propagate.  The calls that
+ *     launch work (muon_step, ns_orthogonalize_batched, muon_adamw_step) also
+ *     ask the runtime about every buffer: it must start in device memory of
+ *     the handle's device (or managed memory) and, where the runtime reports
+ *     the allocation holding it, end inside that allocation; otherwise
+ *     MUON_ERR_INVALID_ARGUMENT.  muon_validate_step does not query the
+ *     runtime and accepts any address.
  *   - A handle is not thread-safe; use one handle per host thread.
  *   - Results are deterministic: the same call on the same data gives the same
  *     bits, and a matrix's result does not depend on which other matrices

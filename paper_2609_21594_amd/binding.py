@@ -244,6 +244,15 @@ def params_array(params, grads, moms, entry_coeffs=None, entry_scale_modes=None)
     return arr, keep
 
 
+def _check_device(tensors, device: int):
+    """Every tensor must live on the handle's GPU: a host tensor's address
+    must never reach a kernel."""
+    for t in tensors:
+        t = t.t if isinstance(t, RowBlocks) else t
+        if t.device.type != "cuda" or t.device.index != device:
+            raise ValueError(f"tensor on {t.device}, the handle runs on cuda:{device}")
+
+
 def _stream_ptr(stream) -> int:
     import torch
     if stream is None:
@@ -308,6 +317,7 @@ class Muon:
              **hp_kw):
         """In place: momentum and params updated, grads read (muon_step).
         entry_coeffs / entry_scale_modes: optional per-entry overrides."""
+        _check_device(list(params) + list(grads) + list(moms), self.device)
         arr, keep_e = params_array(params, grads, moms, entry_coeffs, entry_scale_modes)
         hp, keep = make_hparams(**hp_kw)
         self._check(self.lib.muon_step(self.h, arr, len(params), ctypes.byref(hp),
@@ -321,6 +331,7 @@ class Muon:
         n = len(params)
         if not (len(grads) == len(exp_avgs) == len(exp_avg_sqs) == n):
             raise ValueError("params, grads and moments must have equal length")
+        _check_device(list(params) + list(grads) + list(exp_avgs) + list(exp_avg_sqs), self.device)
         arr = (AdamWParam * max(1, n))()
         for i, (p, g, m, v) in enumerate(zip(params, grads, exp_avgs, exp_avg_sqs)):
             if not (p.numel() == g.numel() == m.numel() == v.numel()):
@@ -345,6 +356,7 @@ class Muon:
             raise ValueError("inputs and outputs differ in length")
         if n == 0:
             return
+        _check_device(list(inputs) + list(outputs), self.device)
         dt = _dtype_code(inputs[0])
         ins = (ctypes.c_void_p * n)()
         outs = (ctypes.c_void_p * n)()

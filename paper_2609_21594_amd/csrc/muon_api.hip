@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdint>
 #include <cstring>
 #include <map>
 #include <new>
@@ -271,6 +272,18 @@ muon_status_t check_dims(int64_t rows, int64_t cols, int64_t batch, const char* 
   return MUON_OK;
 }
 
+// The first and one-past-last byte a buffer of a call touches.
+struct Span { uintptr_t lo, hi; };
+
+Span hull(const std::vector<Run>& rs, size_t from) {
+  Span s{UINTPTR_MAX, 0};
+  for (size_t i = from; i < rs.size(); ++i) {
+    s.lo = std::min(s.lo, rs[i].lo);
+    s.hi = std::max(s.hi, rs[i].hi());
+  }
+  return s;
+}
+
 // The bytes a view of `batch` planes occupies, as runs.  Row i of plane e
 // starts at element e*ps + (i / rb)*bs + (i % rb)*ld; validation has already
 // ensured that rows, blocks and planes follow each other without overlap.
@@ -313,7 +326,8 @@ void view_runs(uintptr_t base, size_t es, int64_t rows, int64_t cols, int64_t ba
 }
 
 muon_status_t validate_step(const muon_param_t* params, int64_t n, const muon_hparams_t* hp,
-                            std::vector<Item>* items, CoeffTables* tables, Msg& msg) {
+                            std::vector<Item>* items, CoeffTables* tables, Msg& msg,
+                            std::vector<Span>* spans = nullptr) {
   muon_status_t st = check_hparams(hp, msg);
   if (st != MUON_OK) return st;
   if (tables) {
@@ -393,10 +407,20 @@ muon_status_t validate_step(const muon_param_t* params, int64_t n, const muon_hp
       msg.set("entry %lld: pointer not aligned to its element size", (long long)i);
       return MUON_ERR_INVALID_ARGUMENT;
     }
+    const size_t r0 = runs.size();
     view_runs(W, dtype_size(p.param_dtype), p.rows, p.cols, p.batch, ld, rb, bs, ps, true, runs);
+    const size_t r1 = runs.size();
     view_runs(G, dtype_size(p.grad_dtype), p.rows, p.cols, p.batch, ld, rb, bs, ps, false, runs);
+    const size_t r2 = runs.size();
     if (mdense) view_runs(M, 4, p.rows, p.cols, p.batch, p.cols, p.rows, plane, plane, true, runs);
     else view_runs(M, 4, p.rows, p.cols, p.batch, ld, rb, bs, ps, true, runs);
+    if (spans) {
+      const std::vector<Run> w(runs.begin() + long(r0), runs.begin() + long(r1));
+      const std::vector<Run> g(runs.begin() + long(r1), runs.begin() + long(r2));
+      spans->push_back(hull(w, 0));
+      spans->push_back(hull(g, 0));
+      spans->push_back(hull(runs, r2));
+    }
     if (items) {
       for (int64_t e = 0; e < p.batch; ++e) {
         Item it;
@@ -432,7 +456,7 @@ muon_status_t validate_step(const muon_param_t* params, int64_t n, const muon_hp
 muon_status_t validate_orth(const void* const* in, void* const* out, const int64_t* rows,
                             const int64_t* cols, int64_t n, int dtype, int32_t ns_steps,
                             const float* coeffs, float eps, int prec, std::vector<Item>* items,
-                            Msg& msg) {
+                            Msg& msg, std::vector<Span>* spans = nullptr) {
   if (n < 0) { msg.set("n must be >= 0"); return MUON_ERR_INVALID_ARGUMENT; }
   if (n > 0 && (!in || !out || !rows || !cols)) { msg.set("NULL array argument"); return MUON_ERR_INVALID_ARGUMENT; }
   if (!dtype_ok(dtype)) { msg.set("unknown dtype"); return MUON_ERR_INVALID_ARGUMENT; }
@@ -456,6 +480,10 @@ muon_status_t validate_orth(const void* const* in, void* const* out, const int64
     } else {
       runs.push_back({a, bytes, bytes, 1, false});
       runs.push_back({b, bytes, bytes, 1, true});
+    }
+    if (spans) {
+      spans->push_back({a, a + bytes});
+      if (b != a) spans->push_back({b, b + bytes});
     }
     if (items) {
       Item it;
@@ -802,7 +830,7 @@ muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Pla
 // AdamW: checks, then one launch per (param, grad) dtype pair over the
 // tensors of that pair.
 muon_status_t validate_adamw(const muon_adamw_param_t* params, int64_t n, const muon_adamw_hparams_t* hp,
-                             Msg& msg) {
+                             Msg& msg, std::vector<Span>* spans = nullptr) {
   if (!hp) { msg.set("hparams is NULL"); return MUON_ERR_INVALID_ARGUMENT; }
   if (!std::isfinite(hp->lr) || !std::isfinite(hp->weight_decay) || !std::isfinite(hp->eps) ||
       !(hp->eps > 0.f)) {
@@ -833,8 +861,46 @@ muon_status_t validate_adamw(const muon_adamw_param_t* params, int64_t n, const 
     runs.push_back({G, ne * gs, ne * gs, 1, false});
     runs.push_back({M, ne * 4, ne * 4, 1, true});
     runs.push_back({V, ne * 4, ne * 4, 1, true});
+    if (spans)
+      for (const Span& sp : {Span{P, P + ne * ps}, Span{G, G + ne * gs}, Span{M, M + ne * 4}, Span{V, V + ne * 4}})
+        spans->push_back(sp);
   }
   if (!runs_disjoint(runs)) { msg.set("param, grad and moment buffers overlap"); return MUON_ERR_INVALID_ARGUMENT; }
+  return MUON_OK;
+}
+
+// Launching calls only (host-only validation takes any address): every
+// buffer must start in device memory of the handle's device, or in managed
+// memory, and where the runtime reports the allocation that holds it, end
+// inside that allocation.  A host pointer or a view past the end of its
+// allocation is an error here instead of a fault in a kernel.
+muon_status_t check_device_spans(muon_handle_t h, const std::vector<Span>& spans) {
+  for (const Span& s : spans) {
+    if (s.hi <= s.lo) continue;
+    void* p = reinterpret_cast<void*>(s.lo);
+    hipPointerAttribute_t a{};
+    if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+      (void)hipGetLastError();
+      set_err(h, "buffer at %p is not device memory", p);
+      return MUON_ERR_INVALID_ARGUMENT;
+    }
+    const bool managed = a.isManaged || a.type == hipMemoryTypeManaged;
+    if (!managed && !(a.type == hipMemoryTypeDevice && a.device == h->device)) {
+      set_err(h, "buffer at %p is not device memory of device %d", p, h->device);
+      return MUON_ERR_INVALID_ARGUMENT;
+    }
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    if (hipMemGetAddressRange(&base, &size, p) == hipSuccess && base) {
+      const uintptr_t end = reinterpret_cast<uintptr_t>(base) + size;
+      if (s.hi > end) {
+        set_err(h, "buffer at %p reaches %zu bytes past the end of its allocation", p, size_t(s.hi - end));
+        return MUON_ERR_INVALID_ARGUMENT;
+      }
+    } else {
+      (void)hipGetLastError();
+    }
+  }
   return MUON_OK;
 }
 
@@ -1025,9 +1091,11 @@ muon_status_t muon_step(muon_handle_t h, const muon_param_t* params, int64_t n,
   Msg m{buf, sizeof buf};
   std::vector<Item> items;
   CoeffTables tables;
-  muon_status_t st = validate_step(params, n, hp, &items, &tables, m);
+  std::vector<Span> spans;
+  muon_status_t st = validate_step(params, n, hp, &items, &tables, m, &spans);
   if (st != MUON_OK) { h->err = buf; return st; }
   if (items.empty()) return MUON_OK;
+  if ((st = check_device_spans(h, spans)) != MUON_OK) return st;
   const bool f32 = hp->ns_precision == MUON_NS_F32;
   const Plan plan = make_plan(items, hp->max_chunk_elems, f32, step_counts(tables));
   StepScalars sc{};
@@ -1047,8 +1115,10 @@ muon_status_t muon_adamw_step(muon_handle_t h, const muon_adamw_param_t* params,
   h->err.clear();
   char buf[256] = {0};
   Msg m{buf, sizeof buf};
-  muon_status_t st = validate_adamw(params, n, hp, m);
+  std::vector<Span> spans;
+  muon_status_t st = validate_adamw(params, n, hp, m, &spans);
   if (st != MUON_OK) { h->err = buf; return st; }
+  if ((st = check_device_spans(h, spans)) != MUON_OK) return st;
   const hipStream_t stream = static_cast<hipStream_t>(stream_);
   // tensors grouped by dtype pair; workgroup ranges per group
   std::vector<muon::AdamDesc> table;
@@ -1113,9 +1183,11 @@ muon_status_t ns_orthogonalize_batched(muon_handle_t h, const void* const* in, v
   char buf[256] = {0};
   Msg m{buf, sizeof buf};
   std::vector<Item> items;
-  muon_status_t st = validate_orth(in, out, rows, cols, n, dtype, ns_steps, ns_coeffs, eps, prec, &items, m);
+  std::vector<Span> spans;
+  muon_status_t st = validate_orth(in, out, rows, cols, n, dtype, ns_steps, ns_coeffs, eps, prec, &items, m, &spans);
   if (st != MUON_OK) { h->err = buf; return st; }
   if (items.empty()) return MUON_OK;
+  if ((st = check_device_spans(h, spans)) != MUON_OK) return st;
   const bool f32 = prec == MUON_NS_F32;
   const CoeffTables tables{coefficient_table(ns_steps, ns_coeffs)};
   const Plan plan = make_plan(items, 0, f32, step_counts(tables));

@@ -44,3 +44,13 @@ def test_overlapping_layouts_are_refused(make):
 def test_columns_must_be_contiguous():
     with pytest.raises(ValueError):
         _view(torch.zeros(8, 8).t())
+
+
+def test_tensors_off_the_handles_device_are_refused():
+    from paper_2609_21594_amd.binding import _check_device
+    W = torch.zeros(4, 8)
+    with pytest.raises(ValueError, match="cuda:0"):
+        _check_device([W], 0)
+    with pytest.raises(ValueError):
+        _check_device([RowBlocks(W.view(2, 2, 8))], 0)
+    _check_device([], 0)
