@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstdint>
 #include <cstring>
 #include <map>
@@ -102,6 +103,7 @@ struct muon_handle {
   int nstreams = 2;
   hipStream_t side = nullptr;
   hipEvent_t fork = nullptr, join = nullptr;
+  bool log = false;                  // MUON_HIP_LOG set (and not "0"): each call's plan on stderr
   std::string err;
 };
 
@@ -777,6 +779,20 @@ muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Pla
   }
   muon_status_t st = ensure_workspace(h, two ? slot + side_bytes : plan.ws_bytes);
   if (st != MUON_OK) return st;
+  if (h->log) {
+    std::fprintf(stderr, "muon: %zu matrices in %zu chunks, %s NS, %s, workspace %zu bytes\n",
+                 plan.order.size(), plan.chunks.size(), ns_f32 ? "fp32" : "bf16",
+                 two ? "two streams" : "one stream", h->ws_bytes);
+    for (size_t ci = 0; ci < plan.chunks.size(); ++ci) {
+      const Chunk& c = plan.chunks[ci];
+      std::fprintf(stderr,
+                   "muon:   chunk %zu: %lld matrices of %lld x %lld (padded %lld x %lld), K = %zu, "
+                   "coefficient set %d, X^T %s, %s stream, %zu workspace bytes\n",
+                   ci, (long long)c.count, (long long)c.s, (long long)c.l, (long long)c.S, (long long)c.L,
+                   tables[size_t(c.cset)].size() / 3, int(c.cset), c.keeps_xt ? "kept" : "not kept",
+                   on_side[ci] ? "second" : "caller's", c.bytes);
+    }
+  }
   if ((st = begin_call(h, stream)) != MUON_OK) return st;
   // From here every exit records call_done, so that later calls wait for
   // whatever this one managed to enqueue.
@@ -945,6 +961,8 @@ muon_status_t muon_create(muon_handle_t* out, int device) {
   muon_handle* h = new (std::nothrow) muon_handle();
   if (!h) return MUON_ERR_OUT_OF_MEMORY;
   h->device = device;
+  const char* lg = std::getenv("MUON_HIP_LOG");
+  h->log = lg && *lg && std::strcmp(lg, "0") != 0;
   DeviceGuard dg(device);
   auto drop_side = [h]() {
     if (h->side) (void)hipStreamDestroy(h->side);

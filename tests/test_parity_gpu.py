@@ -195,6 +195,41 @@ def test_custom_per_step_coefficients(muon):
         assert rel(to_host(o), want) <= 1e-4
 
 
+@pytest.mark.parametrize("prec", ["bf16", "f32"])
+@pytest.mark.parametrize("steps", [1, 2])
+def test_one_and_two_steps_match_oracle(muon, steps, prec):
+    # K = 1: the first step is also the last, so the last-step kernel applies
+    # the norm scale r itself (on the 256 x 256 kernel for the bf16 upper
+    # shapes, on the 128 x 128 kernel otherwise); K = 2: one exchange of the
+    # ping-pong iterates.  Both the parameter update and the standalone
+    # orthogonalisation, whose last kernel writes O.
+    import torch
+    shapes = UPPER_SHAPES + [(300, 200), (129, 257)]
+    # lr large enough that one step's update stands well above the bf16
+    # rounding of W (X1 is still far from orthogonal, so O is small)
+    hp = ref.MuonHParams(lr=0.5, beta=0.95, weight_decay=0.01, ns_steps=steps)
+    Ws = [gen(s, 0.02, "bf16", 24, steps, i, 0) for i, s in enumerate(shapes)]
+    gs = [gen(s, 1e-3, "bf16", 24, steps, i, 1) for i, s in enumerate(shapes)]
+    bs = [gen(s, 1e-3, "f32", 24, steps, i, 2) for i, s in enumerate(shapes)]
+    dW, dg, db = [to_dev(w, "bf16") for w in Ws], [to_dev(g, "bf16") for g in gs], [to_dev(b, "f32") for b in bs]
+    muon.step(dW, dg, db, lr=hp.lr, beta=hp.beta, weight_decay=hp.weight_decay, ns_steps=steps,
+              ns_precision=prec)
+    torch.cuda.synchronize()
+    for s, W, g, b, w_dev, b_dev in zip(shapes, Ws, gs, bs, dW, db):
+        W0 = decode(W, "bf16")
+        r = ref.muon_step_matrix(W0, decode(g, "bf16"), np.asarray(b, np.float64), hp)
+        err, rho = w_gate(to_host(w_dev), r.W_new, W0, "bf16")
+        print(f"K={steps} {prec} step {s}: W err {err:.3e} (rho {rho:.1e})", flush=True)
+        assert err <= tol_for(prec, s) + rho, (s, err, rho)
+        assert rel(to_host(b_dev), r.buf_new) <= MOMENTUM_TOL, s
+    G, outs = run_orth(muon, shapes, "bf16", prec, ns_steps=steps, key=25 + steps)
+    for s, g, o in zip(shapes, G, outs):
+        want = ref.orthogonalize(decode(g, "bf16"), steps)
+        err, rho = o_gate(to_host(o), want, "bf16")
+        print(f"K={steps} {prec} orthogonalize {s}: O err {err:.3e} (rho {rho:.1e})", flush=True)
+        assert err <= tol_for(prec, s) + rho, (s, err, rho)
+
+
 def test_zero_steps_returns_normalised_input(muon):
     G, outs = run_orth(muon, [(40, 70), (70, 40)], "f32", "f32", ns_steps=0, key=5)
     for g, o in zip(G, outs):
