@@ -40,9 +40,9 @@
  *     tensors are never checked; NaN and Inf propagate.  The calls that
  *     launch work (muon_step, ns_orthogonalize_batched, muon_adamw_step) also
  *     ask the runtime about every buffer: it must start in device memory of
- *     the handle's device (or managed memory) and, where the runtime reports
- *     the allocation holding it, end inside that allocation; otherwise
- *     MUON_ERR_INVALID_ARGUMENT.  muon_validate_step does not query the
+ *     the handle's device (or managed memory), and if it reaches beyond the
+ *     allocation that holds its start, its last byte must be such memory too
+ *     (allocations mapped back to back); otherwise MUON_ERR_INVALID_ARGUMENT.  muon_validate_step does not query the
  *     runtime and accepts any address.
  *   - A handle is not thread-safe; use one handle per host thread.
  *   - Results are deterministic: the same call on the same data gives the same

@@ -886,35 +886,37 @@ muon_status_t validate_adamw(const muon_adamw_param_t* params, int64_t n, const 
 }
 
 // Launching calls only (host-only validation takes any address): every
-// buffer must start in device memory of the handle's device, or in managed
-// memory, and where the runtime reports the allocation that holds it, end
-// inside that allocation.  A host pointer or a view past the end of its
-// allocation is an error here instead of a fault in a kernel.
+// buffer must start in device memory of the handle's device (or managed
+// memory), and if it reaches beyond the allocation that holds its start, its
+// last byte must be such memory too (a tensor may span several allocations
+// mapped back to back).  A host pointer, another device's memory, or a view
+// that runs past its allocation into unmapped addresses is an error here
+// instead of a fault in a kernel.
 muon_status_t check_device_spans(muon_handle_t h, const std::vector<Span>& spans) {
+  const auto device_mem = [&](uintptr_t addr) {
+    hipPointerAttribute_t a{};
+    if (hipPointerGetAttributes(&a, reinterpret_cast<const void*>(addr)) != hipSuccess) {
+      (void)hipGetLastError();
+      return false;
+    }
+    return a.isManaged || a.type == hipMemoryTypeManaged || (a.type == hipMemoryTypeDevice && a.device == h->device);
+  };
   for (const Span& s : spans) {
     if (s.hi <= s.lo) continue;
-    void* p = reinterpret_cast<void*>(s.lo);
-    hipPointerAttribute_t a{};
-    if (hipPointerGetAttributes(&a, p) != hipSuccess) {
-      (void)hipGetLastError();
-      set_err(h, "buffer at %p is not device memory", p);
-      return MUON_ERR_INVALID_ARGUMENT;
-    }
-    const bool managed = a.isManaged || a.type == hipMemoryTypeManaged;
-    if (!managed && !(a.type == hipMemoryTypeDevice && a.device == h->device)) {
-      set_err(h, "buffer at %p is not device memory of device %d", p, h->device);
+    if (!device_mem(s.lo)) {
+      set_err(h, "buffer at %p is not device memory of device %d", reinterpret_cast<void*>(s.lo), h->device);
       return MUON_ERR_INVALID_ARGUMENT;
     }
     hipDeviceptr_t base = nullptr;
     size_t size = 0;
-    if (hipMemGetAddressRange(&base, &size, p) == hipSuccess && base) {
-      const uintptr_t end = reinterpret_cast<uintptr_t>(base) + size;
-      if (s.hi > end) {
-        set_err(h, "buffer at %p reaches %zu bytes past the end of its allocation", p, size_t(s.hi - end));
-        return MUON_ERR_INVALID_ARGUMENT;
-      }
-    } else {
-      (void)hipGetLastError();
+    if (hipMemGetAddressRange(&base, &size, reinterpret_cast<hipDeviceptr_t>(s.lo)) == hipSuccess && base &&
+        s.hi <= reinterpret_cast<uintptr_t>(base) + size)
+      continue;
+    (void)hipGetLastError();
+    if (!device_mem(s.hi - 1)) {
+      set_err(h, "buffer at %p reaches past the end of its allocation: its last byte (%p) is not device memory of device %d",
+              reinterpret_cast<void*>(s.lo), reinterpret_cast<void*>(s.hi - 1), h->device);
+      return MUON_ERR_INVALID_ARGUMENT;
     }
   }
   return MUON_OK;

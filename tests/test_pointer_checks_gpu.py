@@ -63,23 +63,33 @@ def test_host_buffers_are_refused(guarded):
 
 
 def test_view_past_its_allocation_is_refused(guarded):
-    # a parameter that starts 4 KB before the end of a device allocation and
-    # spans 8 KB: its start is device memory, its end is not
+    # a two-row parameter whose second row starts 32 TB after its first: the
+    # first lies in a device allocation, the last byte in unmapped addresses
     import torch
+    from paper_2609_21594_amd import binding as B
     hip = ctypes.CDLL("libamdhip64.so")
-    torch.cuda.empty_cache()
     t = torch.empty(16 << 20, dtype=torch.uint8, device="cuda")
+    g = torch.zeros((2, 4096), dtype=torch.bfloat16, device="cuda")
+    mom = torch.zeros((2, 4096), dtype=torch.float32, device="cuda")
+    ld = 1 << 44  # elements
+    # the gradient: the next 8 KB of the same allocation, in the same layout;
+    # the momentum dense
+    arr = (B.MuonParam * 1)(B.MuonParam(t.data_ptr(), t.data_ptr() + 8192, mom.data_ptr(), 2, 4096, 1, ld,
+                                        B.BF16, B.BF16, 0, 0, 0, 1, 0))
+    hp, keep = B.make_hparams()
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    st = guarded.lib.muon_step(guarded.h, arr, 1, ctypes.byref(hp), stream)
+    msg = guarded.lib.muon_last_error(guarded.h).decode()
+    assert st == INVALID and "past the end" in msg, (st, msg)
+    # a view that ends exactly at the end of its allocation passes the checks
+    # and stops at the workspace limit
     base, size = ctypes.c_void_p(), ctypes.c_size_t()
     assert hip.hipMemGetAddressRange(ctypes.byref(base), ctypes.byref(size), ctypes.c_void_p(t.data_ptr())) == 0
     end = base.value + size.value
-    g = torch.zeros((1, 4096), dtype=torch.bfloat16, device="cuda")
-    mom = torch.zeros((1, 4096), dtype=torch.float32, device="cuda")
     for a in (g, mom):  # the other buffers lie in allocations of their own
         assert not (base.value <= a.data_ptr() < end)
-    st, msg = step_raw(guarded, end - 4096, g.data_ptr(), mom.data_ptr(), 1, 4096)
-    assert st == INVALID and "past the end" in msg, (st, msg)
-    # the same view ending exactly at the end of the allocation passes the
-    # checks and stops at the workspace limit
-    st, msg = step_raw(guarded, end - 8192, g.data_ptr(), mom.data_ptr(), 1, 4096)
-    assert st == OOM, (st, msg)
+    arr = (B.MuonParam * 1)(B.MuonParam(end - 8192, g.data_ptr(), mom.data_ptr(), 1, 4096, 1, 0,
+                                        B.BF16, B.BF16))
+    st = guarded.lib.muon_step(guarded.h, arr, 1, ctypes.byref(hp), stream)
+    assert st == OOM, (st, guarded.lib.muon_last_error(guarded.h).decode())
     torch.cuda.synchronize()
