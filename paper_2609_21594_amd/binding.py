@@ -126,13 +126,22 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     return lib
 
 
+def _coeff_table(ns_coeffs, ns_steps):
+    """Flattened K x 3 table; the library reads 3 * ns_steps values, so the
+    table must have exactly ns_steps rows of three."""
+    rows = [tuple(float(v) for v in r) for r in ns_coeffs]
+    if any(len(r) != 3 for r in rows) or len(rows) != int(ns_steps):
+        raise ValueError(f"ns_coeffs must be {int(ns_steps)} rows of (a, b, c), got {len(rows)}")
+    return [v for r in rows for v in r]
+
+
 def make_hparams(lr=0.02, beta=0.95, weight_decay=0.0, eps=1e-7, ns_steps=5, nesterov=True,
                  ns_coeffs: Optional[Sequence[Sequence[float]]] = None, ns_precision="bf16",
                  scale_mode=0, max_chunk_elems=0):
     """Returns (struct, keepalive) — keep the second item alive during the call."""
     coeff_arr = None
     if ns_coeffs is not None:
-        flat = [float(v) for row in ns_coeffs for v in row]
+        flat = _coeff_table(ns_coeffs, ns_steps)
         coeff_arr = (ctypes.c_float * max(1, len(flat)))(*flat)
     hp = MuonHParams(lr, beta, weight_decay, eps, int(ns_steps), int(bool(nesterov)),
                      ctypes.cast(coeff_arr, ctypes.POINTER(ctypes.c_float)) if coeff_arr else None,
@@ -232,8 +241,8 @@ def params_array(params, grads, moms, entry_coeffs=None, entry_scale_modes=None)
             raise ValueError(f"entry {i}: momentum must have the param's view or be dense")
         ctab, csteps = None, 0
         if entry_coeffs[i] is not None:
-            flat = [float(v) for r in entry_coeffs[i] for v in r]
-            csteps = len(flat) // 3
+            csteps = len(entry_coeffs[i])
+            flat = _coeff_table(entry_coeffs[i], csteps)
             ctab = (ctypes.c_float * max(1, len(flat)))(*flat)
             keep.append(ctab)
         smode = 0 if entry_scale_modes[i] is None else 1 + int(entry_scale_modes[i])
@@ -373,7 +382,7 @@ class Muon:
             rows[i], cols[i] = a.shape[0], a.shape[1]
         coeff = None
         if ns_coeffs is not None:
-            flat = [float(v) for r in ns_coeffs for v in r]
+            flat = _coeff_table(ns_coeffs, ns_steps)
             coeff = (ctypes.c_float * max(1, len(flat)))(*flat)
         self._check(self.lib.ns_orthogonalize_batched(
             self.h, ins, outs, rows, cols, n, dt, int(ns_steps),

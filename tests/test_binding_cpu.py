@@ -54,3 +54,19 @@ def test_tensors_off_the_handles_device_are_refused():
     with pytest.raises(ValueError):
         _check_device([RowBlocks(W.view(2, 2, 8))], 0)
     _check_device([], 0)
+
+
+def test_coefficient_tables_must_match_the_step_count():
+    # the library reads 3 * ns_steps values from the table
+    from paper_2609_21594_amd.binding import make_hparams
+    make_hparams(ns_coeffs=[(1.5, -0.5, 0.0)] * 3, ns_steps=3)
+    with pytest.raises(ValueError):
+        make_hparams(ns_coeffs=[(1.5, -0.5, 0.0)] * 2, ns_steps=3)
+    with pytest.raises(ValueError):
+        make_hparams(ns_coeffs=[(1.5, -0.5)] * 3, ns_steps=3)
+
+
+def test_optimizer_needs_gpu_parameters():
+    from paper_2609_21594_amd.optim import MuonAdamW
+    with pytest.raises(ValueError, match="one GPU"):
+        MuonAdamW([torch.nn.Parameter(torch.zeros(4, 4))])
