@@ -110,3 +110,34 @@ def test_groups_late_parameters_and_state_dict():
             opt2.close()
     finally:
         opt.close()
+
+
+def test_trains_a_small_mlp():
+    # autograd forward/backward in torch (fp32), updates by the library: the
+    # weights (2-D) take Muon, the biases AdamW; a fixed random target
+    # function is fitted, and the loss must fall well below where it starts
+    require_gpu()
+    import torch
+    from paper_2609_21594_amd.optim import MuonAdamW
+    g = torch.Generator(device="cpu").manual_seed(1234)
+    X = torch.randn(512, 64, generator=g).cuda()
+    A, Bm = torch.randn(64, 48, generator=g).cuda() / 8, torch.randn(48, 16, generator=g).cuda() / 7
+    Y = torch.tanh(X @ A) @ Bm
+    torch.manual_seed(0)
+    model = torch.nn.Sequential(torch.nn.Linear(64, 128), torch.nn.Tanh(), torch.nn.Linear(128, 16)).cuda()
+    opt = MuonAdamW(model.parameters(), lr=0.02, weight_decay=0.0, adamw_lr=3e-3)
+    start = [p.detach().clone() for p in model.parameters()]
+    losses = []
+    try:
+        for _ in range(60):
+            loss = torch.nn.functional.mse_loss(model(X), Y)
+            opt.zero_grad()
+            loss.backward()
+            opt.step()
+            losses.append(float(loss.detach()))
+    finally:
+        opt.close()
+    print(f"mlp loss {losses[0]:.4f} -> {losses[-1]:.4f}", flush=True)
+    assert losses[-1] < 0.25 * losses[0], losses[::10]
+    for p, p0 in zip(model.parameters(), start):
+        assert not torch.equal(p.detach(), p0)
