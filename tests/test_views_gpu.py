@@ -49,7 +49,9 @@ def oracle_check(W_dev, W0, g, m0, m_dev, pdt):
     assert rel(to_host(m_dev), r.buf_new) <= MOMENTUM_TOL
 
 
-@pytest.mark.parametrize("H,hd,d", [(4, 64, 256), (3, 40, 200)])
+# (8, 128, 512): q and k are 1024 x 512, tall, so they are transposed first
+# and their last step writes W blocks back transposed through the row blocks
+@pytest.mark.parametrize("H,hd,d", [(4, 64, 256), (3, 40, 200), (8, 128, 512)])
 def test_interleaved_heads_of_fused_qkv(muon, H, hd, d):
     # [3*H*hd, d] with rows grouped per head as (q_h, k_h, v_h); q and k are
     # [H*hd, d] logical matrices of H row blocks each; v is left alone
@@ -76,7 +78,9 @@ def test_interleaved_heads_of_fused_qkv(muon, H, hd, d):
 
 
 @pytest.mark.parametrize("pdt", ["bf16", "f32"])
-@pytest.mark.parametrize("E,d,f", [(2, 512, 256), (2, 256, 384)])
+# (2, 1024, 256): tall 1024 x 256 halves, transposed first, on the 256 x 256
+# kernel with a column-range view
+@pytest.mark.parametrize("E,d,f", [(2, 512, 256), (2, 256, 384), (2, 1024, 256)])
 def test_gate_up_halves_of_packed_expert_weights(muon, pdt, E, d, f):
     # [E, d, 2f] packed gate|up: two stacked [E, d, f] views (ld = 2f, plane
     # stride d*2f).  The gate's momentum shares the view; the up half keeps
