@@ -905,26 +905,35 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
     qto[i] = static_cast<uint32_t>(t * ga.ldq + ((lane % 32) ^ ((t & 3) << 2)) * 16);
   }
   const uint32_t lds0 = lds_offset(smem);
-  auto issue = [&](int ks) __attribute__((always_inline)) {
+  // The loads of slab ks, one operand at a time: P's NLP instructions or Q's
+  // NLQ, into the slab's stage.
+  auto issue_op = [&](auto qc, int ks) __attribute__((always_inline)) {
     const uint32_t base = lds0 + (ks & 1) * STAGE;
-    if (CAN_PT && ks < p_tr_end) {
-      const char* b = Pt + static_cast<int64_t>(ks) * 64 * ga.ldp;
+    if constexpr (!decltype(qc)::value) {
+      if (CAN_PT && ks < p_tr_end) {
+        const char* b = Pt + static_cast<int64_t>(ks) * 64 * ga.ldp;
 #pragma unroll
-      for (int i = 0; i < NLP; ++i) load_lds16(b, pto[i], base + (wave * PR + RPI * i) * SLAB);
+        for (int i = 0; i < NLP; ++i) load_lds16(b, pto[i], base + (wave * PR + RPI * i) * SLAB);
+      } else {
+        const char* b = Pd + ks * SLAB;
+#pragma unroll
+        for (int i = 0; i < NLP; ++i) load_lds16(b, pdo[i], base + (wave * PR + RPI * i) * SLAB);
+      }
     } else {
-      const char* b = Pd + ks * SLAB;
+      if (CAN_QT && (!CAN_QD || ks < q_tr_end)) {
+        const char* b = Qt + static_cast<int64_t>(ks) * 64 * ga.ldq;
 #pragma unroll
-      for (int i = 0; i < NLP; ++i) load_lds16(b, pdo[i], base + (wave * PR + RPI * i) * SLAB);
+        for (int i = 0; i < NLQ; ++i) load_lds16(b, qto[i], base + OPQ + (wave * QR + RPI * i) * SLAB);
+      } else {
+        const char* b = Qd + ks * SLAB;
+#pragma unroll
+        for (int i = 0; i < NLQ; ++i) load_lds16(b, qdo[i], base + OPQ + (wave * QR + RPI * i) * SLAB);
+      }
     }
-    if (CAN_QT && (!CAN_QD || ks < q_tr_end)) {
-      const char* b = Qt + static_cast<int64_t>(ks) * 64 * ga.ldq;
-#pragma unroll
-      for (int i = 0; i < NLQ; ++i) load_lds16(b, qto[i], base + OPQ + (wave * QR + RPI * i) * SLAB);
-    } else {
-      const char* b = Qd + ks * SLAB;
-#pragma unroll
-      for (int i = 0; i < NLQ; ++i) load_lds16(b, qdo[i], base + OPQ + (wave * QR + RPI * i) * SLAB);
-    }
+  };
+  auto issue = [&](int ks) __attribute__((always_inline)) {
+    issue_op(std::false_type{}, ks);
+    issue_op(std::true_type{}, ks);
   };
 
   f32x16_t acc[BI][BJ];
@@ -1075,15 +1084,23 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   // With NEXT, the fragments of the next slab's group 0 (same mode) are read
   // while the last group's MFMAs issue; without, the last group runs alone
   // (the slab before a change of mode, and the last one).
-  // When a slab's loads are issued: right after the barrier that frees its
-  // stage (a whole slab of MFMA work ahead of the barrier that publishes it;
-  // measured faster for the Gram product, whose long K streams the most
-  // operand data), or at the top of the slab before it (3/4 of a slab ahead;
-  // measured faster for the other products).
+  // When a slab's loads are issued, one operand at a time, so that the
+  // workgroups of an XCD do not ask for a whole slab at once:
+  //  - Gram product (EARLY): Q's right after the barrier that frees the
+  //    stage, P's at the top of the next slab (the slab of lead that was
+  //    measured faster for its long K);
+  //  - the other products: Q's at the top of the slab before, P's after
+  //    that slab's first MFMA group (3/4 and 1/2 of a slab ahead).
+  // Splitting the burst by operand measured 2-3% faster on the step than
+  // issuing a slab at once; splitting each operand in halves, or P later,
+  // measured slower.
   constexpr bool EARLY = EPI == EPI_GRAM;
   auto slab = [&](auto ptc, auto qtc, auto nextc, auto ec, int ks) __attribute__((always_inline)) {
     const char* sp = smem + (ks & 1) * STAGE;
-    if (!EARLY && ks + 1 < nk) issue(ks + 1);
+    if (ks + 1 < nk) {
+      if (!EARLY) issue_op(std::true_type{}, ks + 1);
+      else if (ks >= 1) issue_op(std::false_type{}, ks + 1);  // slab 1 went out whole with slab 0
+    }
     if constexpr (decltype(ec)::value) {
       if (ks == e_ks0 || ks == e_ks1) {  // wave-uniform; at most twice a tile
         __builtin_amdgcn_sched_barrier(0);
@@ -1098,6 +1115,8 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
     __builtin_amdgcn_sched_barrier(0);
     rd(ptc, qtc, sp, I_<1>{}, I_<1>{}); mm(I_<0>{}); interleave(ptc, qtc);
     __builtin_amdgcn_sched_barrier(0);
+    if (!EARLY && ks + 1 < nk) issue_op(std::false_type{}, ks + 1);
+    __builtin_amdgcn_sched_barrier(0);
     rd(ptc, qtc, sp, I_<2>{}, I_<0>{}); mm(I_<1>{}); interleave(ptc, qtc);
     __builtin_amdgcn_sched_barrier(0);
     rd(ptc, qtc, sp, I_<3>{}, I_<1>{}); mm(I_<0>{}); interleave(ptc, qtc);
@@ -1105,7 +1124,7 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // slab ks + 1 has landed
     __syncthreads();
     // every wave is done with slab ks: its stage can take slab ks + 2
-    if (EARLY && ks + 2 < nk) issue(ks + 2);
+    if (EARLY && ks + 2 < nk) issue_op(std::true_type{}, ks + 2);
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (decltype(nextc)::value) {
       rd(ptc, qtc, smem + ((ks + 1) & 1) * STAGE, I_<0>{}, I_<0>{});
