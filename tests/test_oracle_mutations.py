@@ -2,8 +2,9 @@
 
 Each case swaps one oracle function for a plausible wrong version (a dropped
 term, a wrong sign, a transposed operand, eps in the wrong place, the other
-momentum convention, decay applied in the wrong order, rounding twice) and
-runs the pins; the case passes when some pin fails.
+momentum convention, decay applied in the wrong order, rounding twice), or
+one digit of the default coefficient table for another, and runs the pins;
+the case passes when some pin fails.
 """
 import numpy as np
 import pytest
@@ -105,6 +106,10 @@ def _run_all_pins():
         ("diag", pins.test_ns_diagonal_reduces_to_scalars, {}),
         ("apply_scale", pins.test_apply_scale_uses_long_side, {"shape": (6, 9)}),
         ("zero_update", pins.test_apply_zero_update_is_pure_decay, {}),
+        ("legacy_orthogonal", pins.test_legacy_values_on_orthogonal_input, {"n": 128}),
+        ("legacy_vector", pins.test_legacy_value_on_vectors, {"shape": (1, 37)}),
+        ("legacy_rank_one", pins.test_legacy_value_on_rank_one, {}),
+        ("legacy_slope", pins.test_legacy_slope_at_zero, {}),
     ]
     for shape in [(8, 5), (5, 8), (6, 6)]:
         cases.append((f"spectral{shape}", pins.test_ns_spectral_closed_form,
@@ -130,6 +135,11 @@ MUTANTS = {
     "scale_min_side": ("rms_scale", _scale_min_side),
     "decay_after_update": ("apply_update", _apply_decay_after),
     "bf16_double_round": ("round_to_bf16", _round_bf16_via_f32),
+    # one digit off in each coefficient of the default table
+    "legacy_a_typo": ("LEGACY_QUINTIC", (3.4454, -4.7750, 2.0315)),
+    "legacy_b_typo": ("LEGACY_QUINTIC", (3.4445, -4.7705, 2.0315)),
+    "legacy_c_typo": ("LEGACY_QUINTIC", (3.4445, -4.7750, 2.0351)),
+    "legacy_c_last_digit": ("LEGACY_QUINTIC", (3.4445, -4.7750, 2.0316)),
 }
 
 

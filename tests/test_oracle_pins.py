@@ -285,6 +285,62 @@ def test_coefficient_table_validation():
 
 
 # --------------------------------------------------------------------------
+# Values of the default (legacy constant quintic) table, as literals
+#
+# The paper names the legacy constant quintic (Sec. 2.3, Sec. 6.6) but
+# prints no values.  The pins above compute their expectations through the
+# oracle's own constant, so a typo there would move oracle and expectation
+# together.  These pins state, as fixed decimals, what five steps of the
+# default table do to one singular value (f below), and the slope a^5 of f
+# at zero; each value is reached only through the oracle's default table.
+# --------------------------------------------------------------------------
+LEGACY_F_AT_1 = 0.696436            # f(1)
+LEGACY_F_ORTHOGONAL = {             # f(1/sqrt(n)): an n x n orthogonal input
+    128: 0.722762, 256: 1.070524, 512: 0.808607, 4096: 0.902526}
+LEGACY_SLOPE_AT_0 = 484.876287      # f'(0) = a^5
+LEGACY_TOL = 1e-6                   # the literals carry six decimals
+
+
+@pytest.mark.parametrize("n", sorted(LEGACY_F_ORTHOGONAL))
+def test_legacy_values_on_orthogonal_input(n):
+    # Q orthogonal: X_0 = Q / sqrt(n) has every singular value 1/sqrt(n), so
+    # O = f(1/sqrt(n)) Q.  Recover f as <O, Q> / n.
+    rng = np.random.default_rng(n)
+    Q, _ = np.linalg.qr(rng.standard_normal((n, n)))
+    O = ref.orthogonalize(Q, 5, eps=0.0)
+    assert abs(np.sum(O * Q) / n - LEGACY_F_ORTHOGONAL[n]) < LEGACY_TOL
+
+
+@pytest.mark.parametrize("shape", [(1, 37), (37, 1), (1, 1)])
+def test_legacy_value_on_vectors(shape):
+    # a vector has one singular value, ||x||/(||x||+eps) ~ 1: O = f(1) x/||x||
+    rng = np.random.default_rng(17)
+    x = rng.standard_normal(shape) * 5.0
+    O = ref.orthogonalize(x, 5)
+    got = float(np.sum(O * x) / np.linalg.norm(x))
+    assert abs(got - LEGACY_F_AT_1) < LEGACY_TOL
+    np.testing.assert_allclose(O, LEGACY_F_AT_1 * x / np.linalg.norm(x), atol=LEGACY_TOL)
+
+
+def test_legacy_value_on_rank_one():
+    rng = np.random.default_rng(23)
+    u = rng.standard_normal(48); u /= np.linalg.norm(u)
+    v = rng.standard_normal(20); v /= np.linalg.norm(v)
+    O = ref.orthogonalize(12.5 * np.outer(u, v), 5)
+    assert abs(u @ O @ v - LEGACY_F_AT_1) < LEGACY_TOL
+
+
+def test_legacy_slope_at_zero():
+    # diag(1, t) with t tiny: the small singular value t/||d|| leaves Muon
+    # multiplied by f'(0) = a^5 (the cubic and quintic terms are ~t^3).
+    t = 1e-9
+    d = np.array([1.0, t])
+    O = ref.orthogonalize(np.diag(d), 5, eps=0.0)
+    sigma = t / np.sqrt(1.0 + t * t)
+    assert abs(O[1, 1] / sigma - LEGACY_SLOPE_AT_0) < 1e-5
+
+
+# --------------------------------------------------------------------------
 # Update, decay, whole step
 # --------------------------------------------------------------------------
 def test_whole_step_hand_example():
