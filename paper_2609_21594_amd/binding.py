@@ -100,10 +100,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.muon_workspace_bytes.argtypes = [vp]
     lib.muon_workspace_bytes.restype = ctypes.c_size_t
     lib.muon_step.argtypes = [vp, ctypes.POINTER(MuonParam), i64, ctypes.POINTER(MuonHParams), vp]
-    lib.ns_orthogonalize_batched.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp),
-                                             ctypes.POINTER(i64), ctypes.POINTER(i64), i64,
-                                             ctypes.c_int, i32, ctypes.POINTER(ctypes.c_float),
-                                             ctypes.c_float, ctypes.c_int, vp]
+    for name in ("ns_orthogonalize_batched",):
+        getattr(lib, name).argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                       ctypes.POINTER(i64), ctypes.POINTER(i64), i64,
+                                       ctypes.c_int, i32, ctypes.POINTER(ctypes.c_float),
+                                       ctypes.c_float, ctypes.c_int, vp]
     lib.muon_validate_step.argtypes = [ctypes.POINTER(MuonParam), i64, ctypes.POINTER(MuonHParams),
                                        ctypes.c_char_p, ctypes.c_size_t]
     lib.muon_plan_step.argtypes = [ctypes.POINTER(MuonParam), i64, ctypes.POINTER(MuonHParams),

@@ -104,7 +104,7 @@ struct muon_handle {
   hipStream_t side = nullptr;
   hipEvent_t fork = nullptr, join = nullptr;
   bool log = false;                  // MUON_HIP_LOG set (and not "0"): each call's plan on stderr
-  std::string err;
+  char err[512] = {0};               // message of the last failure (fixed: setting it allocates nothing)
 };
 
 namespace {
@@ -129,12 +129,10 @@ struct Msg {
 
 void set_err(muon_handle_t h, const char* fmt, ...) {
   if (!h) return;
-  char tmp[512];
   va_list ap;
   va_start(ap, fmt);
-  vsnprintf(tmp, sizeof tmp, fmt, ap);
+  vsnprintf(h->err, sizeof h->err, fmt, ap);
   va_end(ap);
-  h->err = tmp;
 }
 
 size_t dtype_size(int dt) { return dt == MUON_BF16 ? 2 : 4; }
@@ -455,10 +453,10 @@ muon_status_t validate_step(const muon_param_t* params, int64_t n, const muon_hp
   return MUON_OK;
 }
 
-muon_status_t validate_orth(const void* const* in, void* const* out, const int64_t* rows,
-                            const int64_t* cols, int64_t n, int dtype, int32_t ns_steps,
-                            const float* coeffs, float eps, int prec, std::vector<Item>* items,
-                            Msg& msg, std::vector<Span>* spans = nullptr) {
+// The checks of ns_orthogonalize_batched that concern no single matrix.
+muon_status_t check_orth_args(const void* const* in, void* const* out, const int64_t* rows,
+                              const int64_t* cols, int64_t n, int dtype, int32_t ns_steps,
+                              const float* coeffs, float eps, int prec, Msg& msg) {
   if (n < 0) { msg.set("n must be >= 0"); return MUON_ERR_INVALID_ARGUMENT; }
   if (n > 0 && (!in || !out || !rows || !cols)) { msg.set("NULL array argument"); return MUON_ERR_INVALID_ARGUMENT; }
   if (!dtype_ok(dtype)) { msg.set("unknown dtype"); return MUON_ERR_INVALID_ARGUMENT; }
@@ -468,14 +466,44 @@ muon_status_t validate_orth(const void* const* in, void* const* out, const int64
   if (coeffs)
     for (int i = 0; i < 3 * ns_steps; ++i)
       if (!std::isfinite(coeffs[i])) { msg.set("ns_coeffs[%d] is not finite", i); return MUON_ERR_INVALID_ARGUMENT; }
+  return MUON_OK;
+}
+
+// One matrix of ns_orthogonalize_batched: pointers, extents, alignment.
+muon_status_t check_orth_matrix(const void* in, const void* out, int64_t rows, int64_t cols, size_t es,
+                                int64_t i, Msg& msg) {
+  if (!in || !out) { msg.set("matrix %lld: NULL pointer", (long long)i); return MUON_ERR_INVALID_ARGUMENT; }
+  const muon_status_t st = check_dims(rows, cols, 1, "matrix", i, msg);
+  if (st != MUON_OK) return st;
+  if (reinterpret_cast<uintptr_t>(in) % es || reinterpret_cast<uintptr_t>(out) % es) {
+    msg.set("matrix %lld: pointer not aligned to its element size", (long long)i);
+    return MUON_ERR_INVALID_ARGUMENT;
+  }
+  return MUON_OK;
+}
+
+Item orth_item(const void* in, void* out, int64_t rows, int64_t cols, int dtype, int64_t i) {
+  Item it{};
+  it.flat = i; it.rows = rows; it.cols = cols;
+  it.pdt = dtype; it.gdt = dtype;
+  it.W = nullptr; it.g = in; it.buf = nullptr; it.out = out;
+  set_dense(it);
+  it.cset = 0;
+  it.scale_mode = 1;
+  return it;
+}
+
+muon_status_t validate_orth(const void* const* in, void* const* out, const int64_t* rows,
+                            const int64_t* cols, int64_t n, int dtype, int32_t ns_steps,
+                            const float* coeffs, float eps, int prec, std::vector<Item>* items,
+                            Msg& msg, std::vector<Span>* spans = nullptr) {
+  muon_status_t st = check_orth_args(in, out, rows, cols, n, dtype, ns_steps, coeffs, eps, prec, msg);
+  if (st != MUON_OK) return st;
   std::vector<Run> runs;
   const size_t es = dtype_size(dtype);
-  muon_status_t st;
   for (int64_t i = 0; i < n; ++i) {
-    if (!in[i] || !out[i]) { msg.set("matrix %lld: NULL pointer", (long long)i); return MUON_ERR_INVALID_ARGUMENT; }
-    if ((st = check_dims(rows[i], cols[i], 1, "matrix", i, msg)) != MUON_OK) return st;
+    if ((st = check_orth_matrix(in[i], out[i], rows[i], cols[i], es, i, msg)) != MUON_OK) return st;
     const uintptr_t a = reinterpret_cast<uintptr_t>(in[i]), b = reinterpret_cast<uintptr_t>(out[i]);
-    if (a % es || b % es) { msg.set("matrix %lld: pointer not aligned to its element size", (long long)i); return MUON_ERR_INVALID_ARGUMENT; }
     const uintptr_t bytes = uintptr_t(rows[i]) * uintptr_t(cols[i]) * es;
     if (a == b) {
       runs.push_back({a, bytes, bytes, 1, true});
@@ -487,16 +515,7 @@ muon_status_t validate_orth(const void* const* in, void* const* out, const int64
       spans->push_back({a, a + bytes});
       if (b != a) spans->push_back({b, b + bytes});
     }
-    if (items) {
-      Item it;
-      it.flat = i; it.rows = rows[i]; it.cols = cols[i];
-      it.pdt = dtype; it.gdt = dtype;
-      it.W = nullptr; it.g = in[i]; it.buf = nullptr; it.out = out[i];
-      set_dense(it);
-      it.cset = 0;
-      it.scale_mode = 1;
-      items->push_back(it);
-    }
+    if (items) items->push_back(orth_item(in[i], out[i], rows[i], cols[i], dtype, i));
   }
   if (!runs_disjoint(runs)) { msg.set("an output overlaps another buffer"); return MUON_ERR_INVALID_ARGUMENT; }
   return MUON_OK;
@@ -525,6 +544,30 @@ struct Plan {
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
+// Workspace of a chunk of c.count matrices of padded extent c.S x c.L: two
+// X buffers (and two X^T where kept), A, B, the fp64 norm partials, then r
+// (fp64) and the first step's scale (fp32) per matrix; byte offsets and the
+// total in c.
+void layout_chunk(Chunk& c, bool ns_f32, int K) {
+  const size_t es = ns_f32 ? 4 : 2;
+  const size_t xb = align256(size_t(c.count) * size_t(c.S) * size_t(c.L) * es);
+  const size_t ab = align256(size_t(c.count) * size_t(c.S) * size_t(c.S) * es);
+  const size_t pb = align256(size_t(c.count) * size_t(muon::norm_tiles(c.S, c.L)) * 8);
+  c.keeps_xt = muon::chunk_keeps_xt(c.S, c.L, ns_f32, K);
+  size_t off = 0;
+  c.off_X[0] = off; off += xb;
+  c.off_X[1] = off; off += xb;
+  if (c.keeps_xt) {
+    c.off_XT[0] = off; off += xb;
+    c.off_XT[1] = off; off += xb;
+  }
+  c.off_A = off; off += ab;
+  c.off_B = off; off += ab;
+  c.off_part = off; off += pb;
+  c.off_r = off; off += align256(size_t(c.count) * 12);  // rscale (fp64), then xscale (fp32)
+  c.bytes = off;
+}
+
 // `steps[c]` is the step count of coefficient table c; the work of a
 // bucket is s^2 l per step (at least one, so K = 0 buckets keep their
 // shape order).
@@ -551,7 +594,6 @@ Plan make_plan(const std::vector<Item>& items, int64_t cap, bool ns_f32, const s
     return first_seen[a] < first_seen[b];
   });
   Plan plan;
-  const size_t es = ns_f32 ? 4 : 2;
   for (const Key& k : keys) {
     const auto& idx = buckets[k];
     const int64_t s = std::get<0>(k), l = std::get<1>(k);
@@ -566,23 +608,8 @@ Plan make_plan(const std::vector<Item>& items, int64_t cap, bool ns_f32, const s
       c.first = int64_t(plan.order.size());
       c.count = std::min<int64_t>(per, int64_t(idx.size() - b));
       for (int64_t j = 0; j < c.count; ++j) plan.order.push_back(idx[b + size_t(j)]);
-      const size_t xb = align256(size_t(c.count) * size_t(c.S) * size_t(c.L) * es);
-      const size_t ab = align256(size_t(c.count) * size_t(c.S) * size_t(c.S) * es);
-      const size_t pb = align256(size_t(c.count) * size_t(muon::norm_tiles(c.S, c.L)) * 4);
-      c.keeps_xt = muon::chunk_keeps_xt(c.S, c.L, ns_f32, steps[size_t(c.cset)]);
-      size_t off = 0;
-      c.off_X[0] = off; off += xb;
-      c.off_X[1] = off; off += xb;
-      if (c.keeps_xt) {
-        c.off_XT[0] = off; off += xb;
-        c.off_XT[1] = off; off += xb;
-      }
-      c.off_A = off; off += ab;
-      c.off_B = off; off += ab;
-      c.off_part = off; off += pb;
-      c.off_r = off; off += align256(size_t(c.count) * 8);  // rscale, then xscale
-      c.bytes = off;
-      plan.ws_bytes = std::max(plan.ws_bytes, off);
+      layout_chunk(c, ns_f32, steps[size_t(c.cset)]);
+      plan.ws_bytes = std::max(plan.ws_bytes, c.bytes);
       plan.chunks.push_back(c);
     }
   }
@@ -824,9 +851,9 @@ muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Pla
     b.XT[0] = c.keeps_xt ? ws + c.off_XT[0] : nullptr;
     b.XT[1] = c.keeps_xt ? ws + c.off_XT[1] : nullptr;
     b.A = ws + c.off_A; b.B = ws + c.off_B;
-    b.partials = reinterpret_cast<float*>(ws + c.off_part);
-    b.rscale = reinterpret_cast<float*>(ws + c.off_r);
-    b.xscale = b.rscale + c.count;
+    b.partials = reinterpret_cast<double*>(ws + c.off_part);
+    b.rscale = reinterpret_cast<double*>(ws + c.off_r);
+    b.xscale = reinterpret_cast<float*>(b.rscale + c.count);
     const std::vector<float>& ct = tables[size_t(c.cset)];
     launch_err = muon::run_chunk(g, d_desc + c.first, b, sc, ct.data(), int(ct.size() / 3), cs,
                                  h->profiling ? &h->timer : nullptr);
@@ -892,7 +919,7 @@ muon_status_t validate_adamw(const muon_adamw_param_t* params, int64_t n, const 
 // mapped back to back).  A host pointer, another device's memory, or a view
 // that runs past its allocation into unmapped addresses is an error here
 // instead of a fault in a kernel.
-muon_status_t check_device_spans(muon_handle_t h, const std::vector<Span>& spans) {
+muon_status_t check_device_spans(muon_handle_t h, const Span* spans, size_t n) {
   const auto device_mem = [&](uintptr_t addr) {
     hipPointerAttribute_t a{};
     if (hipPointerGetAttributes(&a, reinterpret_cast<const void*>(addr)) != hipSuccess) {
@@ -901,7 +928,8 @@ muon_status_t check_device_spans(muon_handle_t h, const std::vector<Span>& spans
     }
     return a.isManaged || a.type == hipMemoryTypeManaged || (a.type == hipMemoryTypeDevice && a.device == h->device);
   };
-  for (const Span& s : spans) {
+  for (size_t i = 0; i < n; ++i) {
+    const Span& s = spans[i];
     if (s.hi <= s.lo) continue;
     if (!device_mem(s.lo)) {
       set_err(h, "buffer at %p is not device memory of device %d", reinterpret_cast<void*>(s.lo), h->device);
@@ -920,6 +948,10 @@ muon_status_t check_device_spans(muon_handle_t h, const std::vector<Span>& spans
     }
   }
   return MUON_OK;
+}
+
+muon_status_t check_device_spans(muon_handle_t h, const std::vector<Span>& spans) {
+  return check_device_spans(h, spans.data(), spans.size());
 }
 
 std::vector<float> coefficient_table(int K, const float* coeffs) {
@@ -952,7 +984,7 @@ const char* muon_status_string(muon_status_t s) {
   return "MUON_ERR_UNKNOWN";
 }
 
-const char* muon_last_error(muon_handle_t h) { return h ? h->err.c_str() : "NULL handle"; }
+const char* muon_last_error(muon_handle_t h) { return h ? h->err : "NULL handle"; }
 
 muon_status_t muon_create(muon_handle_t* out, int device) {
   if (!out) return MUON_ERR_INVALID_ARGUMENT;
@@ -1018,7 +1050,7 @@ muon_status_t muon_destroy(muon_handle_t h) {
 muon_status_t muon_set_streams(muon_handle_t h, int streams) {
   if (!h || (streams != 1 && streams != 2)) return MUON_ERR_INVALID_ARGUMENT;
   if (streams == 2 && !h->side) {
-    h->err = "the second stream could not be created";
+    set_err(h, "the second stream could not be created");
     return MUON_ERR_DEVICE;
   }
   h->nstreams = streams;
@@ -1106,14 +1138,14 @@ muon_status_t muon_plan_step(const muon_param_t* params, int64_t n, const muon_h
 muon_status_t muon_step(muon_handle_t h, const muon_param_t* params, int64_t n,
                         const muon_hparams_t* hp, void* stream) {
   if (!h) return MUON_ERR_INVALID_ARGUMENT;
-  h->err.clear();
+  h->err[0] = '\0';
   char buf[256] = {0};
   Msg m{buf, sizeof buf};
   std::vector<Item> items;
   CoeffTables tables;
   std::vector<Span> spans;
   muon_status_t st = validate_step(params, n, hp, &items, &tables, m, &spans);
-  if (st != MUON_OK) { h->err = buf; return st; }
+  if (st != MUON_OK) { set_err(h, "%s", buf); return st; }
   if (items.empty()) return MUON_OK;
   if ((st = check_device_spans(h, spans)) != MUON_OK) return st;
   const bool f32 = hp->ns_precision == MUON_NS_F32;
@@ -1132,12 +1164,12 @@ muon_status_t muon_step(muon_handle_t h, const muon_param_t* params, int64_t n,
 muon_status_t muon_adamw_step(muon_handle_t h, const muon_adamw_param_t* params, int64_t n,
                               const muon_adamw_hparams_t* hp, void* stream_) {
   if (!h) return MUON_ERR_INVALID_ARGUMENT;
-  h->err.clear();
+  h->err[0] = '\0';
   char buf[256] = {0};
   Msg m{buf, sizeof buf};
   std::vector<Span> spans;
   muon_status_t st = validate_adamw(params, n, hp, m, &spans);
-  if (st != MUON_OK) { h->err = buf; return st; }
+  if (st != MUON_OK) { set_err(h, "%s", buf); return st; }
   if ((st = check_device_spans(h, spans)) != MUON_OK) return st;
   const hipStream_t stream = static_cast<hipStream_t>(stream_);
   // tensors grouped by dtype pair; workgroup ranges per group
@@ -1199,13 +1231,13 @@ muon_status_t ns_orthogonalize_batched(muon_handle_t h, const void* const* in, v
                                        muon_dtype_t dtype, int32_t ns_steps, const float* ns_coeffs,
                                        float eps, muon_ns_precision_t prec, void* stream) {
   if (!h) return MUON_ERR_INVALID_ARGUMENT;
-  h->err.clear();
+  h->err[0] = '\0';
   char buf[256] = {0};
   Msg m{buf, sizeof buf};
   std::vector<Item> items;
   std::vector<Span> spans;
   muon_status_t st = validate_orth(in, out, rows, cols, n, dtype, ns_steps, ns_coeffs, eps, prec, &items, m, &spans);
-  if (st != MUON_OK) { h->err = buf; return st; }
+  if (st != MUON_OK) { set_err(h, "%s", buf); return st; }
   if (items.empty()) return MUON_OK;
   if ((st = check_device_spans(h, spans)) != MUON_OK) return st;
   const bool f32 = prec == MUON_NS_F32;
@@ -1217,5 +1249,6 @@ muon_status_t ns_orthogonalize_batched(muon_handle_t h, const void* const* in, v
   sc.final_kind = 1;
   return execute(h, items, plan, 0.0, 0.0, sc, f32, tables, static_cast<hipStream_t>(stream));
 }
+
 
 }  // extern "C"

@@ -70,8 +70,8 @@ struct ChunkBuffers {
   void* XT[2];          // L x S, row stride S
   void* A;              // S x S
   void* B;              // S x S
-  float* partials;      // nmat x norm_tiles(S, L)
-  float* rscale;        // nmat: r = 1 / (||u||_F + eps)
+  double* partials;     // nmat x norm_tiles(S, L), sums of u^2 in fp64
+  double* rscale;       // nmat: r = 1 / (||u||_F + eps), fp64
   float* xscale;        // nmat: the scale the first Newton-Schulz step applies
                         // to X: r, or 1 where X already holds r*u
 };

@@ -102,15 +102,32 @@ __device__ __forceinline__ void store8(T* base, int64_t i, const float in[8]) {
 }
 
 // Fixed-order sum over a 256-thread block: butterfly within each 64-lane
-// wavefront, then the four wave sums in wave order.  Deterministic.
-__device__ __forceinline__ float block_sum_256(float v, float* red4) {
+// wavefront, then the four wave sums in wave order.  Deterministic.  In fp64:
+// the sums of u^2 stay finite for every finite u (|u| < 2^128 and at most
+// 2^62 elements), where binary32 would overflow once |u| passes 2^64.
+__device__ __forceinline__ double block_sum_256(double v, double* red4) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
   const int wave = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) red4[wave] = v;
   __syncthreads();
-  float s = ((red4[0] + red4[1]) + red4[2]) + red4[3];
-  return s;
+  return ((red4[0] + red4[1]) + red4[2]) + red4[3];
+}
+
+// The factor r = 1 / (||u|| + eps) as two binary32 factors whose product is r
+// (rounded once), each a normal number: r itself when it is one, else a power
+// of two 2^-64 or 2^64 times the rest, for norms beyond 2^126 or below 2^-126.
+__device__ __forceinline__ void split_scale(double r, float& s1, float& s2) {
+  if (r < 0x1p-126 && r > 0.0) {
+    s1 = 0x1p-64f;
+    s2 = static_cast<float>(r * 0x1p64);
+  } else if (r > 0x1p126) {
+    s1 = 0x1p64f;
+    s2 = static_cast<float>(r * 0x1p-64);
+  } else {
+    s1 = 1.0f;
+    s2 = static_cast<float>(r);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -200,15 +217,15 @@ __device__ __forceinline__ void write_transposed(const XT* tile, const TileDst<X
 
 // One tile of the prologue (UPDATE_MOM: advance the momentum and write it
 // back; otherwise the momentum has been advanced already).  Returns this
-// thread's sum of u^2.  out = scale * u.
+// thread's sum of u^2 (fp64).  out = (u * s1) * s2.
 template <typename GT, typename XT, bool MOM, bool UPDATE_MOM, bool WIDE>
-__device__ __forceinline__ float prologue_tile(const MatDesc& md, const StepScalars& sc, const TileDst<XT>& t,
-                                               float scale, XT* tile) {
+__device__ __forceinline__ double prologue_tile(const MatDesc& md, const StepScalars& sc, const TileDst<XT>& t,
+                                                float s1, float s2, XT* tile) {
   constexpr int LDT = TileStage<XT>::LDT;
   constexpr int CPR = WIDE ? 16 : 8;              // 8-element chunks per tile row
   const GT* __restrict__ g = static_cast<const GT*>(md.g);
   const float beta = sc.beta, omb = sc.one_minus_beta;
-  float acc = 0.f;
+  double acc = 0.0;
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
     const int c = threadIdx.x + 256 * k;          // chunk: row c / CPR, columns 8 (c % CPR) ..
@@ -234,8 +251,8 @@ __device__ __forceinline__ float prologue_tile(const MatDesc& md, const StepScal
       }
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
-        acc = fmaf(v[q], v[q], acc);
-        v[q] *= scale;
+        acc = fma(static_cast<double>(v[q]), static_cast<double>(v[q]), acc);
+        v[q] = (v[q] * s1) * s2;
       }
     } else {  // padding stays exactly zero, whatever the scale
 #pragma unroll
@@ -254,8 +271,8 @@ __device__ __forceinline__ float prologue_tile(const MatDesc& md, const StepScal
           } else {
             v[q] = gv;
           }
-          acc = fmaf(v[q], v[q], acc);
-          v[q] *= scale;
+          acc = fma(static_cast<double>(v[q]), static_cast<double>(v[q]), acc);
+          v[q] = (v[q] * s1) * s2;
         }
       }
     }
@@ -271,16 +288,16 @@ __device__ __forceinline__ float prologue_tile(const MatDesc& md, const StepScal
 template <typename GT, typename XT, bool MOM>
 __global__ __launch_bounds__(256) void k_prologue(const MatDesc* __restrict__ desc, StepScalars sc, ChunkGeom cg,
                                                   XT* __restrict__ X, XT* __restrict__ XTb,
-                                                  float* __restrict__ partials) {
+                                                  double* __restrict__ partials) {
   __shared__ XT tile[64 * TileStage<XT>::LDT];
-  __shared__ float red4[4];
+  __shared__ double red4[4];
   const int m = blockIdx.z;
   const MatDesc md = desc[m];
   bool wide;
   const TileDst<XT> t = tile_of(md, cg, m, blockIdx.y * gridDim.x + blockIdx.x, X, XTb, wide);
-  const float acc = wide ? prologue_tile<GT, XT, MOM, true, true>(md, sc, t, 1.f, tile)
-                         : prologue_tile<GT, XT, MOM, true, false>(md, sc, t, 1.f, tile);
-  const float s = block_sum_256(acc, red4);  // (its barrier also publishes the LDS tile)
+  const double acc = wide ? prologue_tile<GT, XT, MOM, true, true>(md, sc, t, 1.f, 1.f, tile)
+                          : prologue_tile<GT, XT, MOM, true, false>(md, sc, t, 1.f, 1.f, tile);
+  const double s = block_sum_256(acc, red4);  // (its barrier also publishes the LDS tile)
   if (threadIdx.x == 0)
     partials[static_cast<int64_t>(m) * (gridDim.x * gridDim.y) + blockIdx.y * gridDim.x + blockIdx.x] = s;
   if (!t.Tb) return;  // uniform over the block
@@ -288,18 +305,18 @@ __global__ __launch_bounds__(256) void k_prologue(const MatDesc* __restrict__ de
   write_transposed(tile, t);
 }
 
-// r = 1 / (sqrt(sum of partials) + eps), one workgroup per matrix, and the
-// scale the first products apply: r itself while X~ X~^T stays well inside
-// the fp32 range (||u|| between 2^-40 and 2^40), else 1 (k_rescale then
-// writes r*u into X instead).  1024 threads each sum every 1024th partial
-// into four accumulators (independent loads in flight; an 8192 x 28672
-// matrix has 57344 partials), combined in a fixed order.
-__global__ __launch_bounds__(1024) void k_finalize(const float* __restrict__ partials, int nparts, float eps,
-                                                   float* __restrict__ rscale, float* __restrict__ xscale) {
-  __shared__ float red16[16];
+// r = 1 / (sqrt(sum of partials) + eps), one workgroup per matrix, in fp64,
+// and the scale the first products apply: r itself while X~ X~^T stays well
+// inside the fp32 range (||u|| between 2^-40 and 2^40), else 1 (k_rescale
+// then writes r*u into X instead).  1024 threads each sum every 1024th
+// partial into four accumulators (independent loads in flight; an 8192 x
+// 28672 matrix has 57344 partials), combined in a fixed order.
+__global__ __launch_bounds__(1024) void k_finalize(const double* __restrict__ partials, int nparts, float eps,
+                                                   double* __restrict__ rscale, float* __restrict__ xscale) {
+  __shared__ double red16[16];
   const int m = blockIdx.x;
-  const float* p = partials + static_cast<int64_t>(m) * nparts;
-  float a[4] = {0.f, 0.f, 0.f, 0.f};
+  const double* p = partials + static_cast<int64_t>(m) * nparts;
+  double a[4] = {0.0, 0.0, 0.0, 0.0};
   int i = threadIdx.x;
   for (; i + 3 * 1024 < nparts; i += 4 * 1024) {
 #pragma unroll
@@ -308,18 +325,18 @@ __global__ __launch_bounds__(1024) void k_finalize(const float* __restrict__ par
   if (i < nparts) a[0] += p[i];
   if (i + 1024 < nparts) a[1] += p[i + 1024];
   if (i + 2048 < nparts) a[2] += p[i + 2048];
-  float v = (a[0] + a[1]) + (a[2] + a[3]);
+  double v = (a[0] + a[1]) + (a[2] + a[3]);
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
   if ((threadIdx.x & 63) == 0) red16[threadIdx.x >> 6] = v;
   __syncthreads();
-  float s = 0.f;
+  double s = 0.0;
 #pragma unroll
   for (int w = 0; w < 16; ++w) s += red16[w];
   if (threadIdx.x == 0) {
-    const float r = 1.0f / (sqrtf(s) + eps);
+    const double r = 1.0 / (sqrt(s) + static_cast<double>(eps));
     rscale[m] = r;
-    xscale[m] = (r >= 0x1p-40f && r <= 0x1p40f) ? r : 1.0f;  // NaN fails both tests
+    xscale[m] = (r >= 0x1p-40 && r <= 0x1p40) ? static_cast<float>(r) : 1.0f;  // NaN fails both tests
   }
 }
 
@@ -328,20 +345,22 @@ __global__ __launch_bounds__(1024) void k_finalize(const float* __restrict__ par
 // matrix's workgroups return at once.  The momentum is already advanced.
 // grid = (workgroups per matrix, matrices); each loops over its tiles.
 template <typename GT, typename XT, bool MOM>
-__global__ __launch_bounds__(256) void k_rescale(const MatDesc* __restrict__ desc, const float* __restrict__ rscale,
+__global__ __launch_bounds__(256) void k_rescale(const MatDesc* __restrict__ desc, const double* __restrict__ rscale,
                                                  const float* __restrict__ xscale, StepScalars sc, ChunkGeom cg,
                                                  XT* __restrict__ X, XT* __restrict__ XTb) {
   __shared__ XT tile[64 * TileStage<XT>::LDT];
   const int m = blockIdx.y;
-  const float r = rscale[m];
-  if (r == xscale[m]) return;  // uniform over the block
+  const double r = rscale[m];
+  if (xscale[m] != 1.0f || r == 1.0) return;  // uniform over the block
+  float s1, s2;
+  split_scale(r, s1, s2);
   const MatDesc md = desc[m];
   const int ntiles = (cg.L / 64) * (cg.S / 64);
   for (int tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
     bool wide;
     const TileDst<XT> t = tile_of(md, cg, m, tt, X, XTb, wide);
-    if (wide) (void)prologue_tile<GT, XT, MOM, false, true>(md, sc, t, r, tile);
-    else (void)prologue_tile<GT, XT, MOM, false, false>(md, sc, t, r, tile);
+    if (wide) (void)prologue_tile<GT, XT, MOM, false, true>(md, sc, t, s1, s2, tile);
+    else (void)prologue_tile<GT, XT, MOM, false, false>(md, sc, t, s1, s2, tile);
     if (t.Tb) {  // uniform over the block
       __syncthreads();
       write_transposed(tile, t);
@@ -1603,14 +1622,14 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
       hipLaunchKernelGGL((k_prologue<GT, XT, false>), grid, dim3(256), 0, st, d_desc, sc, cg, x0, xt0, wb.partials);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // reads g (and the momentum), writes the momentum and X~ (and X~^T)
-    tm.done(0, 0, nm * ne * (gsz + (sc.momentum ? 8.0 : 0.0) + (qtr ? 1.0 : 2.0) * xsz) + nm * nparts * 4.0);
+    tm.done(0, 0, nm * ne * (gsz + (sc.momentum ? 8.0 : 0.0) + (qtr ? 1.0 : 2.0) * xsz) + nm * nparts * 8.0);
   }
   {
     Timed tm(timer, KK_FINALIZE, st);
     hipLaunchKernelGGL(k_finalize, dim3(nmat), dim3(1024), 0, st, wb.partials, nparts, sc.eps, wb.rscale,
                        wb.xscale);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    tm.done(0, 0, nm * nparts * 4.0 + nm * 8.0);
+    tm.done(0, 0, nm * nparts * 8.0 + nm * 12.0);
   }
   {
     Timed tm(timer, KK_NORMALIZE, st);
@@ -1622,7 +1641,7 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
       hipLaunchKernelGGL((k_rescale<GT, XT, false>), grid, dim3(256), 0, st, d_desc, wb.rscale, wb.xscale, sc,
                          cg, x0, xt0);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    tm.done(0, 0, nm * 8.0);  // nothing else unless a norm is out of range
+    tm.done(0, 0, nm * 12.0);  // nothing else unless a norm is out of range
   }
 
   if (K == 0) {

@@ -5,7 +5,11 @@
 For every matrix of a workload the fp64 oracle (oracle/muon_ref.py) runs the
 whole Muon step (or, for workload 4, the standalone orthogonalisation) on the
 seeded inputs of paper_2609_21594_amd/synth.py, one matrix at a time, and the
-values at NSAMP seeded positions are stored in tests/golden/workload<k>_samples.npz:
+values at seeded positions are stored in tests/golden/workload<k>_samples.npz.
+The positions are stratified over the 256 x 256 tiles of the matrix (edge
+tiles clipped): every tile holds at least TILE_SAMPLES of them, and at least
+MIN_SAMPLES fall in every matrix, so an error confined to any one output tile
+of the kernels is sampled.
 
   dW     W_final - W_initial at the sampled positions (float32)   [Muon steps]
   buf    final momentum at the sampled positions (float32)        [Muon steps]
@@ -34,15 +38,27 @@ sys.path.insert(0, ROOT)
 from oracle import muon_ref as ref  # noqa: E402
 from paper_2609_21594_amd import synth  # noqa: E402
 
-NSAMP = {2: 1024, 3: 512, 4: 256, 5: 512}
-SAMPLE_STREAM = 777
+TILE = 256
+TILE_SAMPLES = 2
+MIN_SAMPLES = 256
+SAMPLE_STREAM = 778
 
 
-def sample_indices(workload: int, index: int, numel: int, n: int) -> np.ndarray:
-    """Seeded flat positions (with replacement, sorted) inside one matrix."""
+def sample_indices(workload: int, index: int, rows: int, cols: int) -> np.ndarray:
+    """Seeded flat positions inside one rows x cols matrix (row-major), the
+    same number in each 256 x 256 tile (at least TILE_SAMPLES, and enough for
+    MIN_SAMPLES in all), uniform inside the tile; sorted."""
     rng = np.random.Generator(np.random.PCG64(
         np.random.SeedSequence([synth.ROOT_SEED, workload, SAMPLE_STREAM, index])))
-    return np.sort(rng.integers(0, numel, size=n))
+    tr, tc = -(-rows // TILE), -(-cols // TILE)
+    per = max(TILE_SAMPLES, -(-MIN_SAMPLES // (tr * tc)))
+    r0 = np.repeat(np.arange(tr) * TILE, tc * per)
+    c0 = np.tile(np.repeat(np.arange(tc) * TILE, per), tr)
+    hr = np.minimum(TILE, rows - r0)
+    hc = np.minimum(TILE, cols - c0)
+    r = r0 + (rng.random(r0.size) * hr).astype(np.int64)
+    c = c0 + (rng.random(c0.size) * hc).astype(np.int64)
+    return np.sort(r * cols + c)
 
 
 def decode(x, dtype):
@@ -55,8 +71,7 @@ def golden_path(workload: int) -> str:
 
 def run_matrix(wl: synth.Workload, i: int):
     spec = wl.matrices[i]
-    ns = NSAMP[wl.index]
-    idx = sample_indices(wl.index, i, spec.rows * spec.cols, ns)
+    idx = sample_indices(wl.index, i, spec.rows, spec.cols)
     hp = ref.MuonHParams(lr=wl.lr, beta=wl.beta, weight_decay=wl.weight_decay,
                          ns_steps=wl.ns_steps, nesterov=wl.nesterov)
     if wl.orthogonalize_only:
@@ -87,16 +102,21 @@ def make(workload: int):
     wl = synth.WORKLOADS[workload]
     n = len(wl.matrices)
     cols = {k: [] for k in ("O", "dW", "buf", "rho")}
+    counts = []
     t0 = time.time()
     for i in range(n):
         res = run_matrix(wl, i)
         for k in cols:
             cols[k].append(res[k])
+        counts.append(len(res["O"]))
         print(f"workload {workload}: matrix {i + 1}/{n} {wl.matrices[i].rows}x{wl.matrices[i].cols} "
               f"done at {time.time() - t0:.0f}s", flush=True)
-    np.savez_compressed(golden_path(workload), O=np.stack(cols["O"]), dW=np.stack(cols["dW"]),
-                        buf=np.stack(cols["buf"]), rho=np.array(cols["rho"]),
-                        nsamp=NSAMP[workload], workload=workload)
+    # matrices hold different sample counts: stored concatenated, with offsets
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int64)
+    np.savez_compressed(golden_path(workload), O=np.concatenate(cols["O"]),
+                        dW=np.concatenate(cols["dW"]), buf=np.concatenate(cols["buf"]),
+                        rho=np.array(cols["rho"]), offsets=offsets, workload=workload,
+                        sample_stream=SAMPLE_STREAM)
     print(f"wrote {golden_path(workload)} in {time.time() - t0:.0f}s", flush=True)
 
 

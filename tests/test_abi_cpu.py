@@ -428,12 +428,14 @@ def test_plan_keeps_no_transpose_where_the_tile_kernel_reads_x(lib):
         return total
     s, l = 512, 1280
     xb, ab = s * l * 2, s * s * 2
-    tail = 768 + 256  # norm partials (8 x 20 (or 22) floats); 1/(norm+eps) and the first scale
+    # norm partials (8 x 20, or 8 x 22, doubles, in 256-byte units); then
+    # 1/(norm+eps) (double) and the first scale (float)
+    tail = 1280 + 256
     assert ws((s, l)) == 2 * xb + 2 * ab + tail
     assert ws((l, s)) == 2 * xb + 2 * ab + tail  # transposed to 512 x 1280 first
     assert ws((s, l), ns_steps=0) == 4 * xb + 2 * ab + tail
     assert ws((s, l), ns_precision="f32") == 8 * xb + 4 * ab + tail
-    assert ws((s, 1300)) == 4 * (s * 1408 * 2) + 2 * ab + tail
+    assert ws((s, 1300)) == 4 * (s * 1408 * 2) + 2 * ab + 1536 + 256
 
 
 def test_plan_separates_dtypes(lib):

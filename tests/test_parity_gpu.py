@@ -53,8 +53,9 @@ def test_orthogonalize_matches_oracle(muon, dtype, prec):
     G, outs = run_orth(muon, SHAPES, dtype, prec, key=1)
     for s, g, o in zip(SHAPES, G, outs):
         want = ref.orthogonalize(decode(g, dtype), 5)
-        err, rho = o_gate(to_host(o), want, dtype)
-        assert err <= tol_for(prec, s) + rho, (s, err, rho)
+        err, gate = o_gate(to_host(o), want, dtype, prec, G=decode(g, dtype))
+        print(f"orthogonalize {dtype}/{prec} {s}: O err {err:.3e} (gate {gate:.2e})", flush=True)
+        assert err <= gate, (s, err, gate)
 
 
 @pytest.mark.parametrize("nesterov", [True, False])
@@ -77,7 +78,9 @@ def test_muon_step_matches_oracle(muon, pdt, gdt, prec, nesterov):
         W0 = decode(W, pdt)
         r = ref.muon_step_matrix(W0, decode(g, gdt), np.asarray(b, np.float64), hp)
         err, rho = w_gate(to_host(w_dev), r.W_new, W0, pdt)
-        assert err <= tol_for(prec, s) + rho, (s, err, rho)
+        gate = tol_for(prec, s, G=ref.momentum_update(decode(g, gdt), b, hp.beta, nesterov)[1])
+        print(f"step {pdt}/{gdt}/{prec} {s}: W err {err:.3e} (gate {gate:.2e} + rho {rho:.1e})", flush=True)
+        assert err <= gate + rho, (s, err, gate, rho)
         assert rel(to_host(b_dev), r.buf_new) <= MOMENTUM_TOL, s
 
 
@@ -115,8 +118,8 @@ def test_upper_tile_path_orthogonalize_matches_oracle(muon):
     G, outs = run_orth(muon, UPPER_SHAPES, "bf16", "bf16", key=21)
     for s, g, o in zip(UPPER_SHAPES, G, outs):
         want = ref.orthogonalize(decode(g, "bf16"), 5)
-        err, rho = o_gate(to_host(o), want, "bf16")
-        assert err <= tol_for("bf16", s) + rho, (s, err, rho)
+        err, gate = o_gate(to_host(o), want, "bf16", "bf16")
+        assert err <= gate, (s, err, gate)
 
 
 def test_upper_tile_path_zero_c_steps_match_oracle(muon):
@@ -127,9 +130,9 @@ def test_upper_tile_path_zero_c_steps_match_oracle(muon):
     G, outs = run_orth(muon, UPPER_SHAPES, "bf16", "bf16", ns_steps=len(coeffs), coeffs=coeffs, key=22)
     for s, g, o in zip(UPPER_SHAPES, G, outs):
         want = ref.orthogonalize(decode(g, "bf16"), len(coeffs), coeffs)
-        err, rho = o_gate(to_host(o), want, "bf16")
-        print(f"zero-c schedule {s}: err {err:.3e} (rho {rho:.1e})", flush=True)
-        assert err <= tol_for("bf16", s) + rho, (s, err, rho)
+        err, gate = o_gate(to_host(o), want, "bf16", "bf16", len(coeffs), coeffs)
+        print(f"zero-c schedule {s}: err {err:.3e} (gate {gate:.1e})", flush=True)
+        assert err <= gate, (s, err, gate)
 
 
 def test_rows_past_the_tile_kernel_offsets(muon):
@@ -225,9 +228,9 @@ def test_one_and_two_steps_match_oracle(muon, steps, prec):
     G, outs = run_orth(muon, shapes, "bf16", prec, ns_steps=steps, key=25 + steps)
     for s, g, o in zip(shapes, G, outs):
         want = ref.orthogonalize(decode(g, "bf16"), steps)
-        err, rho = o_gate(to_host(o), want, "bf16")
-        print(f"K={steps} {prec} orthogonalize {s}: O err {err:.3e} (rho {rho:.1e})", flush=True)
-        assert err <= tol_for(prec, s) + rho, (s, err, rho)
+        err, gate = o_gate(to_host(o), want, "bf16", prec, steps)
+        print(f"K={steps} {prec} orthogonalize {s}: O err {err:.3e} (gate {gate:.1e})", flush=True)
+        assert err <= gate, (s, err, gate)
 
 
 def test_zero_steps_returns_normalised_input(muon):
@@ -287,20 +290,25 @@ def test_norms_outside_the_folded_range(muon, prec):
     # The first Newton-Schulz step applies r = 1/(||u|| + eps) to products of
     # u itself while r lies in [2^-40, 2^40]; beyond that X0 = r*u is written
     # out first.  Power-of-two scales keep the inputs exact in both dtypes:
-    # ||u|| ~ 2^-44 and 2^56 here.  eps = 0 makes the result scale-invariant.
+    # ||u|| ~ 2^-44, 2^56, 2^76 (u^2 past the binary32 range: the norm sums
+    # run in fp64) and 2^127 (r below the normal binary32 range: applied as
+    # two factors).  eps = 0 makes the result scale-invariant.
     import torch
     base = gen((48, 80), 1.0, "f32", 28, 0)
+    base /= np.float32(np.abs(base).max())   # |entries| <= 1, so 2^126 x base stays finite
     if prec == "bf16":
         base = decode(synth.f32_to_bf16_bits(base), "bf16").astype(np.float32)
     want = ref.orthogonalize(base.astype(np.float64), 5, eps=0.0)
-    scales = (1.0, 2.0 ** -50, 2.0 ** 50)
+    scales = (1.0, 2.0 ** -50, 2.0 ** 50, 2.0 ** 70, 2.0 ** 126)
     dt = torch.float32 if prec == "f32" else torch.bfloat16
     ins = [torch.from_numpy(base * np.float32(sc)).to(dt).cuda() for sc in scales]
     outs = [torch.empty_like(t) for t in ins]
     muon.orthogonalize(ins, outs, ns_precision=prec, eps=0.0)
     torch.cuda.synchronize()
     for sc, o in zip(scales, outs):
-        assert rel(to_host(o), want) <= TOL[prec], sc
+        err = rel(to_host(o), want)
+        print(f"norm scale 2^{int(np.log2(sc))} {prec}: O err {err:.3e}", flush=True)
+        assert err <= TOL[prec], sc
     # the same through muon_step: zero momentum, beta = 0, no decay, lr = 1
     # and no rescale, so W' = W - O
     Ws = [torch.zeros(48, 80, dtype=dt, device="cuda") for _ in scales]
@@ -445,8 +453,8 @@ def test_in_place_orthogonalize(muon):
     t = to_dev(g, "bf16")
     muon.orthogonalize([t], [t])
     torch.cuda.synchronize()
-    err, rho = o_gate(to_host(t), ref.orthogonalize(decode(g, "bf16"), 5), "bf16")
-    assert err <= TOL["bf16"] + rho
+    err, gate = o_gate(to_host(t), ref.orthogonalize(decode(g, "bf16"), 5), "bf16", "bf16")
+    assert err <= gate, (err, gate)
 
 
 def test_non_default_stream(muon):

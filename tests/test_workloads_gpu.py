@@ -5,8 +5,12 @@ configuration the benchmark times (one call over every matrix, default
 Workload 1 (one 256x128 fp32 matrix) is compared with the oracle run here.
 Workloads 2-5 are compared at seeded sample positions with oracle values that
 tests/golden/make_golden.py computed (fp64, whole matrices) from the same
-seeded inputs; the relative error over the samples estimates the relative
-Frobenius error per matrix.
+seeded inputs; the positions are stratified over the 256 x 256 output tiles
+(at least two in each), and the relative error over the samples estimates the
+relative Frobenius error per matrix.  One call over 7B-like shapes is also
+compared element by element with the oracle run here (every tile, both tile
+bands of a 4096 short side, several persistent rounds, both orientations of
+the fused last-step update).
 """
 import os
 
@@ -15,8 +19,8 @@ import pytest
 
 from oracle import muon_ref as ref
 from paper_2609_21594_amd import synth
-from tests.golden.make_golden import NSAMP, golden_path, sample_indices
-from tests.gpu_util import MOMENTUM_TOL, TOL, decode, o_gate, rel, require_gpu, to_dev, to_host
+from tests.golden.make_golden import golden_path, sample_indices
+from tests.gpu_util import MOMENTUM_TOL, TOL, decode, rel, require_gpu, to_dev, to_host, w_gate
 
 pytestmark = pytest.mark.gpu
 
@@ -67,12 +71,13 @@ def test_workload_muon_step_sampled(muon, workload):
     wl = synth.WORKLOADS[workload]
     gold = _load_golden(workload)
     n = len(wl.matrices)
-    ns = NSAMP[workload]
+    off = gold["offsets"]
     W, G, B, W0s, idxs = [], [], [], [], []
     for lo in range(0, n, 8):  # bounded host memory
         for m in synth.make_workload(wl, 0, indices=range(lo, min(n, lo + 8))):
             i = len(W)
-            idx = sample_indices(workload, i, m.spec.rows * m.spec.cols, ns)
+            idx = sample_indices(workload, i, m.spec.rows, m.spec.cols)
+            assert idx.size == off[i + 1] - off[i], "stored samples do not match the sampler"
             idxs.append(idx)
             W0s.append(decode(m.W.reshape(-1)[idx], wl.param_dtype))
             W.append(to_dev(m.W, wl.param_dtype))
@@ -89,9 +94,10 @@ def test_workload_muon_step_sampled(muon, workload):
         print(f"workload {workload}: step {t + 1}/{wl.steps} done", flush=True)
     worst_w = worst_b = 0.0
     for i in range(n):
+        sl = slice(off[i], off[i + 1])
         dW = _gather(W[i], idxs[i]) - W0s[i]
-        err = rel(dW, gold["dW"][i].astype(np.float64))
-        berr = rel(_gather(B[i], idxs[i]), gold["buf"][i].astype(np.float64))
+        err = rel(dW, gold["dW"][sl].astype(np.float64))
+        berr = rel(_gather(B[i], idxs[i]), gold["buf"][sl].astype(np.float64))
         worst_w, worst_b = max(worst_w, err), max(worst_b, berr)
         assert err <= TOL[wl.ns_precision] + gold["rho"][i], (i, err, gold["rho"][i])
         assert berr <= 1e-5, (i, berr)  # float32 storage of the expected samples
@@ -107,10 +113,55 @@ def test_workload4_orthogonalize_sampled(muon):
     muon.orthogonalize(ins, outs, ns_steps=wl.ns_steps, ns_precision="bf16")
     torch.cuda.synchronize()
     worst = 0.0
+    off = gold["offsets"]
     for i, o in enumerate(outs):
         spec = wl.matrices[i]
-        idx = sample_indices(4, i, spec.rows * spec.cols, NSAMP[4])
-        err, rho = o_gate(_gather(o, idx), gold["O"][i].astype(np.float64), "bf16")
+        idx = sample_indices(4, i, spec.rows, spec.cols)
+        assert idx.size == off[i + 1] - off[i], "stored samples do not match the sampler"
+        err = rel(_gather(o, idx), gold["O"][off[i]:off[i + 1]].astype(np.float64))
         worst = max(worst, err)
-        assert err <= TOL["bf16"] + rho, (i, spec, err, rho)
+        assert err <= TOL["bf16"], (i, spec, err)
     print(f"workload 4: worst sampled O err {worst:.3e}", flush=True)
+
+
+def test_7b_shapes_element_by_element(muon):
+    # One call over 4096x4096 (twice), 11008x4096 and 4096x11008, seeded as
+    # the 7B-like share: chunks (4096, 4096) x 2 and (4096, 11008) x 2, whose
+    # Gram launches hold 272 upper tiles each (more than one persistent round)
+    # over two bands of 8 tile-rows, and whose last step updates W both in
+    # its own layout and transposed.  Every element against the oracle run
+    # here on the same inputs (about 30 s of fp64 on 16 cores).
+    import torch
+    wl = synth.WORKLOADS[3]
+    picks = [0, 1, 4, 6]     # l0.q, l0.k, l0.gate (11008 x 4096), l0.down (4096 x 11008)
+    mats = synth.make_workload(wl, 0, indices=picks)
+    assert [(m.spec.rows, m.spec.cols) for m in mats] == [(4096, 4096), (4096, 4096),
+                                                          (11008, 4096), (4096, 11008)]
+    W = [to_dev(m.W, "bf16") for m in mats]
+    G = [to_dev(m.g, "bf16") for m in mats]
+    B = [to_dev(m.buf, "f32") for m in mats]
+    muon.step(W, G, B, lr=wl.lr, beta=wl.beta, weight_decay=0.1, ns_steps=wl.ns_steps,
+              nesterov=wl.nesterov, ns_precision="bf16")
+    torch.cuda.synchronize()
+    hp = ref.MuonHParams(lr=wl.lr, beta=wl.beta, weight_decay=0.1, ns_steps=wl.ns_steps,
+                         nesterov=wl.nesterov)
+    for m, w_dev, b_dev in zip(mats, W, B):
+        print(f"7B shapes: oracle on {m.spec.name} {m.spec.rows}x{m.spec.cols}", flush=True)
+        W0 = decode(m.W, "bf16")
+        r = ref.muon_step_matrix(W0, decode(m.g, "bf16"), np.asarray(m.buf, np.float64), hp)
+        Wg = to_host(w_dev)
+        err, rho = w_gate(Wg, r.W_new, W0, "bf16")
+        berr = rel(to_host(b_dev), r.buf_new)
+        # the worst 256 x 256 tile, so that one bad tile cannot hide in the norm
+        d = (Wg - r.W_new) ** 2
+        u = (r.W_new - W0) ** 2
+        tr, tc = -(-m.spec.rows // 256), -(-m.spec.cols // 256)
+        pad = ((0, tr * 256 - m.spec.rows), (0, tc * 256 - m.spec.cols))
+        dt = np.pad(d, pad).reshape(tr, 256, tc, 256).sum(axis=(1, 3))
+        ut = np.pad(u, pad).reshape(tr, 256, tc, 256).sum(axis=(1, 3))
+        tile_worst = float(np.sqrt((dt / ut).max()))
+        print(f"7B shapes {m.spec.rows}x{m.spec.cols}: W err {err:.3e} (rho {rho:.1e}), "
+              f"worst tile {tile_worst:.3e}, momentum {berr:.1e}", flush=True)
+        assert err <= TOL["bf16"] + rho, (m.spec, err, rho)
+        assert tile_worst <= 2 * (TOL["bf16"] + rho), (m.spec, tile_worst)
+        assert berr <= MOMENTUM_TOL
