@@ -206,6 +206,30 @@ muon_status_t ns_orthogonalize_batched(muon_handle_t h, const void* const* in,
                                        muon_ns_precision_t prec, void* stream);
 
 /*
+ * ns_orthogonalize_batched without any allocation, for callers that cannot
+ * allocate: code under HIP stream capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  Same arguments, checks and results (bit for bit)
+ * as ns_orthogonalize_batched.  The workspace and the descriptor table live
+ * in a fixed 64 MiB array of device memory that the library holds on each
+ * device it runs on until the process ends (its address is resolved by
+ * muon_create); the call makes no hipMalloc, hipFree, pinned-host or other
+ * allocating call, and queues no host-to-device copy (the descriptors travel
+ * as kernel arguments).
+ * Limits: at most 64 matrices per call, and each chunk of same-shape
+ * matrices must fit the array: a single matrix whose workspace exceeds it
+ * (about 2048 x 5632 in bf16) returns MUON_ERR_UNSUPPORTED.  The handle's own
+ * workspace, tables, second stream and profiling are not used.
+ * Every call on one device shares that device's array and leaves its last
+ * contents there: calls that overlap in time on one device race, so issue
+ * them one at a time or in order on one stream.
+ */
+muon_status_t ns_orthogonalize_batched_noalloc(muon_handle_t h, const void* const* in,
+                                               void* const* out, const int64_t* rows,
+                                               const int64_t* cols, int64_t n, muon_dtype_t dtype,
+                                               int32_t ns_steps, const float* ns_coeffs, float eps,
+                                               muon_ns_precision_t prec, void* stream);
+
+/*
  * AdamW for the parameters Muon does not take: Sec. 6.4 (Fig. "muon-
  * grouping") sends one-dimensional and scalar parameters to AdamW through a
  * chained optimizer, with decoupled weight decay.  The paper prints no

@@ -78,7 +78,7 @@ EXPORTS = ["muon_create", "muon_destroy", "muon_reserve", "muon_set_workspace_li
            "muon_workspace_bytes", "muon_step", "ns_orthogonalize_batched",
            "muon_validate_step", "muon_plan_step", "muon_status_string", "muon_last_error",
            "muon_abi_version", "muon_profile_enable", "muon_profile_read", "muon_adamw_step",
-           "muon_set_streams"]
+           "muon_set_streams", "ns_orthogonalize_batched_noalloc"]
 
 _lib: Optional[ctypes.CDLL] = None
 
@@ -100,7 +100,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.muon_workspace_bytes.argtypes = [vp]
     lib.muon_workspace_bytes.restype = ctypes.c_size_t
     lib.muon_step.argtypes = [vp, ctypes.POINTER(MuonParam), i64, ctypes.POINTER(MuonHParams), vp]
-    for name in ("ns_orthogonalize_batched",):
+    for name in ("ns_orthogonalize_batched", "ns_orthogonalize_batched_noalloc"):
         getattr(lib, name).argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp),
                                        ctypes.POINTER(i64), ctypes.POINTER(i64), i64,
                                        ctypes.c_int, i32, ctypes.POINTER(ctypes.c_float),
@@ -121,7 +121,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.muon_last_error.restype = ctypes.c_char_p
     for name in ("muon_create", "muon_destroy", "muon_reserve", "muon_set_workspace_limit",
                  "muon_step", "ns_orthogonalize_batched", "muon_validate_step", "muon_plan_step",
-                 "muon_profile_enable", "muon_profile_read", "muon_adamw_step", "muon_set_streams"):
+                 "muon_profile_enable", "muon_profile_read", "muon_adamw_step", "muon_set_streams",
+                 "ns_orthogonalize_batched_noalloc"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -359,8 +360,10 @@ class Muon:
                                              ctypes.c_void_p(_stream_ptr(stream))))
 
     def orthogonalize(self, inputs, outputs, ns_steps=5, ns_coeffs=None, eps=1e-7,
-                      ns_precision="bf16", stream=None):
-        """outputs[i] <- NS(inputs[i]) (ns_orthogonalize_batched); 2-D tensors."""
+                      ns_precision="bf16", stream=None, noalloc=False):
+        """outputs[i] <- NS(inputs[i]) (ns_orthogonalize_batched); 2-D tensors.
+        With noalloc, ns_orthogonalize_batched_noalloc: the library's fixed
+        device array instead of the handle's workspace (no allocation)."""
         n = len(inputs)
         if len(outputs) != n:
             raise ValueError("inputs and outputs differ in length")
@@ -385,7 +388,8 @@ class Muon:
         if ns_coeffs is not None:
             flat = _coeff_table(ns_coeffs, ns_steps)
             coeff = (ctypes.c_float * max(1, len(flat)))(*flat)
-        self._check(self.lib.ns_orthogonalize_batched(
+        fn = self.lib.ns_orthogonalize_batched_noalloc if noalloc else self.lib.ns_orthogonalize_batched
+        self._check(fn(
             self.h, ins, outs, rows, cols, n, dt, int(ns_steps),
             ctypes.cast(coeff, ctypes.POINTER(ctypes.c_float)) if coeff else None,
             float(eps), NS_F32 if ns_precision == "f32" else NS_BF16,

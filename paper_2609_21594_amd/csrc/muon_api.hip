@@ -11,6 +11,7 @@
 #include <cstdint>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <new>
 #include <string>
 #include <tuple>
@@ -105,6 +106,7 @@ struct muon_handle {
   hipEvent_t fork = nullptr, join = nullptr;
   bool log = false;                  // MUON_HIP_LOG set (and not "0"): each call's plan on stderr
   char err[512] = {0};               // message of the last failure (fixed: setting it allocates nothing)
+  void* scratch = nullptr;           // this device's copy of the scratch array (see below), or null
 };
 
 namespace {
@@ -967,6 +969,51 @@ std::vector<int> step_counts(const CoeffTables& tables) {
   return k;
 }
 
+// ---------------------------------------------------------------------------
+// Allocation-free orthogonalisation (ns_orthogonalize_batched_noalloc).
+// Its workspace and descriptor table live in `scratch`, a fixed array of this
+// library in device memory: each device the library runs on holds its own
+// copy until the process ends.  In host code `scratch` names a host-side
+// stand-in, never the device memory: its device address on each device is
+// taken once with hipGetSymbolAddress (muon_create, with the device current)
+// and kept per device; only that address reaches kernels.  Every call on a
+// device shares that device's array, so calls that overlap in time on one
+// device race (one at a time per device, or ordered on one stream).
+// ---------------------------------------------------------------------------
+constexpr size_t kScratchBytes = size_t(64) << 20;
+constexpr int kNoAllocMaxMats = 64;
+constexpr size_t kScratchDescBytes = (kNoAllocMaxMats * sizeof(MatDesc) + 255) & ~size_t(255);
+constexpr int kMaxDevices = 64;
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices] = {};
+
+// This device's address of `scratch` (device current), resolved once per
+// device; null when the runtime cannot give it.
+void* resolve_scratch(int device) {
+  if (device < 0 || device >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[device]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    g_scratch_addr[device] = p;
+  }
+  return g_scratch_addr[device];
+}
+
+// Do [a, a + na) and [b, b + nb) share a byte?
+bool bytes_meet(uintptr_t a, uintptr_t na, uintptr_t b, uintptr_t nb) { return a < b + nb && b < a + na; }
+
 }  // namespace
 
 extern "C" {
@@ -1022,6 +1069,8 @@ muon_status_t muon_create(muon_handle_t* out, int device) {
     delete h;
     return MUON_ERR_DEVICE;
   }
+  // the allocation-free entry point's array on this device (once per device)
+  h->scratch = resolve_scratch(device);
   *out = h;
   return MUON_OK;
 }
@@ -1250,5 +1299,148 @@ muon_status_t ns_orthogonalize_batched(muon_handle_t h, const void* const* in, v
   return execute(h, items, plan, 0.0, 0.0, sc, f32, tables, static_cast<hipStream_t>(stream));
 }
 
+
+muon_status_t ns_orthogonalize_batched_noalloc(muon_handle_t h, const void* const* in, void* const* out,
+                                               const int64_t* rows, const int64_t* cols, int64_t n,
+                                               muon_dtype_t dtype, int32_t ns_steps, const float* ns_coeffs,
+                                               float eps, muon_ns_precision_t prec, void* stream_) {
+  if (!h) return MUON_ERR_INVALID_ARGUMENT;
+  h->err[0] = '\0';
+  char buf[256] = {0};
+  Msg m{buf, sizeof buf};
+  muon_status_t st = check_orth_args(in, out, rows, cols, n, dtype, ns_steps, ns_coeffs, eps, prec, m);
+  if (st != MUON_OK) { set_err(h, "%s", buf); return st; }
+  if (n > kNoAllocMaxMats) {
+    set_err(h, "%lld matrices: the allocation-free entry point takes at most %d per call", (long long)n,
+            kNoAllocMaxMats);
+    return MUON_ERR_UNSUPPORTED;
+  }
+  if (n == 0) return MUON_OK;
+  // the matrices, and the bytes each reads (when not in place) and writes
+  const size_t es = dtype_size(dtype);
+  Item items[kNoAllocMaxMats];
+  Span spans[2 * kNoAllocMaxMats];
+  size_t nspans = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    if ((st = check_orth_matrix(in[i], out[i], rows[i], cols[i], es, i, m)) != MUON_OK) {
+      set_err(h, "%s", buf);
+      return st;
+    }
+    items[i] = orth_item(in[i], out[i], rows[i], cols[i], dtype, i);
+    const uintptr_t a = reinterpret_cast<uintptr_t>(in[i]), b = reinterpret_cast<uintptr_t>(out[i]);
+    const uintptr_t bytes = uintptr_t(rows[i]) * uintptr_t(cols[i]) * es;
+    spans[nspans++] = {b, b + bytes};
+    if (a != b) spans[nspans++] = {a, a + bytes};
+  }
+  // an output meets no other output and no input but its own exact in-place one
+  for (int64_t i = 0; i < n; ++i) {
+    const uintptr_t bi = reinterpret_cast<uintptr_t>(out[i]), ni = uintptr_t(rows[i] * cols[i]) * es;
+    for (int64_t j = 0; j < n; ++j) {
+      const uintptr_t aj = reinterpret_cast<uintptr_t>(in[j]), bj = reinterpret_cast<uintptr_t>(out[j]);
+      const uintptr_t nj = uintptr_t(rows[j] * cols[j]) * es;
+      if ((j != i && bytes_meet(bi, ni, bj, nj)) || (aj != bj && bytes_meet(bi, ni, aj, nj))) {
+        set_err(h, "an output overlaps another buffer");
+        return MUON_ERR_INVALID_ARGUMENT;
+      }
+    }
+  }
+  if (!h->scratch) {
+    set_err(h, "the scratch array of device %d is not available", h->device);
+    return MUON_ERR_DEVICE;
+  }
+  if ((st = check_device_spans(h, spans, nspans)) != MUON_OK) return st;
+  // Plan, as make_plan does: buckets by (short side, long side) in order of
+  // first appearance, sorted by work (stable), chunks of at most 2^29
+  // elements, and here also no larger than the scratch array holds.
+  const bool f32 = prec == MUON_NS_F32;
+  const int K = ns_steps;
+  int64_t bs[kNoAllocMaxMats], bl[kNoAllocMaxMats];
+  int nb = 0;
+  int bucket_of[kNoAllocMaxMats];
+  for (int64_t i = 0; i < n; ++i) {
+    const int64_t s = std::min(rows[i], cols[i]), l = std::max(rows[i], cols[i]);
+    int b = 0;
+    while (b < nb && !(bs[b] == s && bl[b] == l)) ++b;
+    if (b == nb) { bs[nb] = s; bl[nb] = l; ++nb; }
+    bucket_of[i] = b;
+  }
+  int korder[kNoAllocMaxMats];
+  for (int b = 0; b < nb; ++b) korder[b] = b;
+  const auto work = [&](int b) { return double(bs[b]) * double(bs[b]) * double(bl[b]) * std::max(1, K); };
+  for (int x = 1; x < nb; ++x)  // stable insertion sort, largest work first
+    for (int y = x; y > 0 && work(korder[y]) > work(korder[y - 1]); --y) std::swap(korder[y], korder[y - 1]);
+  Chunk chunks[kNoAllocMaxMats];
+  int64_t order[kNoAllocMaxMats];
+  int nc = 0, np = 0;
+  const size_t room = kScratchBytes - kScratchDescBytes;
+  for (int kb = 0; kb < nb; ++kb) {
+    const int b = korder[kb];
+    int64_t members[kNoAllocMaxMats];
+    int64_t nm = 0;
+    for (int64_t i = 0; i < n; ++i)
+      if (bucket_of[i] == b) members[nm++] = i;
+    Chunk c{};
+    c.s = bs[b]; c.l = bl[b];
+    c.S = muon::round_up(c.s, muon::kPad);
+    c.L = muon::round_up(c.l, muon::kPad);
+    c.pdt = dtype; c.gdt = dtype; c.cset = 0;
+    int64_t per = std::max<int64_t>(1, std::min<int64_t>(kMaxChunkMats, kDefaultChunkElems / (c.s * c.l)));
+    per = std::min(per, nm);
+    for (;; --per) {
+      c.count = per;
+      layout_chunk(c, f32, K);
+      if (c.bytes <= room) break;
+      if (per == 1) {
+        set_err(h, "a %lld x %lld matrix needs %zu workspace bytes; the allocation-free entry point has %zu",
+                (long long)c.s, (long long)c.l, c.bytes, room);
+        return MUON_ERR_UNSUPPORTED;
+      }
+    }
+    for (int64_t f = 0; f < nm; f += per) {
+      Chunk cc = c;
+      cc.first = np;
+      cc.count = std::min(per, nm - f);
+      layout_chunk(cc, f32, K);
+      for (int64_t j = 0; j < cc.count; ++j) order[np++] = members[f + j];
+      chunks[nc++] = cc;
+    }
+  }
+  float ct[3 * kMaxSteps];
+  for (int k = 0; k < K; ++k)
+    for (int j = 0; j < 3; ++j) ct[3 * k + j] = ns_coeffs ? ns_coeffs[3 * k + j] : kLegacyQuintic[j];
+  MatDesc table[kNoAllocMaxMats];
+  for (int p = 0; p < np; ++p) table[p] = make_desc(items[order[p]], 0.0, 0.0);
+  DeviceGuard dg(h->device);
+  if (!dg.ok) { set_err(h, "cannot select device %d", h->device); return MUON_ERR_DEVICE; }
+  const hipStream_t stream = static_cast<hipStream_t>(stream_);
+  char* const base = static_cast<char*>(h->scratch);
+  MatDesc* const d_desc = reinterpret_cast<MatDesc*>(base);
+  char* const ws = base + kScratchDescBytes;
+  hipError_t e = muon::put_descriptors(table, np, d_desc, stream);
+  if (e != hipSuccess) return device_fail(h, "descriptor upload", e);
+  StepScalars sc{};
+  sc.momentum = 0;
+  sc.eps = eps;
+  sc.final_kind = 1;
+  for (int ci = 0; ci < nc; ++ci) {
+    const Chunk& c = chunks[ci];
+    ChunkGeom g{};
+    g.s = int32_t(c.s); g.l = int32_t(c.l); g.S = int32_t(c.S); g.L = int32_t(c.L);
+    g.nmat = int32_t(c.count);
+    g.ns_f32 = f32 ? 1 : 0;
+    g.grad_dtype = g.param_dtype = dtype == MUON_BF16 ? muon::DT_BF16 : muon::DT_F32;
+    ChunkBuffers b{};
+    b.X[0] = ws + c.off_X[0]; b.X[1] = ws + c.off_X[1];
+    b.XT[0] = c.keeps_xt ? ws + c.off_XT[0] : nullptr;
+    b.XT[1] = c.keeps_xt ? ws + c.off_XT[1] : nullptr;
+    b.A = ws + c.off_A; b.B = ws + c.off_B;
+    b.partials = reinterpret_cast<double*>(ws + c.off_part);
+    b.rscale = reinterpret_cast<double*>(ws + c.off_r);
+    b.xscale = reinterpret_cast<float*>(b.rscale + c.count);
+    if ((e = muon::run_chunk(g, d_desc + c.first, b, sc, ct, K, stream, nullptr)) != hipSuccess)
+      return device_fail(h, "kernel launch", e);
+  }
+  return MUON_OK;
+}
 
 }  // extern "C"

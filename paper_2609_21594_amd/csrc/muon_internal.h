@@ -151,6 +151,17 @@ hipError_t run_adamw(const AdamDesc* d_desc, int n, int64_t blocks, int param_dt
                      int grad_dtype, const AdamScalars& sc, double bytes, hipStream_t stream,
                      LaunchTimer* timer);
 
+// Copies n descriptor records from host memory into the device table `dev`
+// on `stream`, as kernel arguments (kDescPerLaunch records per launch): no
+// staging buffer and no allocation.
+constexpr int kDescPerLaunch = 16;
+struct DescBatch {
+  int32_t n;
+  int32_t pad[3];
+  MatDesc d[kDescPerLaunch];
+};
+hipError_t put_descriptors(const MatDesc* host, int n, MatDesc* dev, hipStream_t stream);
+
 // Enqueues the whole step for one chunk on `stream`: momentum + partial
 // norms, norm finalisation, normalise + transpose-first + cast, K
 // Newton-Schulz steps (Gram, polynomial, update), and the final apply.

@@ -1820,6 +1820,31 @@ __global__ __launch_bounds__(256) void k_adamw(const AdamDesc* __restrict__ desc
   }
 }
 
+// Descriptor records copied into device memory by a kernel that takes them
+// as its arguments: the allocation-free entry point fills its table this
+// way, with no host staging buffer.  Indices are compile-time constants, so
+// the records are read straight from the argument segment.
+namespace {
+__global__ __launch_bounds__(64) void k_put_desc(DescBatch b, MatDesc* __restrict__ dst) {
+  if (threadIdx.x != 0) return;
+#pragma unroll
+  for (int i = 0; i < kDescPerLaunch; ++i)
+    if (i < b.n) dst[i] = b.d[i];
+}
+}  // namespace
+
+hipError_t put_descriptors(const MatDesc* host, int n, MatDesc* dev, hipStream_t st) {
+  for (int first = 0; first < n; first += kDescPerLaunch) {
+    DescBatch b{};
+    b.n = min(kDescPerLaunch, n - first);
+    for (int i = 0; i < b.n; ++i) b.d[i] = host[first + i];
+    hipLaunchKernelGGL(k_put_desc, dim3(1), dim3(64), 0, st, b, dev + first);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 hipError_t run_adamw(const AdamDesc* d_desc, int n, int64_t blocks, int param_dtype, int grad_dtype,
                      const AdamScalars& sc, double bytes, hipStream_t st, LaunchTimer* timer) {
   if (n <= 0 || blocks <= 0) return hipSuccess;
