@@ -92,13 +92,21 @@ def upload(inputs, wl):
 def cpu_baseline(wl, inputs):
     """Times the oracle on one matrix per (short, long) shape bucket and
     extrapolates to the workload's mix of shapes."""
+    import contextlib
+
     import numpy as np
     from oracle import muon_ref as ref
+    from paper_2609_21594_amd import synth as synth_mod
     try:
         from threadpoolctl import threadpool_limits
     except ImportError:  # pragma: no cover
         threadpool_limits = None
-    cores = min(16, len(os.sched_getaffinity(0)))
+    # every core in the process affinity, unless the environment sets a
+    # smaller BLAS/OpenMP thread count (a GPU host's per-GPU CPU share)
+    affinity = len(os.sched_getaffinity(0))
+    env_threads = [int(v) for k in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS")
+                   if (v := os.environ.get(k, "")).isdigit() and int(v) > 0]
+    cores = min([affinity] + env_threads)
     buckets = {}
     for i, m in enumerate(wl.matrices):
         key = (min(m.rows, m.cols), max(m.rows, m.cols))
@@ -107,7 +115,6 @@ def cpu_baseline(wl, inputs):
                          ns_steps=wl.ns_steps, nesterov=wl.nesterov)
     dec = (lambda a, dt: ref.decode_bf16(a) if dt == "bf16" else np.asarray(a, np.float64))
     total, sampled = 0.0, []
-    import contextlib
     limit = threadpool_limits(limits=cores) if threadpool_limits else contextlib.nullcontext()
     with limit:
         for key, idx in buckets.items():
@@ -122,6 +129,20 @@ def cpu_baseline(wl, inputs):
             dt = time.perf_counter() - t0
             total += dt * len(idx)
             sampled.append(f"{wl.matrices[i].name} {wl.matrices[i].rows}x{wl.matrices[i].cols}: {dt:.2f}s")
+    # workload 1 (one 256 x 128 fp32 matrix) on a single thread, median of 20
+    wl1 = synth_mod.WORKLOADS[1]
+    m1 = synth_mod.make_matrix(wl1, 0)
+    hp1 = ref.MuonHParams(lr=wl1.lr, beta=wl1.beta, weight_decay=wl1.weight_decay,
+                          ns_steps=wl1.ns_steps, nesterov=wl1.nesterov)
+    one = threadpool_limits(limits=1) if threadpool_limits else contextlib.nullcontext()
+    t1 = []
+    with one:
+        for _ in range(20):
+            t0 = time.perf_counter()
+            ref.muon_step_matrix(np.asarray(m1.W, np.float64), np.asarray(m1.g, np.float64),
+                                 np.asarray(m1.buf, np.float64), hp1)
+            t1.append(time.perf_counter() - t0)
+    single_ms = float(np.median(t1)) * 1e3
     cpu = "unknown"
     try:
         with open("/proc/cpuinfo") as f:
@@ -132,10 +153,13 @@ def cpu_baseline(wl, inputs):
     except OSError:
         pass
     return {"value": len(wl.matrices) / total, "unit": "matrices/s", "cores": cores,
-            "kind": "oracle",
+            "kind": "oracle", "affinity_cores": affinity, "cpu_model": cpu,
+            "workload1_single_thread_ms": single_ms,
             "sample": (f"fp64 NumPy oracle, one full {'orthogonalisation' if wl.orthogonalize_only else 'Muon step'} on one matrix per shape bucket "
                        f"({'; '.join(sampled)}), extrapolated by bucket counts to all "
-                       f"{len(wl.matrices)} matrices; {cores} BLAS threads on {cpu}")}
+                       f"{len(wl.matrices)} matrices; {cores} BLAS threads ({affinity} cores in the "
+                       f"process affinity{', capped by the thread count the environment sets' if cores < affinity else ''}) "
+                       f"on {cpu}; workload 1 (256x128 fp32, one step) on one thread: {single_ms:.2f} ms")}
 
 
 def views_step(muon, W, G, B, wl, hp, steps, warmup):
