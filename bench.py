@@ -28,7 +28,9 @@ views: the same step with every layer's q, k and v taken as zero-copy,
   head-interleaved views of one fused QKV weight (and its gradient and
   momentum), as a model adapter would hand them over;
 adamw: the chained AdamW over the parameters a 7B-like model leaves to it
-  (embedding and output head 2 x 32000 x 4096, 65 norm weights of 4096).
+  (embedding and output head 2 x 32000 x 4096, 65 norm weights of 4096);
+hbm_reference: the library's streaming copy over 4 GiB, the achievable HBM
+  rate the bandwidth-bound kernels are compared with.
 """
 from __future__ import annotations
 
@@ -229,6 +231,30 @@ def adamw_bench(muon, steps, warmup):
             "bytes_per_elem": 22, "gbs": gbs, "frac_hbm": gbs / PEAK_HBM_GBS}
 
 
+def hbm_reference(muon, steps=10, mib=4096):
+    """Rate of the library's reference streaming copy (muon_stream_copy) over
+    `mib` MiB: the achievable HBM ceiling for the bandwidth-bound kernels."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        muon.stream_copy(dst, src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        muon.stream_copy(dst, src)   # on the current stream, which the events see
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    bytes_ = 2.0 * n * 4
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"kernel": "k_stream_copy (muon_stream_copy)", "bytes": bytes_, "ms": ms,
+            "gbs": bytes_ / (ms * 1e-3) / 1e9, "frac_hbm": bytes_ / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS}
+
+
 def reference_gemm(wl):
     """Vendor-library context on the same GPU: torch.matmul (hipBLASLt) for
     the update product B(s x s) @ X(s x l) of each shape bucket, batched over
@@ -325,16 +351,22 @@ def main():
         run_step()
     torch.cuda.synchronize()
 
+    host_ms = []
+
     def timed(profile):
         if profile:
             muon.profile(True)
             muon.profile_read(reset=True)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
+        host = 0.0
         for _ in range(args.steps):
+            h0 = time.perf_counter()
             run_step()
+            host += time.perf_counter() - h0
         torch.cuda.synchronize()
         el = time.perf_counter() - t0
+        host_ms.append(host * 1e3 / args.steps)
         st = None
         if profile:
             st = muon.profile_read(reset=True)
@@ -395,8 +427,9 @@ def main():
     # The Newton-Schulz contractions alone: dense flops (Eq. 1 count) and the
     # MFMA work the kernels execute (upper tiles of the symmetric products,
     # padded extents), over the summed kernel time.
-    gemm_names = [k for k in ("gram_syrk", "poly_syrk", "update_gemm", "update_apply_gemm") if k in stats]
-    g_ms = sum(stats[k]["total_ms"] for k in gemm_names) / args.steps
+    gemm_names = [k for k in ("gram_syrk", "poly_syrk", "update_gemm", "update_apply_gemm", "ns_small")
+                  if k in stats and stats[k]["launches"]]
+    g_ms = max(1e-12, sum(stats[k]["total_ms"] for k in gemm_names) / args.steps)
     g_exec = sum(stats[k]["exec_flops"] for k in gemm_names) / args.steps
     ns_gemm = {"ms_per_step": g_ms,
                "dense_tflops": ns_flops / (g_ms * 1e-3) / 1e12,
@@ -422,6 +455,7 @@ def main():
         "roofline": roof,
         "kernels": kernels,
         "input_generation_s": gen_s,
+        "host_ms_per_call": host_ms[0],
     }
     if wl.index == 3 and not args.no_side:
         vms = views_step(muon, W, G, B, wl, hp, args.steps, args.warmup)
@@ -430,6 +464,10 @@ def main():
         del W, G, B
         torch.cuda.empty_cache()
         out["adamw"] = adamw_bench(muon, args.steps, args.warmup)
+        ref = hbm_reference(muon)
+        ref["momentum_norm_vs_copy"] = kernels["momentum_norm"]["gbs"] / ref["gbs"]
+        ref["adamw_vs_copy"] = out["adamw"]["gbs"] / ref["gbs"]
+        out["hbm_reference"] = ref
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, inputs)
     muon.close()

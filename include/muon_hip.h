@@ -293,7 +293,9 @@ muon_status_t muon_plan_step(const muon_param_t* params, int64_t n, const muon_h
  * unscaled X0 in one pass), norm_finalize, rescale (X0 = r*u for matrices
  * whose r is too large or small to be applied in the first products),
  * gram_syrk, poly_syrk, update_gemm, update_apply_gemm,
- * apply_x0, adamw.  `reset` != 0 clears the counters after reading. */
+ * apply_x0, adamw, ns_small (the whole step of a chunk whose short side is
+ * at most 128 with fp32 Newton-Schulz, in one fused launch).  `reset` != 0
+ * clears the counters after reading. */
 typedef struct {
   const char* name;
   int64_t launches;
@@ -305,6 +307,15 @@ typedef struct {
 muon_status_t muon_profile_enable(muon_handle_t h, int enable);
 muon_status_t muon_profile_read(muon_handle_t h, muon_kernel_stats_t* out, int cap, int* n,
                                 int reset);
+
+/* Measurement aid, no part of the Muon step: copies `bytes` from src to dst
+ * (device memory of the handle's device, 16-byte aligned, not overlapping)
+ * on `stream` with the access pattern that reaches the highest HBM rate
+ * (each workgroup a contiguous 256 KiB, 16-byte non-temporal accesses).  Its
+ * rate, 2*bytes over its time, is the achievable HBM ceiling the
+ * bandwidth-bound kernels (momentum/norm prologue, AdamW) are compared to. */
+muon_status_t muon_stream_copy(muon_handle_t h, void* dst, const void* src, size_t bytes,
+                               void* stream);
 
 const char* muon_status_string(muon_status_t s);
 /* Message of the last failure on h (empty string if none); valid until the

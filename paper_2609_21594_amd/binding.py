@@ -78,7 +78,7 @@ EXPORTS = ["muon_create", "muon_destroy", "muon_reserve", "muon_set_workspace_li
            "muon_workspace_bytes", "muon_step", "ns_orthogonalize_batched",
            "muon_validate_step", "muon_plan_step", "muon_status_string", "muon_last_error",
            "muon_abi_version", "muon_profile_enable", "muon_profile_read", "muon_adamw_step",
-           "muon_set_streams", "ns_orthogonalize_batched_noalloc"]
+           "muon_set_streams", "ns_orthogonalize_batched_noalloc", "muon_stream_copy"]
 
 _lib: Optional[ctypes.CDLL] = None
 
@@ -113,6 +113,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.muon_adamw_step.argtypes = [vp, ctypes.POINTER(AdamWParam), i64, ctypes.POINTER(AdamWHParams), vp]
     lib.muon_profile_enable.argtypes = [vp, ctypes.c_int]
     lib.muon_set_streams.argtypes = [vp, ctypes.c_int]
+    lib.muon_stream_copy.argtypes = [vp, vp, vp, ctypes.c_size_t, vp]
     lib.muon_profile_read.argtypes = [vp, ctypes.POINTER(MuonKernelStats), ctypes.c_int,
                                       ctypes.POINTER(ctypes.c_int), ctypes.c_int]
     lib.muon_status_string.argtypes = [ctypes.c_int]
@@ -122,7 +123,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     for name in ("muon_create", "muon_destroy", "muon_reserve", "muon_set_workspace_limit",
                  "muon_step", "ns_orthogonalize_batched", "muon_validate_step", "muon_plan_step",
                  "muon_profile_enable", "muon_profile_read", "muon_adamw_step", "muon_set_streams",
-                 "ns_orthogonalize_batched_noalloc"):
+                 "ns_orthogonalize_batched_noalloc", "muon_stream_copy"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -319,6 +320,17 @@ class Muon:
         self._check(self.lib.muon_profile_read(self.h, arr, 16, ctypes.byref(n), int(bool(reset))))
         return {arr[i].name.decode(): {f: getattr(arr[i], f) for f, _ in MuonKernelStats._fields_[1:]}
                 for i in range(n.value)}
+
+    def stream_copy(self, dst, src, stream=None):
+        """dst <- src with the library's HBM reference copy (muon_stream_copy);
+        same-size device tensors, contiguous."""
+        _check_device([dst, src], self.device)
+        nbytes = src.numel() * src.element_size()
+        if dst.numel() * dst.element_size() != nbytes or not (dst.is_contiguous() and src.is_contiguous()):
+            raise ValueError("stream_copy needs contiguous tensors of equal size")
+        self._check(self.lib.muon_stream_copy(self.h, ctypes.c_void_p(dst.data_ptr()),
+                                              ctypes.c_void_p(src.data_ptr()), nbytes,
+                                              ctypes.c_void_p(_stream_ptr(stream))))
 
     @property
     def workspace_bytes(self) -> int:

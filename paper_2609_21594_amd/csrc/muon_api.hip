@@ -534,7 +534,7 @@ struct Chunk {
   int64_t first, count;
   size_t bytes;
   // byte offsets inside the workspace
-  size_t off_X[2], off_XT[2], off_A, off_B, off_part, off_r;
+  size_t off_X[2], off_XT[2], off_A, off_B, off_part, off_r, off_sync;
   bool keeps_xt;  // X^T buffers present (see chunk_keeps_xt)
 };
 
@@ -554,7 +554,9 @@ void layout_chunk(Chunk& c, bool ns_f32, int K) {
   const size_t es = ns_f32 ? 4 : 2;
   const size_t xb = align256(size_t(c.count) * size_t(c.S) * size_t(c.L) * es);
   const size_t ab = align256(size_t(c.count) * size_t(c.S) * size_t(c.S) * es);
-  const size_t pb = align256(size_t(c.count) * size_t(muon::norm_tiles(c.S, c.L)) * 8);
+  const bool small = muon::chunk_is_small(c.S, c.L, ns_f32);
+  const size_t parts = std::max<size_t>(size_t(muon::norm_tiles(c.S, c.L)), small ? muon::kSmallMaxGroup : 0);
+  const size_t pb = align256(size_t(c.count) * parts * 8);
   c.keeps_xt = muon::chunk_keeps_xt(c.S, c.L, ns_f32, K);
   size_t off = 0;
   c.off_X[0] = off; off += xb;
@@ -567,6 +569,7 @@ void layout_chunk(Chunk& c, bool ns_f32, int K) {
   c.off_B = off; off += ab;
   c.off_part = off; off += pb;
   c.off_r = off; off += align256(size_t(c.count) * 12);  // rscale (fp64), then xscale (fp32)
+  c.off_sync = off; off += small ? size_t(muon::kSmallSyncBytes) : 0;
   c.bytes = off;
 }
 
@@ -856,6 +859,7 @@ muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Pla
     b.partials = reinterpret_cast<double*>(ws + c.off_part);
     b.rscale = reinterpret_cast<double*>(ws + c.off_r);
     b.xscale = reinterpret_cast<float*>(b.rscale + c.count);
+    b.sync = muon::chunk_is_small(c.S, c.L, ns_f32) ? reinterpret_cast<unsigned*>(ws + c.off_sync) : nullptr;
     const std::vector<float>& ct = tables[size_t(c.cset)];
     launch_err = muon::run_chunk(g, d_desc + c.first, b, sc, ct.data(), int(ct.size() / 3), cs,
                                  h->profiling ? &h->timer : nullptr);
@@ -1131,7 +1135,7 @@ muon_status_t muon_profile_read(muon_handle_t h, muon_kernel_stats_t* out, int c
                                 int reset) {
   static const char* const kNames[muon::KK_COUNT] = {
       "momentum_norm", "norm_finalize", "rescale", "gram_syrk",
-      "poly_syrk", "update_gemm", "update_apply_gemm", "apply_x0", "adamw"};
+      "poly_syrk", "update_gemm", "update_apply_gemm", "apply_x0", "adamw", "ns_small"};
   if (!h || (cap > 0 && !out)) return MUON_ERR_INVALID_ARGUMENT;
   DeviceGuard dg(h->device);
   const bool ok = h->timer.collect();
@@ -1437,10 +1441,34 @@ muon_status_t ns_orthogonalize_batched_noalloc(muon_handle_t h, const void* cons
     b.partials = reinterpret_cast<double*>(ws + c.off_part);
     b.rscale = reinterpret_cast<double*>(ws + c.off_r);
     b.xscale = reinterpret_cast<float*>(b.rscale + c.count);
+    b.sync = muon::chunk_is_small(c.S, c.L, f32) ? reinterpret_cast<unsigned*>(ws + c.off_sync) : nullptr;
     if ((e = muon::run_chunk(g, d_desc + c.first, b, sc, ct, K, stream, nullptr)) != hipSuccess)
       return device_fail(h, "kernel launch", e);
   }
   return MUON_OK;
+}
+
+
+muon_status_t muon_stream_copy(muon_handle_t h, void* dst, const void* src, size_t bytes, void* stream) {
+  if (!h) return MUON_ERR_INVALID_ARGUMENT;
+  h->err[0] = '\0';
+  if (bytes == 0) return MUON_OK;
+  const uintptr_t d = reinterpret_cast<uintptr_t>(dst), s = reinterpret_cast<uintptr_t>(src);
+  if (!dst || !src || d % 16 || s % 16) {
+    set_err(h, "dst and src must be non-NULL and 16-byte aligned");
+    return MUON_ERR_INVALID_ARGUMENT;
+  }
+  if (bytes_meet(d, bytes, s, bytes)) {
+    set_err(h, "dst and src overlap");
+    return MUON_ERR_INVALID_ARGUMENT;
+  }
+  const Span spans[2] = {{d, d + bytes}, {s, s + bytes}};
+  muon_status_t st = check_device_spans(h, spans, 2);
+  if (st != MUON_OK) return st;
+  DeviceGuard dg(h->device);
+  if (!dg.ok) { set_err(h, "cannot select device %d", h->device); return MUON_ERR_DEVICE; }
+  const hipError_t e = muon::stream_copy(dst, src, bytes, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? MUON_OK : device_fail(h, "kernel launch", e);
 }
 
 }  // extern "C"

@@ -70,7 +70,8 @@ struct ChunkBuffers {
   void* XT[2];          // L x S, row stride S
   void* A;              // S x S
   void* B;              // S x S
-  double* partials;     // nmat x norm_tiles(S, L), sums of u^2 in fp64
+  double* partials;     // nmat x norm_tiles(S, L) (at least kSmallMaxGroup), sums of u^2 in fp64
+  unsigned* sync;       // group counters of the fused small-matrix launch (chunk_is_small), or null
   double* rscale;       // nmat: r = 1 / (||u||_F + eps), fp64
   float* xscale;        // nmat: the scale the first Newton-Schulz step applies
                         // to X: r, or 1 where X already holds r*u
@@ -87,7 +88,7 @@ struct StepScalars {
 // Kernel families, for the optional per-launch timing.
 enum KernelKind : int {
   KK_PARTIALS = 0, KK_FINALIZE, KK_NORMALIZE, KK_GRAM, KK_POLY, KK_UPDATE, KK_FINAL,
-  KK_APPLY_X0, KK_ADAMW, KK_COUNT
+  KK_APPLY_X0, KK_ADAMW, KK_SMALL, KK_COUNT
 };
 
 // Receives a bracket around every launch when timing is enabled.
@@ -114,6 +115,15 @@ inline bool tile_rows_fit(int64_t S, int64_t L, int es) {
 // least one step, rows within that kernel's offsets.
 inline bool chunk_keeps_xt(int64_t S, int64_t L, bool ns_f32, int K) {
   return ns_f32 || S % 256 != 0 || L % 256 != 0 || K == 0 || !tile_rows_fit(S, L, 2);
+}
+// A chunk runs as one fused launch (k_ns_small: momentum, norm, every
+// Newton-Schulz step and the update) when its short side is at most 128 and
+// its NS arithmetic is fp32; such a chunk also needs the group counters
+// (kSmallSyncBytes) and kSmallMaxGroup norm partials per matrix.
+constexpr int kSmallMaxGroup = 32;
+constexpr int64_t kSmallSyncBytes = 64 * 1024;
+inline bool chunk_is_small(int64_t S, int64_t L, bool ns_f32) {
+  return ns_f32 && S == 128 && L <= (int64_t(1) << 16);
 }
 
 // ---------------------------------------------------------------------------
@@ -161,6 +171,9 @@ struct DescBatch {
   MatDesc d[kDescPerLaunch];
 };
 hipError_t put_descriptors(const MatDesc* host, int n, MatDesc* dev, hipStream_t stream);
+
+// The HBM reference copy (dst and src 16-byte aligned, not overlapping).
+hipError_t stream_copy(void* dst, const void* src, size_t bytes, hipStream_t stream);
 
 // Enqueues the whole step for one chunk on `stream`: momentum + partial
 // norms, norm finalisation, normalise + transpose-first + cast, K

@@ -1594,10 +1594,454 @@ struct Timed {
   }
 };
 
+// ---------------------------------------------------------------------------
+// Fused Newton-Schulz for short sides up to 128 (k_ns_small): the whole step
+// of a chunk -- momentum, norm, X0, every Newton-Schulz step and the update --
+// in one launch.  Such matrices are far too small for the tile kernels: a
+// 128 x 256 fp32 product fills one or two workgroups, so separate launches
+// leave the device idle and each product runs on a single compute unit.
+//
+// Each matrix is taken by a group of G = RB x CB workgroups: RB row blocks
+// of 32 rows of X (the padded short side Sx = 32 RB) times CB column groups
+// (a function of the shape alone, so results do not depend on the batch).
+// Per step, every product on MFMA in 16 x 16 units shared out over the four
+// wavefronts:
+//   A[Ri, Cc] = X[Ri, :] X[Cc, :]^T             column blocks c = j, j + CB, ..
+//   -- group barrier --
+//   B[Ri, Cc] = b A[Ri, Cc] + c A[Ri, :] A[Cc, :]^T   (A symmetric)
+//   -- group barrier (CB > 1: rows Ri of B come from several workgroups) --
+//   X'[Ri, Dd] = a X[Ri, Dd] + B[Ri, :] X^T[Dd, :]^T  column blocks d = j, j + CB, ..
+//   -- group barrier --
+// X is kept in both orientations, so every operand is a row-major matrix
+// with K contiguous, stored tiled (see ti).  The prologue writes u itself
+// into X and applies r = 1 / (||u|| + eps) in the first step's products
+// (exact fp32 u; X0 = r u is formed first when r is far from 1).  The last
+// step writes W (or the output) straight from the fp32 values, in the
+// parameter's own layout.  Extents are padded to multiples of 32; the
+// padding of X, A and B is written as zeros and stays zero.
+//
+// The members of a group run on one XCD (workgroup b runs on XCD b % 8, and
+// each workgroup checks its XCC_ID against its group's): their data meets in
+// that XCD's L2, so a barrier drains the memory operations of every wave and
+// bumps a counter, and every read of data that other members wrote is a
+// non-temporal load, which bypasses the compute unit's own (incoherent) L1.
+// Should a group find its members spread over XCDs, every barrier of that
+// group also writes back and invalidates at device scope.  Spins are
+// bounded, so every wave ends whatever happens.
+// ---------------------------------------------------------------------------
+struct SmallArgs {
+  const MatDesc* desc;
+  StepScalars sc;
+  int32_t s, l, S, L, Sx, Lx;
+  int32_t nmat, G, RB, CB, groups, K;
+  int32_t param_dtype;
+  char* X[2];
+  char* XT[2];
+  char* A;
+  char* B;
+  int64_t matX, matA;        // bytes per matrix
+  double* partials;          // nmat x kSmallMaxGroup
+  unsigned* sync;            // per group: [0] counter, [1] spin timeouts, [2 .. 2 + G) member XCC ids
+  float coeffs[3 * 64];      // (a, b, c) per step
+};
+
+__device__ __forceinline__ unsigned xcc_id() {
+  return __builtin_amdgcn_s_getreg((3 << 11) | (0 << 6) | 20) & 15u;  // HW_REG_XCC_ID, bits [3:0]
+}
+
+__device__ __forceinline__ void group_barrier(unsigned* sync, unsigned target, bool local) {
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's loads and stores are done (stores reached L2)
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    if (!local) __threadfence();
+    __hip_atomic_fetch_add(sync, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    unsigned spins = 0;
+    while (__hip_atomic_load(sync, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+      __builtin_amdgcn_s_sleep(2);
+      if (++spins > (1u << 22)) {  // never expected: count it and go on
+        __hip_atomic_fetch_add(sync + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+    }
+    if (!local) __atomic_thread_fence(__ATOMIC_ACQUIRE);
+  }
+  __syncthreads();
+}
+
+// Loads of data other members wrote: non-temporal, so they never allocate, and
+// never hit, a line in this compute unit's L1, which is not coherent with
+// the other compute units (measured: plain loads after the barrier return
+// stale L1 lines; non-temporal ones do not).  The L2 they read is the one
+// the writers' stores reached.
+__device__ __forceinline__ u32x4_t ld16(const char* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+}
+
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// 16 x 16 blocks of P Q^T (fp32), K in k-groups of 16 elements (64 bytes of a
+// row).  Lane l loads the 16 bytes of row l % 16 at byte 16 (l / 16) of a
+// group and issues four v_mfma_f32_16x16x4_f32, the j-th taking element j
+// (k = j, 4 + j, 8 + j, 12 + j across the lanes' four row quarters); even
+// and odd groups accumulate apart and are added at the end of the block.
+// Result layout: lane l, register r holds row 4 (l / 16) + r, column l % 16.
+//
+// small_units runs the 16 x 16 units of one phase, shared out round-robin
+// over the four wavefronts.  unit(u, P, Q, row0, col0) gives unit u's
+// operands (the first chunks of its 16-row blocks, tiled layout) and origin; pre(row, col) is loaded
+// with the unit's first operands; epi(row, col, value, term) receives the 4
+// values of each lane.  A wavefront's units and their K batches form one
+// stream: the loads of the next batch (of the same or the next unit) are in
+// flight while the MFMAs of the current one issue.
+constexpr int kSmallBatch = 8;  // k-groups per batch
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// The fused launch keeps X, X^T, A and B in a tiled layout: each 16-row x
+// 16-k chunk of a row-major matrix is 1 KB, stored in the order of the lanes
+// that take it as an MFMA operand (lane l: row l % 16, k 4 (l / 16) .. + 3),
+// chunks row-block major.  A wavefront's operand load is then 1 KB of
+// consecutive bytes (whole cache lines), where the row-major layout touched
+// 16 lines for 64 bytes each (measured 4x slower).  Element (r, k) of a
+// matrix with kg k-groups per row, in floats:
+__device__ __forceinline__ int64_t ti(int r, int k, int kg) {
+  return (static_cast<int64_t>(r >> 4) * kg + (k >> 4)) * 256 + (((k & 15) >> 2) * 16 + (r & 15)) * 4 + (k & 3);
+}
+
+template <typename Unit, typename Pre, typename Epi>
+__device__ __forceinline__ void small_units(int nunits, int kg, Unit&& unit, Pre&& pre, Epi&& epi) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int mine = nunits > wave ? (nunits - wave + 3) / 4 : 0;  // this wavefront's units
+  const int nbat = (kg + kSmallBatch - 1) / kSmallBatch;
+  const int total = mine * nbat;
+  if (total == 0) return;
+  struct Batch {
+    u32x4_t a[kSmallBatch], b[kSmallBatch];
+    float term[4];
+  };
+  // the operands of stream item `it` (unit it / nbat, batch it % nbat)
+  auto issue = [&](int it, Batch& bt) __attribute__((always_inline)) {
+    const int u = wave + 4 * (it / nbat), bb = it % nbat;
+    const char* P;
+    const char* Q;
+    int row0, col0;
+    unit(u, P, Q, row0, col0);
+    const char* pr = P + lane * 16;
+    const char* qr = Q + lane * 16;
+    const int g0 = bb * kSmallBatch;
+#pragma unroll
+    for (int t = 0; t < kSmallBatch; ++t)
+      if (g0 + t < kg) {
+        bt.a[t] = ld16(pr + static_cast<int64_t>(g0 + t) * 1024);
+        bt.b[t] = ld16(qr + static_cast<int64_t>(g0 + t) * 1024);
+      }
+    if (bb == 0) {
+      const int row = row0 + 4 * (lane >> 4), col = col0 + (lane & 15);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) bt.term[r] = pre(row + r, col);
+    }
+  };
+  f32x4_t acc[2];
+  float term[4];
+  auto consume = [&](int it, Batch& bt) __attribute__((always_inline)) {
+    const int bb = it % nbat, g0 = bb * kSmallBatch;
+    if (bb == 0) {
+      acc[0] = acc[1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) term[r] = bt.term[r];
+    }
+#pragma unroll
+    for (int t = 0; t < kSmallBatch; ++t)
+      if (g0 + t < kg) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[t & 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bt.a[t][j]), __uint_as_float(bt.b[t][j]),
+                                                            acc[t & 1], 0, 0, 0);
+      }
+    if (bb == nbat - 1) {
+      const int u = wave + 4 * (it / nbat);
+      const char* P;
+      const char* Q;
+      int row0, col0;
+      unit(u, P, Q, row0, col0);
+      const f32x4_t v = acc[0] + acc[1];
+      const int row = row0 + 4 * (lane >> 4), col = col0 + (lane & 15);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) epi(row + r, col, v[r], term[r]);
+    }
+  };
+  Batch b0, b1;
+  issue(0, b0);
+  for (int it = 0; it < total; it += 2) {
+    if (it + 1 < total) issue(it + 1, b1);
+    consume(it, b0);
+    if (it + 1 >= total) break;
+    if (it + 2 < total) issue(it + 2, b0);
+    consume(it + 1, b1);
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void put(char* base, int64_t idx, float v) {
+  reinterpret_cast<T*>(base)[idx] = from_f32<T>(v);
+}
+template <typename T>
+__device__ __forceinline__ float get(const char* base, int64_t idx) {
+  return to_f32<T>(__builtin_nontemporal_load(reinterpret_cast<const T*>(base) + idx));
+}
+
+// fp32 Newton-Schulz (the chunks this launch takes; see chunk_is_small).
+template <typename GT, bool MOM>
+__global__ __launch_bounds__(256) void k_ns_small(SmallArgs sa) {
+  using XT = float;
+  __shared__ double red4[4];
+  const int b = blockIdx.x, xcd = b & 7, slot = b >> 3;
+  const int group = (slot / sa.G) * 8 + xcd, member = slot % sa.G;
+  const int bi = member / sa.CB, bj = member % sa.CB;  // row block, column group
+  unsigned* const sync = sa.sync + group * 64;
+  if (threadIdx.x == 0) __hip_atomic_store(sync + 2 + member, xcc_id(), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  unsigned nbar = 0;
+  bool local = false;
+  const int kgx = sa.L / 16, kgs = sa.S / 16;      // k-groups per row of X, of X^T, A and B
+  const int ncb = sa.Lx / 32;                                    // column blocks of X
+  const int c0 = bj * ncb / sa.CB, c1 = (bj + 1) * ncb / sa.CB;  // this member's, in the prologue
+  const int w = (c1 - c0) * 32;                                  // prologue columns of this member
+  const float beta = sa.sc.beta, omb = sa.sc.one_minus_beta;
+  for (int m = group; m < sa.nmat; m += sa.groups) {
+    const MatDesc md = sa.desc[m];
+    const bool tr = md.transposed != 0;
+    const GT* g = static_cast<const GT*>(md.g);
+    char* X0 = sa.X[0] + m * sa.matX;
+    char* XT0 = sa.XT[0] + m * sa.matX;
+    // element e of the member's 32 x w block of X: consecutive threads on
+    // consecutive elements of u's rows (coalesced for either orientation)
+    auto coord = [&](int e, int& xr, int& xc) {
+      if (tr) { xr = bi * 32 + (e & 31); xc = c0 * 32 + (e >> 5); }
+      else { xr = bi * 32 + e / w; xc = c0 * 32 + e % w; }
+    };
+    // ---- prologue pass 1: momentum, u into X (fp32, exact), sum of u^2 ----
+    double acc2 = 0.0;
+    const int ne = 32 * w;
+    for (int e0 = threadIdx.x; e0 < ne; e0 += 256 * 8) {
+      float gv[8], bv[8];
+      int64_t gi[8], bix[8];
+      bool in[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        int xr, xc;
+        coord(e0 + 256 * t, xr, xc);
+        in[t] = e0 + 256 * t < ne && xr < sa.s && xc < sa.l;
+        const int ur = tr ? xc : xr, uc = tr ? xr : xc;
+        gi[t] = in[t] ? view_index(md, ur, uc) : 0;
+        bix[t] = (MOM && in[t]) ? buf_index(md, ur, uc) : 0;
+        gv[t] = in[t] ? to_f32<GT>(g[gi[t]]) : 0.f;
+        bv[t] = (MOM && in[t]) ? md.buf[bix[t]] : 0.f;
+      }
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        if (e0 + 256 * t >= ne) continue;
+        float u = gv[t];
+        if (MOM && in[t]) {
+          const float bn = fmaf(beta, bv[t], omb * gv[t]);
+          md.buf[bix[t]] = bn;
+          u = sa.sc.nesterov ? fmaf(beta, bn, omb * gv[t]) : bn;
+        }
+        acc2 = fma(static_cast<double>(u), static_cast<double>(u), acc2);
+        int xr, xc;
+        coord(e0 + 256 * t, xr, xc);
+        put<XT>(X0, ti(xr, xc, kgx), u);
+        put<XT>(XT0, ti(xc, xr, kgs), u);
+      }
+    }
+    const double part = block_sum_256(acc2, red4);
+    if (threadIdx.x == 0) sa.partials[static_cast<int64_t>(m) * kSmallMaxGroup + member] = part;
+    ++nbar;
+    group_barrier(sync, nbar * sa.G, local);
+    if (nbar == 1) {  // the members' XCDs are known from here on
+      bool same = true;
+      for (int q = 0; q < sa.G; ++q)
+        same = same && __hip_atomic_load(sync + 2 + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                           __hip_atomic_load(sync + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      local = same;
+    }
+    double nsq = 0.0;
+    for (int q = 0; q < sa.G; ++q)
+      nsq += __builtin_nontemporal_load(sa.partials + static_cast<int64_t>(m) * kSmallMaxGroup + q);
+    const double r = 1.0 / (sqrt(nsq) + static_cast<double>(sa.sc.eps));
+    // X holds u itself (exact in fp32).  While r keeps (r u)(r u)^T far
+    // inside the fp32 range, the first step applies it (A0 = r^2 u u^T,
+    // X1 = r (a u + B0 u)); otherwise, and for K = 0, X0 = r u is formed here.
+    const bool fold = sa.K > 0 && r >= 0x1p-40 && r <= 0x1p40;
+    const float xs = fold ? static_cast<float>(r) : 1.f;
+    float s1, s2;
+    split_scale(r, s1, s2);
+    // ---- prologue pass 2 (unless folded): X0 = r u over the member's block ----
+    if (!fold)
+    for (int e0 = threadIdx.x; e0 < ne; e0 += 256 * 8) {
+      float v[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        int xr, xc;
+        coord(e0 + 256 * t, xr, xc);
+        v[t] = e0 + 256 * t < ne ? (get<XT>(X0, ti(xr, xc, kgx)) * s1) * s2 : 0.f;
+      }
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        if (e0 + 256 * t >= ne) continue;
+        int xr, xc;
+        coord(e0 + 256 * t, xr, xc);
+        if (sa.K == 0) {
+          if (xr < sa.s && xc < sa.l) {
+            const int64_t pidx = view_index(md, tr ? xc : xr, tr ? xr : xc);
+            if (sa.sc.final_kind == 0)
+              store_from_f32(md.W, pidx, sa.param_dtype,
+                             fmaf(md.decay, load_as_f32(md.W, pidx, sa.param_dtype), -md.upd_scale * v[t]));
+            else
+              store_from_f32(md.out, pidx, sa.param_dtype, v[t]);
+          }
+        } else {
+          put<XT>(X0, ti(xr, xc, kgx), v[t]);
+          put<XT>(XT0, ti(xc, xr, kgs), v[t]);
+        }
+      }
+    }
+    if (sa.K == 0) continue;
+    if (!fold) {
+      ++nbar;
+      group_barrier(sync, nbar * sa.G, local);
+    }
+    int cur = 0;
+    const int na = (sa.RB - bj + sa.CB - 1) / sa.CB;      // 32-column blocks of A and B of this member
+    for (int k = 0; k < sa.K; ++k) {
+      const float ca = sa.coeffs[3 * k], cb = sa.coeffs[3 * k + 1], cc = sa.coeffs[3 * k + 2];
+      const float sa_ = k == 0 ? xs * xs : 1.f, sx_ = k == 0 ? xs : 1.f;  // the folded r on the first step
+      const char* Xc = sa.X[cur] + m * sa.matX;
+      const char* XTc = sa.XT[cur] + m * sa.matX;
+      char* Am = sa.A + m * sa.matA;
+      char* Bm = sa.B + m * sa.matA;
+      // unit u of a phase over 32 x 32 blocks: block u / 4, quarter u % 4
+      // A = X X^T: rows bi, column blocks bj, bj + CB, ..
+      small_units(
+          4 * na, sa.Lx / 16,
+          [&](int u, const char*& P, const char*& Q, int& row0, int& col0) {
+            row0 = bi * 32 + 16 * ((u & 3) >> 1);
+            col0 = (bj + (u >> 2) * sa.CB) * 32 + 16 * (u & 1);
+            P = Xc + ti(row0, 0, kgx) * 4;
+            Q = Xc + ti(col0, 0, kgx) * 4;
+          },
+          [](int, int) { return 0.f; },
+          [&](int row, int col, float v, float) { put<XT>(Am, ti(row, col, kgs), sa_ * v); });
+      ++nbar;
+      group_barrier(sync, nbar * sa.G, local);
+      // B = b A + c A A (A symmetric: column block c of A is row block c)
+      small_units(
+          4 * na, sa.Sx / 16,
+          [&](int u, const char*& P, const char*& Q, int& row0, int& col0) {
+            row0 = bi * 32 + 16 * ((u & 3) >> 1);
+            col0 = (bj + (u >> 2) * sa.CB) * 32 + 16 * (u & 1);
+            P = Am + ti(row0, 0, kgs) * 4;
+            Q = Am + ti(col0, 0, kgs) * 4;
+          },
+          [&](int row, int col) { return get<XT>(Am, ti(row, col, kgs)); },
+          [&](int row, int col, float v, float a_) { put<XT>(Bm, ti(row, col, kgs), fmaf(cb, a_, cc * v)); });
+      if (sa.CB > 1) {
+        ++nbar;
+        group_barrier(sync, nbar * sa.G, local);
+      }
+      // X' = a X + B X: rows bi, column blocks bj, bj + CB, .. of X
+      const bool last = k + 1 == sa.K;
+      char* Xn = sa.X[cur ^ 1] + m * sa.matX;
+      char* XTn = sa.XT[cur ^ 1] + m * sa.matX;
+      const int nx = (ncb - bj + sa.CB - 1) / sa.CB;
+      small_units(
+          4 * nx, sa.Sx / 16,
+          [&](int u, const char*& P, const char*& Q, int& row0, int& col0) {
+            row0 = bi * 32 + 16 * ((u & 3) >> 1);
+            col0 = (bj + (u >> 2) * sa.CB) * 32 + 16 * (u & 1);
+            P = Bm + ti(row0, 0, kgs) * 4;
+            Q = XTc + ti(col0, 0, kgs) * 4;
+          },
+          [&](int row, int col) { return get<XT>(Xc, ti(row, col, kgx)); },
+          [&](int xr, int xc, float v, float x_) {
+            const float o = sx_ * fmaf(ca, x_, v);
+            if (!last) {
+              put<XT>(Xn, ti(xr, xc, kgx), o);
+              put<XT>(XTn, ti(xc, xr, kgs), o);
+            } else if (xr < sa.s && xc < sa.l) {
+              const int64_t pidx = view_index(md, tr ? xc : xr, tr ? xr : xc);
+              if (sa.sc.final_kind == 0)
+                store_from_f32(md.W, pidx, sa.param_dtype,
+                               fmaf(md.decay, load_as_f32(md.W, pidx, sa.param_dtype), -md.upd_scale * o));
+              else
+                store_from_f32(md.out, pidx, sa.param_dtype, o);
+            }
+          });
+      if (!last) {
+        ++nbar;
+        group_barrier(sync, nbar * sa.G, local);
+      }
+      cur ^= 1;
+    }
+  }
+}
+
+// Zeroes n words (the group counters before a fused launch).
+__global__ __launch_bounds__(256) void k_zero_words(unsigned* p, int n) {
+  for (int i = threadIdx.x; i < n; i += 256) p[i] = 0u;
+}
+
+template <typename GT, typename XT>
+hipError_t run_small(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBuffers& wb, const StepScalars& sc,
+                     const float* coeffs, int K, hipStream_t st, LaunchTimer* timer) {
+  SmallArgs sa{};
+  sa.desc = d_desc;
+  sa.sc = sc;
+  sa.s = cg.s; sa.l = cg.l; sa.S = cg.S; sa.L = cg.L;
+  sa.Sx = (cg.s + 31) / 32 * 32;
+  sa.Lx = (cg.l + 31) / 32 * 32;
+  sa.nmat = cg.nmat;
+  sa.RB = sa.Sx / 32;
+  const int cus = device_cu_count();
+  // column groups: 4, or as many as there are 32-column blocks of X.  A
+  // function of the shape alone, so that the order of every sum, and with
+  // it each matrix's result, does not depend on the other matrices of the call.
+  sa.CB = min(4, sa.Lx / 32);
+  sa.G = sa.RB * sa.CB;
+  // groups: 8 per round (one per XCD), as many rounds as fit one workgroup per CU
+  const int rounds = max(1, min((cg.nmat + 7) / 8, cus / (8 * sa.G)));
+  sa.groups = 8 * rounds;
+  sa.K = K;
+  sa.param_dtype = cg.param_dtype;
+  sa.X[0] = static_cast<char*>(wb.X[0]); sa.X[1] = static_cast<char*>(wb.X[1]);
+  sa.XT[0] = static_cast<char*>(wb.XT[0]); sa.XT[1] = static_cast<char*>(wb.XT[1]);
+  sa.A = static_cast<char*>(wb.A); sa.B = static_cast<char*>(wb.B);
+  sa.matX = static_cast<int64_t>(cg.S) * cg.L * sizeof(XT);
+  sa.matA = static_cast<int64_t>(cg.S) * cg.S * sizeof(XT);
+  sa.partials = wb.partials;
+  sa.sync = wb.sync;
+  for (int i = 0; i < 3 * K; ++i) sa.coeffs[i] = coeffs[i];
+  if constexpr (!std::is_same<XT, float>::value) return hipErrorInvalidValue;  // fp32 NS only
+  Timed tm(timer, KK_SMALL, st);
+  hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(256), 0, st, wb.sync, sa.groups * 64);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const dim3 grid(static_cast<unsigned>(sa.groups * sa.G));
+  if (sc.momentum)
+    hipLaunchKernelGGL((k_ns_small<GT, true>), grid, dim3(256), 0, st, sa);
+  else
+    hipLaunchKernelGGL((k_ns_small<GT, false>), grid, dim3(256), 0, st, sa);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const double nm = cg.nmat, s = cg.s, l = cg.l, Sx = sa.Sx, Lx = sa.Lx;
+  const double gsz = sizeof(GT), psz = cg.param_dtype == DT_BF16 ? 2.0 : 4.0;
+  tm.done(nm * K * (4.0 * s * s * l + 2.0 * s * s * s), nm * K * (4.0 * Sx * Sx * Lx + 2.0 * Sx * Sx * Sx),
+          nm * s * l * (gsz + (sc.momentum ? 8.0 : 0.0) + (sc.final_kind == 0 ? 2.0 * psz : psz)));
+  return hipSuccess;
+}
+
 template <typename GT, typename XT>
 hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBuffers& wb,
                        const StepScalars& sc, const float* coeffs, int K, hipStream_t st,
                        LaunchTimer* timer) {
+  if (wb.sync) return run_small<GT, XT>(cg, d_desc, wb, sc, coeffs, K, st, timer);
   const int nmat = cg.nmat;
   const double nm = nmat;
   const int64_t numel = static_cast<int64_t>(cg.s) * cg.l;
@@ -1841,6 +2285,51 @@ hipError_t put_descriptors(const MatDesc* host, int n, MatDesc* dev, hipStream_t
     hipLaunchKernelGGL(k_put_desc, dim3(1), dim3(64), 0, st, b, dev + first);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// Streaming copy, the reference for what HBM delivers to the elementwise
+// kernels: each workgroup copies its own contiguous 256 KiB with 16-byte
+// non-temporal accesses, four in flight per thread (measured the fastest of
+// grid-stride and block-contiguous variants, 1-8 accesses per thread).
+namespace {
+constexpr int64_t kCopyVecsPerBlock = 16384;
+__global__ __launch_bounds__(256) void k_stream_copy(const u32x4_t* __restrict__ src, u32x4_t* __restrict__ dst,
+                                                     int64_t n) {
+  const int64_t lo = static_cast<int64_t>(blockIdx.x) * kCopyVecsPerBlock;
+  const int64_t hi = min(lo + kCopyVecsPerBlock, n);
+  for (int64_t i = lo + threadIdx.x; i < hi; i += 4 * 256) {
+    u32x4_t v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (i + u * 256 < hi) v[u] = __builtin_nontemporal_load(src + i + u * 256);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (i + u * 256 < hi) __builtin_nontemporal_store(v[u], dst + i + u * 256);
+  }
+}
+__global__ __launch_bounds__(256) void k_copy_tail(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
+                                                   int64_t n) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i < n) dst[i] = src[i];
+}
+}  // namespace
+
+hipError_t stream_copy(void* dst, const void* src, size_t bytes, hipStream_t st) {
+  const int64_t vecs = static_cast<int64_t>(bytes / 16);
+  if (vecs > 0) {
+    const int64_t blocks = (vecs + kCopyVecsPerBlock - 1) / kCopyVecsPerBlock;
+    hipLaunchKernelGGL(k_stream_copy, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st,
+                       static_cast<const u32x4_t*>(src), static_cast<u32x4_t*>(dst), vecs);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const int64_t tail = static_cast<int64_t>(bytes % 16);
+  if (tail > 0) {
+    hipLaunchKernelGGL(k_copy_tail, dim3(1), dim3(256), 0, st, static_cast<const uint8_t*>(src) + vecs * 16,
+                       static_cast<uint8_t*>(dst) + vecs * 16, tail);
+    return hipGetLastError();
   }
   return hipSuccess;
 }
