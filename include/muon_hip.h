@@ -44,6 +44,11 @@
  *     allocation that holds its start, its last byte must be such memory too
  *     (allocations mapped back to back); otherwise MUON_ERR_INVALID_ARGUMENT.  muon_validate_step does not query the
  *     runtime and accepts any address.
+ *   - A call that repeats the handle's previous muon_step or
+ *     ns_orthogonalize_batched request exactly (the same entries, pointers,
+ *     shapes, views, dtypes, coefficient values and options; lr and
+ *     weight_decay may differ) reuses that request's checks and plan: its
+ *     buffers are not queried from the runtime again.
  *   - A handle is not thread-safe; use one handle per host thread.
  *   - Results are deterministic: the same call on the same data gives the same
  *     bits, and a matrix's result does not depend on which other matrices

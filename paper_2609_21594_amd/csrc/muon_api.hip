@@ -83,6 +83,8 @@ struct DeviceTable {
   std::vector<char> last;            // content of `dev`
 };
 
+struct CallCache;
+
 struct muon_handle {
   int device = 0;
   bool profiling = false;
@@ -107,6 +109,9 @@ struct muon_handle {
   bool log = false;                  // MUON_HIP_LOG set (and not "0"): each call's plan on stderr
   char err[512] = {0};               // message of the last failure (fixed: setting it allocates nothing)
   void* scratch = nullptr;           // this device's copy of the scratch array (see below), or null
+  // The last request's validated form and plan, reused when the same request
+  // comes again (see CallCache).
+  CallCache* cache = nullptr;
 };
 
 namespace {
@@ -747,6 +752,89 @@ void destroy_table(DeviceTable& t) {
   t = DeviceTable();
 }
 
+}  // namespace
+
+// The last request of a handle in validated and planned form.  A training
+// loop passes the same tensors, shapes and options every step, so the
+// checks, the runtime queries about each buffer and the planning run once
+// for them.  The key is the request's bytes: the entry array, the
+// hyperparameters except lr and weight decay (they only change the
+// descriptor table, rebuilt every call), the contents of every coefficient
+// table, and the handle settings the plan depends on.
+struct CallCache {
+  bool valid = false;
+  std::vector<char> key;
+  std::vector<Item> items;
+  CoeffTables tables;
+  std::vector<Span> spans;
+  Plan plan;
+};
+
+namespace {
+
+CallCache* cache_of(muon_handle_t h) {
+  if (!h->cache) h->cache = new (std::nothrow) CallCache();
+  return h->cache;
+}
+
+void key_append(std::vector<char>& k, const void* p, size_t n) {
+  const char* c = static_cast<const char*>(p);
+  k.insert(k.end(), c, c + n);
+}
+
+// A coefficient table's contents, when its step count is one validation
+// would accept (otherwise validation rejects the call anyway).
+void key_coeffs(std::vector<char>& k, const float* c, int32_t steps) {
+  if (c && steps > 0 && steps <= kMaxSteps) key_append(k, c, size_t(12) * size_t(steps));
+}
+
+void key_settings(std::vector<char>& k, const muon_handle* h) {
+  key_append(k, &h->nstreams, sizeof h->nstreams);
+  key_append(k, &h->ws_limit, sizeof h->ws_limit);
+}
+
+bool step_key(std::vector<char>& k, const muon_param_t* params, int64_t n, const muon_hparams_t* hp,
+              const muon_handle* h) {
+  if (!hp || n < 0 || (n > 0 && !params)) return false;
+  k.clear();
+  k.reserve(size_t(n) * sizeof(muon_param_t) + 256);
+  k.push_back('S');
+  muon_hparams_t hc = *hp;
+  hc.lr = 0.f;
+  hc.weight_decay = 0.f;
+  hc.ns_coeffs = nullptr;
+  key_append(k, &hc, sizeof hc);
+  key_coeffs(k, hp->ns_coeffs, hp->ns_steps);
+  for (int64_t i = 0; i < n; ++i) {
+    muon_param_t pc = params[i];
+    pc.ns_coeffs = nullptr;
+    key_append(k, &pc, sizeof pc);
+    key_coeffs(k, params[i].ns_coeffs, params[i].ns_steps);
+  }
+  key_settings(k, h);
+  return true;
+}
+
+bool orth_key(std::vector<char>& k, const void* const* in, void* const* out, const int64_t* rows,
+              const int64_t* cols, int64_t n, int dtype, int32_t ns_steps, const float* coeffs, float eps,
+              int prec, const muon_handle* h) {
+  if (n < 0 || (n > 0 && (!in || !out || !rows || !cols))) return false;
+  k.clear();
+  k.push_back('O');
+  key_append(k, &n, sizeof n);
+  key_append(k, &dtype, sizeof dtype);
+  key_append(k, &ns_steps, sizeof ns_steps);
+  key_append(k, &eps, sizeof eps);
+  key_append(k, &prec, sizeof prec);
+  key_coeffs(k, coeffs, ns_steps);
+  key_append(k, in, size_t(n) * sizeof(void*));
+  key_append(k, out, size_t(n) * sizeof(void*));
+  key_append(k, rows, size_t(n) * sizeof(int64_t));
+  key_append(k, cols, size_t(n) * sizeof(int64_t));
+  key_settings(k, h);
+  return true;
+}
+
 MatDesc make_desc(const Item& it, double lr, double wd) {
   MatDesc d{};
   d.W = it.W; d.g = it.g; d.buf = it.buf; d.out = it.out;
@@ -834,45 +922,50 @@ muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Pla
   if ((st = upload_table(h, h->mats, table.data(), table.size() * sizeof(MatDesc), stream)) != MUON_OK)
     return fail(st);
   const MatDesc* d_desc = static_cast<const MatDesc*>(h->mats.dev);
-  if (two) {
-    hipError_t e = hipEventRecord(h->fork, stream);
-    if (e == hipSuccess) e = hipStreamWaitEvent(h->side, h->fork, 0);
-    if (e != hipSuccess) return fail(device_fail(h, "fork", e));
-  }
-  hipError_t launch_err = hipSuccess;
-  for (size_t ci = 0; ci < plan.chunks.size() && launch_err == hipSuccess; ++ci) {
-    const Chunk& c = plan.chunks[ci];
-    const bool odd = on_side[ci] != 0;
-    char* ws = static_cast<char*>(h->ws) + (odd ? slot : 0);
-    const hipStream_t cs = odd ? h->side : stream;
-    ChunkGeom g{};
-    g.s = int32_t(c.s); g.l = int32_t(c.l); g.S = int32_t(c.S); g.L = int32_t(c.L);
-    g.nmat = int32_t(c.count);
-    g.ns_f32 = ns_f32 ? 1 : 0;
-    g.grad_dtype = c.gdt == MUON_BF16 ? muon::DT_BF16 : muon::DT_F32;
-    g.param_dtype = c.pdt == MUON_BF16 ? muon::DT_BF16 : muon::DT_F32;
-    ChunkBuffers b{};
-    b.X[0] = ws + c.off_X[0]; b.X[1] = ws + c.off_X[1];
-    b.XT[0] = c.keeps_xt ? ws + c.off_XT[0] : nullptr;
-    b.XT[1] = c.keeps_xt ? ws + c.off_XT[1] : nullptr;
-    b.A = ws + c.off_A; b.B = ws + c.off_B;
-    b.partials = reinterpret_cast<double*>(ws + c.off_part);
-    b.rscale = reinterpret_cast<double*>(ws + c.off_r);
-    b.xscale = reinterpret_cast<float*>(b.rscale + c.count);
-    b.sync = muon::chunk_is_small(c.S, c.L, ns_f32) ? reinterpret_cast<unsigned*>(ws + c.off_sync) : nullptr;
-    const std::vector<float>& ct = tables[size_t(c.cset)];
-    launch_err = muon::run_chunk(g, d_desc + c.first, b, sc, ct.data(), int(ct.size() / 3), cs,
-                                 h->profiling ? &h->timer : nullptr);
-  }
-  if (two) {  // joined even after a failed launch, so later calls stay ordered
-    hipError_t e = hipEventRecord(h->join, h->side);
-    if (e == hipSuccess) e = hipStreamWaitEvent(stream, h->join, 0);
-    if (e != hipSuccess) {
-      (void)hipStreamSynchronize(h->side);  // not joined: wait on the host instead
-      if (launch_err == hipSuccess) return fail(device_fail(h, "join", e));
+  // The launches of the call on stream `s`: fork, every chunk, join.
+  auto launch_all = [&](hipStream_t s) -> muon_status_t {
+    if (two) {
+      hipError_t e = hipEventRecord(h->fork, s);
+      if (e == hipSuccess) e = hipStreamWaitEvent(h->side, h->fork, 0);
+      if (e != hipSuccess) return device_fail(h, "fork", e);
     }
-  }
-  if (launch_err != hipSuccess) return fail(device_fail(h, "kernel launch", launch_err));
+    hipError_t launch_err = hipSuccess;
+    for (size_t ci = 0; ci < plan.chunks.size() && launch_err == hipSuccess; ++ci) {
+      const Chunk& c = plan.chunks[ci];
+      const bool odd = on_side[ci] != 0;
+      char* ws = static_cast<char*>(h->ws) + (odd ? slot : 0);
+      const hipStream_t cs = odd ? h->side : s;
+      ChunkGeom g{};
+      g.s = int32_t(c.s); g.l = int32_t(c.l); g.S = int32_t(c.S); g.L = int32_t(c.L);
+      g.nmat = int32_t(c.count);
+      g.ns_f32 = ns_f32 ? 1 : 0;
+      g.grad_dtype = c.gdt == MUON_BF16 ? muon::DT_BF16 : muon::DT_F32;
+      g.param_dtype = c.pdt == MUON_BF16 ? muon::DT_BF16 : muon::DT_F32;
+      ChunkBuffers b{};
+      b.X[0] = ws + c.off_X[0]; b.X[1] = ws + c.off_X[1];
+      b.XT[0] = c.keeps_xt ? ws + c.off_XT[0] : nullptr;
+      b.XT[1] = c.keeps_xt ? ws + c.off_XT[1] : nullptr;
+      b.A = ws + c.off_A; b.B = ws + c.off_B;
+      b.partials = reinterpret_cast<double*>(ws + c.off_part);
+      b.rscale = reinterpret_cast<double*>(ws + c.off_r);
+      b.xscale = reinterpret_cast<float*>(b.rscale + c.count);
+      b.sync = muon::chunk_is_small(c.S, c.L, ns_f32) ? reinterpret_cast<unsigned*>(ws + c.off_sync) : nullptr;
+      const std::vector<float>& ct = tables[size_t(c.cset)];
+      launch_err = muon::run_chunk(g, d_desc + c.first, b, sc, ct.data(), int(ct.size() / 3), cs,
+                                   h->profiling ? &h->timer : nullptr);
+    }
+    if (two) {  // joined even after a failed launch, so later calls stay ordered
+      hipError_t e = hipEventRecord(h->join, h->side);
+      if (e == hipSuccess) e = hipStreamWaitEvent(s, h->join, 0);
+      if (e != hipSuccess) {
+        (void)hipStreamSynchronize(h->side);  // not joined: wait on the host instead
+        if (launch_err == hipSuccess) return device_fail(h, "join", e);
+      }
+    }
+    if (launch_err != hipSuccess) return device_fail(h, "kernel launch", launch_err);
+    return MUON_OK;
+  };
+  if ((st = launch_all(stream)) != MUON_OK) return fail(st);
   return end_call(h, stream);
 }
 
@@ -1048,6 +1141,7 @@ muon_status_t muon_create(muon_handle_t* out, int device) {
   h->device = device;
   const char* lg = std::getenv("MUON_HIP_LOG");
   h->log = lg && *lg && std::strcmp(lg, "0") != 0;
+
   DeviceGuard dg(device);
   auto drop_side = [h]() {
     if (h->side) (void)hipStreamDestroy(h->side);
@@ -1075,6 +1169,7 @@ muon_status_t muon_create(muon_handle_t* out, int device) {
   }
   // the allocation-free entry point's array on this device (once per device)
   h->scratch = resolve_scratch(device);
+
   *out = h;
   return MUON_OK;
 }
@@ -1094,6 +1189,7 @@ muon_status_t muon_destroy(muon_handle_t h) {
     if (h->side) (void)hipStreamDestroy(h->side);
     if (h->fork) (void)hipEventDestroy(h->fork);
     if (h->join) (void)hipEventDestroy(h->join);
+    delete h->cache;
     h->timer.destroy();
   }
   delete h;
@@ -1194,15 +1290,39 @@ muon_status_t muon_step(muon_handle_t h, const muon_param_t* params, int64_t n,
   h->err[0] = '\0';
   char buf[256] = {0};
   Msg m{buf, sizeof buf};
-  std::vector<Item> items;
-  CoeffTables tables;
-  std::vector<Span> spans;
-  muon_status_t st = validate_step(params, n, hp, &items, &tables, m, &spans);
-  if (st != MUON_OK) { set_err(h, "%s", buf); return st; }
+  CallCache local;
+  CallCache* c = cache_of(h);
+  std::vector<char> key;
+  const bool keyed = c && step_key(key, params, n, hp, h);
+  if (!c) c = &local;
+  muon_status_t st = MUON_OK;
+  const bool hit = keyed && c->valid && c->key == key;
+  if (hit) {
+    // the same request as the last one: only lr and weight decay may differ
+    if (!std::isfinite(hp->lr) || !std::isfinite(hp->weight_decay)) {
+      set_err(h, "lr, beta, weight_decay must be finite and eps finite and >= 0");
+      return MUON_ERR_INVALID_ARGUMENT;
+    }
+  } else {
+    c->valid = false;
+    c->items.clear();
+    c->spans.clear();
+    st = validate_step(params, n, hp, &c->items, &c->tables, m, &c->spans);
+    if (st != MUON_OK) { set_err(h, "%s", buf); return st; }
+    c->plan = make_plan(c->items, hp->max_chunk_elems, hp->ns_precision == MUON_NS_F32, step_counts(c->tables));
+    c->valid = keyed;
+    if (keyed) c->key.swap(key);
+  }
+  const std::vector<Item>& items = c->items;
+  const CoeffTables& tables = c->tables;
+  const Plan& plan = c->plan;
   if (items.empty()) return MUON_OK;
-  if ((st = check_device_spans(h, spans)) != MUON_OK) return st;
+  // the runtime's view of the buffers was checked when this request first came
+  if (!hit && (st = check_device_spans(h, c->spans)) != MUON_OK) {
+    c->valid = false;
+    return st;
+  }
   const bool f32 = hp->ns_precision == MUON_NS_F32;
-  const Plan plan = make_plan(items, hp->max_chunk_elems, f32, step_counts(tables));
   StepScalars sc{};
   sc.beta = hp->beta;
   sc.one_minus_beta = 1.0f - hp->beta;
@@ -1287,15 +1407,33 @@ muon_status_t ns_orthogonalize_batched(muon_handle_t h, const void* const* in, v
   h->err[0] = '\0';
   char buf[256] = {0};
   Msg m{buf, sizeof buf};
-  std::vector<Item> items;
-  std::vector<Span> spans;
-  muon_status_t st = validate_orth(in, out, rows, cols, n, dtype, ns_steps, ns_coeffs, eps, prec, &items, m, &spans);
-  if (st != MUON_OK) { set_err(h, "%s", buf); return st; }
-  if (items.empty()) return MUON_OK;
-  if ((st = check_device_spans(h, spans)) != MUON_OK) return st;
+  CallCache local;
+  CallCache* c = cache_of(h);
+  std::vector<char> key;
+  const bool keyed = c && orth_key(key, in, out, rows, cols, n, dtype, ns_steps, ns_coeffs, eps, prec, h);
+  if (!c) c = &local;
+  muon_status_t st = MUON_OK;
   const bool f32 = prec == MUON_NS_F32;
-  const CoeffTables tables{coefficient_table(ns_steps, ns_coeffs)};
-  const Plan plan = make_plan(items, 0, f32, step_counts(tables));
+  const bool hit = keyed && c->valid && c->key == key;
+  if (!hit) {
+    c->valid = false;
+    c->items.clear();
+    c->spans.clear();
+    st = validate_orth(in, out, rows, cols, n, dtype, ns_steps, ns_coeffs, eps, prec, &c->items, m, &c->spans);
+    if (st != MUON_OK) { set_err(h, "%s", buf); return st; }
+    c->tables = CoeffTables{coefficient_table(ns_steps, ns_coeffs)};
+    c->plan = make_plan(c->items, 0, f32, step_counts(c->tables));
+    c->valid = keyed;
+    if (keyed) c->key.swap(key);
+  }
+  const std::vector<Item>& items = c->items;
+  const CoeffTables& tables = c->tables;
+  const Plan& plan = c->plan;
+  if (items.empty()) return MUON_OK;
+  if (!hit && (st = check_device_spans(h, c->spans)) != MUON_OK) {
+    c->valid = false;
+    return st;
+  }
   StepScalars sc{};
   sc.momentum = 0;
   sc.eps = eps;

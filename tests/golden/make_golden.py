@@ -98,14 +98,24 @@ def run_matrix(wl: synth.Workload, i: int):
                 rho=resid / max(float(np.linalg.norm(dW)), 1e-300))
 
 
-def make(workload: int):
+def make(workload: int, cache_dir=None):
     wl = synth.WORKLOADS[workload]
     n = len(wl.matrices)
     cols = {k: [] for k in ("O", "dW", "buf", "rho")}
     counts = []
     t0 = time.time()
     for i in range(n):
-        res = run_matrix(wl, i)
+        # optional per-matrix cache, so an interrupted run resumes where it stopped
+        cpath = (os.path.join(cache_dir, f"w{workload}_s{SAMPLE_STREAM}_m{i}.npz")
+                 if cache_dir else None)
+        if cpath and os.path.exists(cpath):
+            with np.load(cpath, allow_pickle=False) as z:
+                res = {k: z[k] for k in ("O", "dW", "buf")}
+                res["rho"] = float(z["rho"])
+        else:
+            res = run_matrix(wl, i)
+            if cpath:
+                np.savez(cpath, **res)
         for k in cols:
             cols[k].append(res[k])
         counts.append(len(res["O"]))
@@ -123,6 +133,9 @@ def make(workload: int):
 if __name__ == "__main__":
     ap = argparse.ArgumentParser()
     ap.add_argument("workloads", nargs="*", type=int, default=[2, 4, 3, 5])
+    ap.add_argument("--cache", default=None, help="directory for per-matrix results (resumable runs)")
     args = ap.parse_args()
+    if args.cache:
+        os.makedirs(args.cache, exist_ok=True)
     for w in args.workloads:
-        make(w)
+        make(w, args.cache)
