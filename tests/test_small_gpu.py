@@ -1,13 +1,14 @@
 """The fused small-matrix launch (fp32 Newton-Schulz, short side <= 128):
 element-wise parity with the oracle over short sides 1..128 and long sides
 128..2048, both orientations, K = 0, 1 and 5; many matrices sharing groups of
-workgroups; batching and repeat determinism."""
+workgroups; batching and repeat determinism.  The same shapes on the bf16
+path (the 128 x 128 tile kernel) against the bf16 gate."""
 import numpy as np
 import pytest
 
 from oracle import muon_ref as ref
 from paper_2609_21594_amd import synth
-from tests.gpu_util import MOMENTUM_TOL, TOL, decode, rel, require_gpu, to_bits, to_dev, to_host
+from tests.gpu_util import MOMENTUM_TOL, TOL, decode, o_gate, rel, require_gpu, to_bits, to_dev, to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -42,6 +43,21 @@ def test_small_orthogonalize_matches_oracle(muon, steps):
         err = rel(to_host(o), ref.orthogonalize(decode(g, "f32"), steps))
         print(f"small fp32 K={steps} {sh}: O err {err:.2e}", flush=True)
         assert err <= TOL["f32"], (sh, err)
+
+
+def test_small_shapes_bf16_path_match_oracle(muon):
+    import torch
+    shapes = [(s, l) for s in SHORT for l in LONG] + [(l, s) for s in (7, 128) for l in LONG]
+    G = [synth.draw(sh, 1.0, "bf16", rng(50, i)) for i, sh in enumerate(shapes)]
+    ins = [to_dev(g, "bf16") for g in G]
+    outs = [torch.full_like(t, float("nan")) for t in ins]
+    muon.orthogonalize(ins, outs, ns_precision="bf16")
+    torch.cuda.synchronize()
+    for sh, g, o in zip(shapes, G, outs):
+        x = decode(g, "bf16")
+        err, gate = o_gate(to_host(o), ref.orthogonalize(x, 5), "bf16", "bf16", G=x)
+        print(f"small bf16 {sh}: O err {err:.2e} (gate {gate:.2e})", flush=True)
+        assert err <= gate, (sh, err, gate)
 
 
 @pytest.mark.parametrize("pdt", ["f32", "bf16"])
