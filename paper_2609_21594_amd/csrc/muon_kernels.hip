@@ -1223,6 +1223,13 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   const bool stage_t = !QTR && ga.CT != nullptr;
   const bool stage_c = !FINAL && !stage_t;
   const bool e_epi = EPI == EPI_POLY && !epoly;  // the term is read in the epilogue
+  // Natural staging (the output tile, no epilogue input): each lane's 4
+  // consecutive rows of one column go to LDS as they are, 8 bytes at
+  // column-major position (col, row) with a 520-byte column pitch, and the
+  // copy-out reads whole rows back through transposing LDS reads.  No
+  // register transposes; diagonal tiles of the symmetric products take
+  // their lower triangle from the mirrored column at copy-out.
+  const bool stage_n = stage_c && !e_epi;
   // The factor the accumulators leave with: c for a polynomial that added
   // (b/c) A in the main loop; on the first step, whose X holds u unscaled,
   // r^2 for the Gram product and r for the update products.
@@ -1299,7 +1306,8 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
     return r * 512 + (((b >> 4) ^ key) << 4) + (b & 15);
   };
   const int wr0 = tr ? bn * BN : bm * BM, wc0 = tr ? bm * BM : bn * BN;  // W block origin
-  if (stage_t || stage_c || stage_w) __syncthreads();  // every wave is done with the operand slabs
+  // (every wave finished its operand-slab reads before the last slab's
+  // barrier, so the staging area, which overlaps the slabs, is free)
   if (stage_w) {
     static_assert(BM * BN * 2 / 1024 == 16 * NW, "W tile: 16 load instructions per wave");
     const char* wb = static_cast<const char*>(md->W) + (static_cast<int64_t>(wr0) * md->ld + wc0) * 2;
@@ -1377,7 +1385,9 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
 #pragma unroll
               for (int q = 0; q < 4; ++q) v[q] = fmaf(ga.alpha, e[q], ga.beta * v[q]);
             }
-            if (!FINAL && diag) {  // stage_c: (row, col) and (col, row) for row <= col
+            if (stage_n) {
+              *reinterpret_cast<uint2*>(smem + (col - bn * BN) * TST + (row0 - bm * BM) * 2) = pack_bf16x4(v);
+            } else if (!FINAL && diag) {  // stage_c: (row, col) and (col, row) for row <= col
               const int cl = col - bn * BN;
 #pragma unroll
               for (int q = 0; q < 4; ++q) {
@@ -1430,7 +1440,46 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
     }
     __syncthreads();  // the next tile's loads overwrite the staging area
   }
-  if (stage_c) {
+  if (stage_n) {
+    __syncthreads();
+    // Copy-out: a wave instruction writes 4 rows x 256 bytes.  In each
+    // 16-lane group G, lane t (r = t / 4, q = t % 4) addresses the 8 bytes
+    // (rows R .. R + 3) of column C0 + 8 q + r, then of column C0 + 8 q + 4 + r;
+    // ds_read_b64_tr_b16 hands lane t row R + t % 4, columns C0 + 8 (t / 4)
+    // .. + 3 and + 4 .. + 7: 16 consecutive bytes of one row.
+    const int G = lane >> 4, t = lane & 15;
+    const int ra = ((t & 3) * 8 + (t >> 2)) * TST;     // column offset of this lane's first address
+    const int rrow = t & 3, rcol = 8 * (t >> 2);       // what it receives
+    static_assert(BM * BN * 2 / 1024 == 16 * NW, "copy-out: 16 instructions per wave");
+    auto out_row = [&](int it, auto diagc) __attribute__((always_inline)) {
+      const int task = it * NW + wave;                 // 4 rows x 128 columns
+      const int R = 4 * (task >> 1), C0 = 128 * (task & 1) + 32 * G;
+      const char* a = smem + C0 * TST + ra + 2 * R;
+      const uint2 lo = tr_read_b64(a), hi = tr_read_b64(a + 4 * TST);
+      u32x4_t v{lo.x, lo.y, hi.x, hi.y};
+      const int row = R + rrow, c = C0 + rcol;
+      if (decltype(diagc)::value && c < row) {
+        // columns c .. c + 7 below the diagonal hold (col, row): row `row`
+        // of the staged column-major tile, i.e. column `row`, rows c ..
+        const char* m = smem + row * TST + 2 * c;
+        const uint2 l0 = *reinterpret_cast<const uint2*>(m), l1 = *reinterpret_cast<const uint2*>(m + 8);
+        const u32x4_t low{l0.x, l0.y, l1.x, l1.y};
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          const int c2 = c + 2 * d;                    // elements c2 (low half) and c2 + 1
+          v[d] = c2 + 1 < row ? low[d] : (c2 < row ? ((low[d] & 0xffffu) | (v[d] & 0xffff0000u)) : v[d]);
+        }
+      }
+      store_out(reinterpret_cast<u32x4_t*>(C + static_cast<int64_t>(bm * BM + row) * ga.ldc + (bn * BN + c) * 2), v);
+    };
+    if (diag) {
+      for (int it = 0; it < 16; ++it) out_row(it, std::true_type{});
+    } else {
+#pragma unroll
+      for (int it = 0; it < 16; ++it) out_row(it, std::false_type{});
+    }
+    __syncthreads();  // the next tile's loads overwrite the staging area
+  } else if (stage_c) {
     __syncthreads();
     // output tile rows (BN bf16 = 512 bytes each) -> C, 16 bytes a thread
     constexpr int CH = BN * 2 / 16;
