@@ -559,7 +559,7 @@ void layout_chunk(Chunk& c, bool ns_f32, int K) {
   const size_t es = ns_f32 ? 4 : 2;
   const size_t xb = align256(size_t(c.count) * size_t(c.S) * size_t(c.L) * es);
   const size_t ab = align256(size_t(c.count) * size_t(c.S) * size_t(c.S) * es);
-  const bool small = muon::chunk_is_small(c.S, c.L, ns_f32);
+  const bool small = muon::chunk_is_small(c.s, c.l, ns_f32);
   const size_t parts = std::max<size_t>(size_t(muon::norm_tiles(c.S, c.L)), small ? muon::kSmallMaxGroup : 0);
   const size_t pb = align256(size_t(c.count) * parts * 8);
   c.keeps_xt = muon::chunk_keeps_xt(c.S, c.L, ns_f32, K);
@@ -949,7 +949,7 @@ muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Pla
       b.partials = reinterpret_cast<double*>(ws + c.off_part);
       b.rscale = reinterpret_cast<double*>(ws + c.off_r);
       b.xscale = reinterpret_cast<float*>(b.rscale + c.count);
-      b.sync = muon::chunk_is_small(c.S, c.L, ns_f32) ? reinterpret_cast<unsigned*>(ws + c.off_sync) : nullptr;
+      b.sync = muon::chunk_is_small(c.s, c.l, ns_f32) ? reinterpret_cast<unsigned*>(ws + c.off_sync) : nullptr;
       const std::vector<float>& ct = tables[size_t(c.cset)];
       launch_err = muon::run_chunk(g, d_desc + c.first, b, sc, ct.data(), int(ct.size() / 3), cs,
                                    h->profiling ? &h->timer : nullptr);
@@ -1579,7 +1579,7 @@ muon_status_t ns_orthogonalize_batched_noalloc(muon_handle_t h, const void* cons
     b.partials = reinterpret_cast<double*>(ws + c.off_part);
     b.rscale = reinterpret_cast<double*>(ws + c.off_r);
     b.xscale = reinterpret_cast<float*>(b.rscale + c.count);
-    b.sync = muon::chunk_is_small(c.S, c.L, f32) ? reinterpret_cast<unsigned*>(ws + c.off_sync) : nullptr;
+    b.sync = muon::chunk_is_small(c.s, c.l, f32) ? reinterpret_cast<unsigned*>(ws + c.off_sync) : nullptr;
     if ((e = muon::run_chunk(g, d_desc + c.first, b, sc, ct, K, stream, nullptr)) != hipSuccess)
       return device_fail(h, "kernel launch", e);
   }

@@ -118,12 +118,18 @@ inline bool chunk_keeps_xt(int64_t S, int64_t L, bool ns_f32, int K) {
 }
 // A chunk runs as one fused launch (k_ns_small: momentum, norm, every
 // Newton-Schulz step and the update) when its short side is at most 128 and
-// its NS arithmetic is fp32; such a chunk also needs the group counters
-// (kSmallSyncBytes) and kSmallMaxGroup norm partials per matrix.
+// the fused launch is the faster one for its shape: always for fp32 NS; for
+// bf16 NS when the short side is at most 64 or the long side at most 512
+// (measured: 64 matrices of 128 x 2048 run twice as fast as 128 x 128 tiles,
+// whose operand units carry four times the flops per byte).  The choice
+// depends on the shape alone, so a matrix gets the same bits in any batch.
+// Such a chunk also needs the group counters (kSmallSyncBytes) and
+// kSmallMaxGroup norm partials per matrix.
 constexpr int kSmallMaxGroup = 32;
 constexpr int64_t kSmallSyncBytes = 64 * 1024;
-inline bool chunk_is_small(int64_t S, int64_t L, bool ns_f32) {
-  return ns_f32 && S == 128 && L <= (int64_t(1) << 16);
+inline bool chunk_is_small(int64_t s, int64_t l, bool ns_f32) {
+  if (s > 128 || l > (int64_t(1) << 16)) return false;
+  return ns_f32 || s <= 64 || l <= 512;
 }
 
 // ---------------------------------------------------------------------------

@@ -1755,8 +1755,19 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ int64_t ti(int r, int k, int kg) {
   return (static_cast<int64_t>(r >> 4) * kg + (k >> 4)) * 256 + (((k & 15) >> 2) * 16 + (r & 15)) * 4 + (k & 3);
 }
+// The bf16 form: 16-row x 32-k chunks of 1 KB (lane l: row l % 16,
+// k 8 (l / 16) .. + 7, the operand of v_mfma_f32_16x16x32_bf16), kg k-groups
+// of 32 per row, in elements.
+__device__ __forceinline__ int64_t ti_b(int r, int k, int kg) {
+  return (static_cast<int64_t>(r >> 4) * kg + (k >> 5)) * 512 + (((k & 31) >> 3) * 16 + (r & 15)) * 8 + (k & 7);
+}
+template <typename XT>
+__device__ __forceinline__ int64_t tix(int r, int k, int kg) {
+  if constexpr (sizeof(XT) == 2) return ti_b(r, k, kg);
+  else return ti(r, k, kg);
+}
 
-template <typename Unit, typename Pre, typename Epi>
+template <typename XT, typename Unit, typename Pre, typename Epi>
 __device__ __forceinline__ void small_units(int nunits, int kg, Unit&& unit, Pre&& pre, Epi&& epi) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int mine = nunits > wave ? (nunits - wave + 3) / 4 : 0;  // this wavefront's units
@@ -1801,10 +1812,15 @@ __device__ __forceinline__ void small_units(int nunits, int kg, Unit&& unit, Pre
 #pragma unroll
     for (int t = 0; t < kSmallBatch; ++t)
       if (g0 + t < kg) {
+        if constexpr (sizeof(XT) == 2) {
+          acc[t & 1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, bt.a[t]),
+                                                               __builtin_bit_cast(bf16x8_t, bt.b[t]), acc[t & 1], 0, 0, 0);
+        } else {
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[t & 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bt.a[t][j]), __uint_as_float(bt.b[t][j]),
-                                                            acc[t & 1], 0, 0, 0);
+          for (int j = 0; j < 4; ++j)
+            acc[t & 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bt.a[t][j]), __uint_as_float(bt.b[t][j]),
+                                                              acc[t & 1], 0, 0, 0);
+        }
       }
     if (bb == nbat - 1) {
       const int u = wave + 4 * (it / nbat);
@@ -1838,10 +1854,11 @@ __device__ __forceinline__ float get(const char* base, int64_t idx) {
   return to_f32<T>(__builtin_nontemporal_load(reinterpret_cast<const T*>(base) + idx));
 }
 
-// fp32 Newton-Schulz (the chunks this launch takes; see chunk_is_small).
-template <typename GT, bool MOM>
+// XT: float (fp32 Newton-Schulz, X exact u) or uint16_t (bf16: X, A and B
+// stored as bfloat16 between the products, fp32 accumulation).
+template <typename GT, typename XT, bool MOM>
 __global__ __launch_bounds__(256) void k_ns_small(SmallArgs sa) {
-  using XT = float;
+  constexpr int KG = sizeof(XT) == 2 ? 32 : 16;  // k per operand chunk
   __shared__ double red4[4];
   const int b = blockIdx.x, xcd = b & 7, slot = b >> 3;
   const int group = (slot / sa.G) * 8 + xcd, member = slot % sa.G;
@@ -1850,7 +1867,7 @@ __global__ __launch_bounds__(256) void k_ns_small(SmallArgs sa) {
   if (threadIdx.x == 0) __hip_atomic_store(sync + 2 + member, xcc_id(), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   unsigned nbar = 0;
   bool local = false;
-  const int kgx = sa.L / 16, kgs = sa.S / 16;      // k-groups per row of X, of X^T, A and B
+  const int kgx = sa.L / KG, kgs = sa.S / KG;      // k-groups per row of X, of X^T, A and B
   const int ncb = sa.Lx / 32;                                    // column blocks of X
   const int c0 = bj * ncb / sa.CB, c1 = (bj + 1) * ncb / sa.CB;  // this member's, in the prologue
   const int w = (c1 - c0) * 32;                                  // prologue columns of this member
@@ -1897,8 +1914,8 @@ __global__ __launch_bounds__(256) void k_ns_small(SmallArgs sa) {
         acc2 = fma(static_cast<double>(u), static_cast<double>(u), acc2);
         int xr, xc;
         coord(e0 + 256 * t, xr, xc);
-        put<XT>(X0, ti(xr, xc, kgx), u);
-        put<XT>(XT0, ti(xc, xr, kgs), u);
+        put<XT>(X0, tix<XT>(xr, xc, kgx), u);
+        put<XT>(XT0, tix<XT>(xc, xr, kgs), u);
       }
     }
     const double part = block_sum_256(acc2, red4);
@@ -1931,7 +1948,23 @@ __global__ __launch_bounds__(256) void k_ns_small(SmallArgs sa) {
       for (int t = 0; t < 8; ++t) {
         int xr, xc;
         coord(e0 + 256 * t, xr, xc);
-        v[t] = e0 + 256 * t < ne ? (get<XT>(X0, ti(xr, xc, kgx)) * s1) * s2 : 0.f;
+        float u = 0.f;
+        if (e0 + 256 * t < ne) {
+          if constexpr (sizeof(XT) == 4) {
+            u = get<XT>(X0, tix<XT>(xr, xc, kgx));  // u itself, exact
+          } else if (xr < sa.s && xc < sa.l) {
+            // X holds u rounded to bf16: form u again from g and the advanced
+            // momentum (this thread's own writes), so r u is rounded once
+            const int ur = tr ? xc : xr, uc = tr ? xr : xc;
+            const float gv = to_f32<GT>(g[view_index(md, ur, uc)]);
+            u = gv;
+            if (MOM) {
+              const float bn = md.buf[buf_index(md, ur, uc)];
+              u = sa.sc.nesterov ? fmaf(beta, bn, omb * gv) : bn;
+            }
+          }
+        }
+        v[t] = (u * s1) * s2;
       }
 #pragma unroll
       for (int t = 0; t < 8; ++t) {
@@ -1948,8 +1981,8 @@ __global__ __launch_bounds__(256) void k_ns_small(SmallArgs sa) {
               store_from_f32(md.out, pidx, sa.param_dtype, v[t]);
           }
         } else {
-          put<XT>(X0, ti(xr, xc, kgx), v[t]);
-          put<XT>(XT0, ti(xc, xr, kgs), v[t]);
+          put<XT>(X0, tix<XT>(xr, xc, kgx), v[t]);
+          put<XT>(XT0, tix<XT>(xc, xr, kgs), v[t]);
         }
       }
     }
@@ -1969,29 +2002,29 @@ __global__ __launch_bounds__(256) void k_ns_small(SmallArgs sa) {
       char* Bm = sa.B + m * sa.matA;
       // unit u of a phase over 32 x 32 blocks: block u / 4, quarter u % 4
       // A = X X^T: rows bi, column blocks bj, bj + CB, ..
-      small_units(
-          4 * na, sa.Lx / 16,
+      small_units<XT>(
+          4 * na, sa.Lx / KG,
           [&](int u, const char*& P, const char*& Q, int& row0, int& col0) {
             row0 = bi * 32 + 16 * ((u & 3) >> 1);
             col0 = (bj + (u >> 2) * sa.CB) * 32 + 16 * (u & 1);
-            P = Xc + ti(row0, 0, kgx) * 4;
-            Q = Xc + ti(col0, 0, kgx) * 4;
+            P = Xc + tix<XT>(row0, 0, kgx) * static_cast<int64_t>(sizeof(XT));
+            Q = Xc + tix<XT>(col0, 0, kgx) * static_cast<int64_t>(sizeof(XT));
           },
           [](int, int) { return 0.f; },
-          [&](int row, int col, float v, float) { put<XT>(Am, ti(row, col, kgs), sa_ * v); });
+          [&](int row, int col, float v, float) { put<XT>(Am, tix<XT>(row, col, kgs), sa_ * v); });
       ++nbar;
       group_barrier(sync, nbar * sa.G, local);
       // B = b A + c A A (A symmetric: column block c of A is row block c)
-      small_units(
-          4 * na, sa.Sx / 16,
+      small_units<XT>(
+          4 * na, sa.Sx / KG,
           [&](int u, const char*& P, const char*& Q, int& row0, int& col0) {
             row0 = bi * 32 + 16 * ((u & 3) >> 1);
             col0 = (bj + (u >> 2) * sa.CB) * 32 + 16 * (u & 1);
-            P = Am + ti(row0, 0, kgs) * 4;
-            Q = Am + ti(col0, 0, kgs) * 4;
+            P = Am + tix<XT>(row0, 0, kgs) * static_cast<int64_t>(sizeof(XT));
+            Q = Am + tix<XT>(col0, 0, kgs) * static_cast<int64_t>(sizeof(XT));
           },
-          [&](int row, int col) { return get<XT>(Am, ti(row, col, kgs)); },
-          [&](int row, int col, float v, float a_) { put<XT>(Bm, ti(row, col, kgs), fmaf(cb, a_, cc * v)); });
+          [&](int row, int col) { return get<XT>(Am, tix<XT>(row, col, kgs)); },
+          [&](int row, int col, float v, float a_) { put<XT>(Bm, tix<XT>(row, col, kgs), fmaf(cb, a_, cc * v)); });
       if (sa.CB > 1) {
         ++nbar;
         group_barrier(sync, nbar * sa.G, local);
@@ -2001,20 +2034,20 @@ __global__ __launch_bounds__(256) void k_ns_small(SmallArgs sa) {
       char* Xn = sa.X[cur ^ 1] + m * sa.matX;
       char* XTn = sa.XT[cur ^ 1] + m * sa.matX;
       const int nx = (ncb - bj + sa.CB - 1) / sa.CB;
-      small_units(
-          4 * nx, sa.Sx / 16,
+      small_units<XT>(
+          4 * nx, sa.Sx / KG,
           [&](int u, const char*& P, const char*& Q, int& row0, int& col0) {
             row0 = bi * 32 + 16 * ((u & 3) >> 1);
             col0 = (bj + (u >> 2) * sa.CB) * 32 + 16 * (u & 1);
-            P = Bm + ti(row0, 0, kgs) * 4;
-            Q = XTc + ti(col0, 0, kgs) * 4;
+            P = Bm + tix<XT>(row0, 0, kgs) * static_cast<int64_t>(sizeof(XT));
+            Q = XTc + tix<XT>(col0, 0, kgs) * static_cast<int64_t>(sizeof(XT));
           },
-          [&](int row, int col) { return get<XT>(Xc, ti(row, col, kgx)); },
+          [&](int row, int col) { return get<XT>(Xc, tix<XT>(row, col, kgx)); },
           [&](int xr, int xc, float v, float x_) {
             const float o = sx_ * fmaf(ca, x_, v);
             if (!last) {
-              put<XT>(Xn, ti(xr, xc, kgx), o);
-              put<XT>(XTn, ti(xc, xr, kgs), o);
+              put<XT>(Xn, tix<XT>(xr, xc, kgx), o);
+              put<XT>(XTn, tix<XT>(xc, xr, kgs), o);
             } else if (xr < sa.s && xc < sa.l) {
               const int64_t pidx = view_index(md, tr ? xc : xr, tr ? xr : xc);
               if (sa.sc.final_kind == 0)
@@ -2068,16 +2101,15 @@ hipError_t run_small(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBuff
   sa.partials = wb.partials;
   sa.sync = wb.sync;
   for (int i = 0; i < 3 * K; ++i) sa.coeffs[i] = coeffs[i];
-  if constexpr (!std::is_same<XT, float>::value) return hipErrorInvalidValue;  // fp32 NS only
   Timed tm(timer, KK_SMALL, st);
   hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(256), 0, st, wb.sync, sa.groups * 64);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const dim3 grid(static_cast<unsigned>(sa.groups * sa.G));
   if (sc.momentum)
-    hipLaunchKernelGGL((k_ns_small<GT, true>), grid, dim3(256), 0, st, sa);
+    hipLaunchKernelGGL((k_ns_small<GT, XT, true>), grid, dim3(256), 0, st, sa);
   else
-    hipLaunchKernelGGL((k_ns_small<GT, false>), grid, dim3(256), 0, st, sa);
+    hipLaunchKernelGGL((k_ns_small<GT, XT, false>), grid, dim3(256), 0, st, sa);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const double nm = cg.nmat, s = cg.s, l = cg.l, Sx = sa.Sx, Lx = sa.Lx;
   const double gsz = sizeof(GT), psz = cg.param_dtype == DT_BF16 ? 2.0 : 4.0;

@@ -411,14 +411,22 @@ def test_plan_padding_and_workspace_bytes(lib):
     assert st == 0
     c, = chunks
     assert (c["s"], c["l"], c["s_pad"], c["l_pad"], c["count"]) == (17, 33, 128, 128, 2)
-    # 4 X buffers + A + B (bf16) + norm partials + 1/(norm+eps)
+    # a short side of at most 64 runs as one fused launch in bf16 too: 4 X
+    # buffers + A + B (bf16), norm partials for up to 32 workgroups per
+    # matrix, 1/(norm+eps), and 64 KiB of group counters
     xb = 2 * 128 * 128 * 2
-    assert c["workspace_bytes"] == 6 * xb + 256 + 256 and ws == c["workspace_bytes"]
-    # fp32 NS with a short side of at most 128 runs as one fused launch: the
-    # same buffers, norm partials for up to 32 workgroups per matrix, and 64 KiB
-    # of group counters
+    assert c["workspace_bytes"] == 6 * xb + 512 + 256 + 65536 and ws == c["workspace_bytes"]
+    # fp32 NS: the same with fp32 buffers
     st, chunks32, ws32, _ = B.plan_step(entries([(17, 33), (33, 17)]), hp(ns_precision="f32"))
     assert ws32 == 6 * 2 * xb + 512 + 256 + 65536
+    # bf16 on the tile kernels (150 x 200 pads to 256 x 256): two X buffers
+    # (no X^T: the update reads X through transposing LDS reads), A, B, one
+    # norm partial per 64 x 64 tile, 1/(norm+eps)
+    st, chunks_t, ws_t, _ = B.plan_step(entries([(150, 200), (200, 150)]), hp())
+    c, = chunks_t
+    assert (c["s_pad"], c["l_pad"], c["count"]) == (256, 256, 2)
+    xb = 2 * 256 * 256 * 2
+    assert ws_t == 4 * xb + 256 + 256
 
 
 def test_plan_keeps_no_transpose_where_the_tile_kernel_reads_x(lib):

@@ -285,16 +285,18 @@ def test_tiny_and_scaled_inputs(muon):
         assert rel(to_host(o), want) <= 1e-4
 
 
+@pytest.mark.parametrize("shape", [(48, 80), (160, 600)])
 @pytest.mark.parametrize("prec", ["f32", "bf16"])
-def test_norms_outside_the_folded_range(muon, prec):
+def test_norms_outside_the_folded_range(muon, prec, shape):
     # The first Newton-Schulz step applies r = 1/(||u|| + eps) to products of
     # u itself while r lies in [2^-40, 2^40]; beyond that X0 = r*u is written
     # out first.  Power-of-two scales keep the inputs exact in both dtypes:
     # ||u|| ~ 2^-44, 2^56, 2^76 (u^2 past the binary32 range: the norm sums
     # run in fp64) and 2^127 (r below the normal binary32 range: applied as
-    # two factors).  eps = 0 makes the result scale-invariant.
+    # two factors).  eps = 0 makes the result scale-invariant.  48 x 80 runs
+    # on the fused small-matrix launch, 160 x 600 on the tile kernels.
     import torch
-    base = gen((48, 80), 1.0, "f32", 28, 0)
+    base = gen(shape, 1.0, "f32", 28, 0)
     base /= np.float32(np.abs(base).max())   # |entries| <= 1, so 2^126 x base stays finite
     if prec == "bf16":
         base = decode(synth.f32_to_bf16_bits(base), "bf16").astype(np.float32)
@@ -307,12 +309,12 @@ def test_norms_outside_the_folded_range(muon, prec):
     torch.cuda.synchronize()
     for sc, o in zip(scales, outs):
         err = rel(to_host(o), want)
-        print(f"norm scale 2^{int(np.log2(sc))} {prec}: O err {err:.3e}", flush=True)
+        print(f"norm scale 2^{int(np.log2(sc))} {prec} {shape}: O err {err:.3e}", flush=True)
         assert err <= TOL[prec], sc
     # the same through muon_step: zero momentum, beta = 0, no decay, lr = 1
     # and no rescale, so W' = W - O
-    Ws = [torch.zeros(48, 80, dtype=dt, device="cuda") for _ in scales]
-    Ms = [torch.zeros(48, 80, dtype=torch.float32, device="cuda") for _ in scales]
+    Ws = [torch.zeros(*shape, dtype=dt, device="cuda") for _ in scales]
+    Ms = [torch.zeros(*shape, dtype=torch.float32, device="cuda") for _ in scales]
     muon.step(Ws, ins, Ms, lr=1.0, beta=0.0, weight_decay=0.0, eps=0.0, ns_precision=prec, scale_mode=1)
     torch.cuda.synchronize()
     for sc, w in zip(scales, Ws):
