@@ -66,6 +66,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--streams", type=int, default=2, choices=(1, 2),
                     help="library chunk concurrency in the timed region (muon_set_streams)")
+    ap.add_argument("--grouping", type=int, default=1, choices=(0, 1),
+                    help="grouped launches for chunks that leave CUs idle (muon_set_grouping)")
     ap.add_argument("--no-side", action="store_true",
                     help="skip the views and AdamW side measurements (counter runs)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -340,6 +342,7 @@ def main():
 
     muon = Muon(0)
     muon.set_streams(args.streams)
+    muon.set_grouping(bool(args.grouping))
     if wl.orthogonalize_only:
         ohp = dict(ns_steps=wl.ns_steps, ns_precision=wl.ns_precision)
         run_step = lambda: muon.orthogonalize(G, outs, **ohp)
@@ -451,6 +454,7 @@ def main():
         "ns_pct_peak": 100.0 * ns_flops / (ms * 1e-3) / 1e12 / peak,
         "ns_gemm": ns_gemm,
         "streams": args.streams,
+        "grouping": args.grouping,
         "serial_ms_per_step": serial_ms if serial_ms is not None else ms,
         "roofline": roof,
         "kernels": kernels,

@@ -176,6 +176,19 @@ muon_status_t muon_destroy(muon_handle_t h);
  * streams: 2 (the default) or 1 (everything on the caller's stream). */
 muon_status_t muon_set_streams(muon_handle_t h, int streams);
 
+/* Grouped launches (Sec. 6.6, one batched launch per group of shapes), for
+ * calls that run on one stream (muon_set_streams(h, 1)): the chunks of a
+ * call that leave compute units idle (as above), run their Newton-Schulz
+ * products on the 256 x 256 tile kernels (bf16 NS, padded extents multiples
+ * of 256) and share the step count and parameter dtype are run together,
+ * up to 8 at a time: per step, one launch per product over the tiles of all
+ * of them.  With two streams such chunks overlap on the streams instead.
+ * Each member keeps its own workspace region, so the call's workspace can
+ * exceed what muon_plan_step reports by the sum of those chunks' sizes
+ * (never beyond the workspace limit: then the chunks run one by one).
+ * Results are bitwise the same either way.  enable: 1 (the default) or 0. */
+muon_status_t muon_set_grouping(muon_handle_t h, int enable);
+
 /* Grows the workspace to at least `bytes` now (hipMalloc synchronises, so do
  * this before timing).  Fails with MUON_ERR_OUT_OF_MEMORY above the limit. */
 muon_status_t muon_reserve(muon_handle_t h, size_t bytes);

@@ -113,6 +113,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.muon_adamw_step.argtypes = [vp, ctypes.POINTER(AdamWParam), i64, ctypes.POINTER(AdamWHParams), vp]
     lib.muon_profile_enable.argtypes = [vp, ctypes.c_int]
     lib.muon_set_streams.argtypes = [vp, ctypes.c_int]
+    lib.muon_set_grouping.argtypes = [vp, ctypes.c_int]
     lib.muon_stream_copy.argtypes = [vp, vp, vp, ctypes.c_size_t, vp]
     lib.muon_profile_read.argtypes = [vp, ctypes.POINTER(MuonKernelStats), ctypes.c_int,
                                       ctypes.POINTER(ctypes.c_int), ctypes.c_int]
@@ -305,6 +306,11 @@ class Muon:
     def set_streams(self, n: int):
         """2 (default): chunks that leave CUs idle run on a second stream; 1: off."""
         self._check(self.lib.muon_set_streams(self.h, int(n)))
+
+    def set_grouping(self, enable: bool):
+        """muon_set_grouping: chunks that leave compute units idle share one
+        launch per product and step (default on)."""
+        self._check(self.lib.muon_set_grouping(self.h, 1 if enable else 0))
 
     def set_workspace_limit(self, nbytes: int):
         self._check(self.lib.muon_set_workspace_limit(self.h, int(nbytes)))

@@ -104,6 +104,9 @@ struct muon_handle {
   // a second stream with their own workspace slot, forked from and joined
   // back into the caller's stream through events.
   int nstreams = 2;
+  // Grouped launches (muon_set_grouping): chunks that leave CUs idle and can
+  // share a launch run each product of each step as one launch.
+  int grouping = 1;
   hipStream_t side = nullptr;
   hipEvent_t fork = nullptr, join = nullptr;
   bool log = false;                  // MUON_HIP_LOG set (and not "0"): each call's plan on stderr
@@ -790,6 +793,7 @@ void key_coeffs(std::vector<char>& k, const float* c, int32_t steps) {
 
 void key_settings(std::vector<char>& k, const muon_handle* h) {
   key_append(k, &h->nstreams, sizeof h->nstreams);
+  key_append(k, &h->grouping, sizeof h->grouping);
   key_append(k, &h->ws_limit, sizeof h->ws_limit);
 }
 
@@ -865,53 +869,135 @@ muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Pla
                       const CoeffTables& tables, hipStream_t stream) {
   DeviceGuard dg(h->device);
   if (!dg.ok) { set_err(h, "cannot select device %d", h->device); return MUON_ERR_DEVICE; }
-  // Which chunks run on the second stream: those whose Gram launch leaves
-  // CUs idle in its last round (occupancy below 0.9) alternate between the
-  // streams, so one chunk's idle CUs take the other's work; chunks that fill
+  // Units of work, in plan order: one chunk, or a group of chunks whose
+  // products run as one launch per product and step (muon::run_group):
+  // chunks whose Gram launch leaves CUs idle in its last round (occupancy
+  // below 0.9), that can share the 256 x 256 kernel, with the same step
+  // count and parameter dtype, at most kGroupMax to a group.  A group's
+  // members each keep their own workspace region.  Groups are formed when
+  // the call runs on one stream: with two, such chunks overlap on the two
+  // streams instead, which measured faster (one block, hidden 2048: 2.17
+  // against 2.36 ms per step; its two chunks' Gram products differ in K, and
+  // a grouped round waits for the longest tile, where a chunk on its own
+  // stream moves on to its next product).  On one stream, groups measured
+  // 2.51 against 2.95 ms.
+  const bool concurrent = h->nstreams > 1 && h->side != nullptr;
+  int cus = 256;
+  (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device);
+  auto geom_of = [&](const Chunk& c) {
+    ChunkGeom g{};
+    g.s = int32_t(c.s); g.l = int32_t(c.l); g.S = int32_t(c.S); g.L = int32_t(c.L);
+    g.nmat = int32_t(c.count);
+    g.ns_f32 = ns_f32 ? 1 : 0;
+    g.grad_dtype = c.gdt == MUON_BF16 ? muon::DT_BF16 : muon::DT_F32;
+    g.param_dtype = c.pdt == MUON_BF16 ? muon::DT_BF16 : muon::DT_F32;
+    return g;
+  };
+  auto steps_of = [&](const Chunk& c) { return int(tables[size_t(c.cset)].size() / 3); };
+  auto idle_of = [&](const Chunk& c) {
+    const bool tile = !ns_f32 && c.S % 256 == 0;
+    const int64_t t = tile ? c.S / 256 : c.S / 128;
+    const int64_t tiles = t * (t + 1) / 2 * c.count, slots = int64_t(tile ? cus : 2 * cus);
+    return double(tiles) / double(((tiles + slots - 1) / slots) * slots) < 0.9;
+  };
+  struct Unit {
+    std::vector<size_t> members;  // chunk indices, plan order
+    std::vector<size_t> off;      // each member's workspace offset inside the unit's region
+    size_t bytes = 0;
+    bool idle = false;
+  };
+  const size_t nch = plan.chunks.size();
+  std::vector<Unit> units;
+  std::vector<char> on_side;
+  bool two = false;
+  size_t slot = 0, need = 0;
+  // (a second pass without groups when the groups' regions would pass the
+  // workspace limit)
+  for (int pass = 0; pass < 2; ++pass) {
+  const bool allow_groups = h->grouping && !concurrent && pass == 0;
+  units.clear();
+  std::vector<char> grouped(nch, 0);
+  if (allow_groups) {
+    std::map<std::pair<int, int32_t>, size_t> open;  // (steps, param dtype) -> unit with room
+    for (size_t ci = 0; ci < nch; ++ci) {
+      const Chunk& c = plan.chunks[ci];
+      if (!idle_of(c) || !muon::group_eligible(geom_of(c), steps_of(c))) continue;
+      const std::pair<int, int32_t> key{steps_of(c), c.pdt};
+      auto it = open.find(key);
+      if (it == open.end() || units[it->second].members.size() >= size_t(muon::kGroupMax)) {
+        units.emplace_back();
+        open[key] = units.size() - 1;
+        it = open.find(key);
+      }
+      units[it->second].members.push_back(ci);
+      grouped[ci] = 1;
+    }
+    // a group of one is a plain chunk
+    for (Unit& u : units)
+      if (u.members.size() == 1) grouped[u.members[0]] = 0;
+    units.erase(std::remove_if(units.begin(), units.end(), [](const Unit& u) { return u.members.size() < 2; }),
+                units.end());
+  }
+  for (size_t ci = 0; ci < nch; ++ci)
+    if (!grouped[ci]) {
+      units.emplace_back();
+      units.back().members.push_back(ci);
+    }
+  std::sort(units.begin(), units.end(), [](const Unit& a, const Unit& b) { return a.members[0] < b.members[0]; });
+  for (Unit& u : units) {
+    for (size_t ci : u.members) {
+      u.off.push_back(u.bytes);
+      u.bytes += align256(plan.chunks[ci].bytes);
+    }
+    u.idle = u.members.size() > 1 || idle_of(plan.chunks[u.members[0]]);
+  }
+  // Which units run on the second stream: idle ones alternate between the
+  // streams, so one unit's idle CUs take the other's work; units that fill
   // every round stay on the caller's stream (two such kernels side by side
   // share the XCDs' L2 less well: measured slower).  The second slot of
   // workspace is used only when it fits under the workspace limit.
-  std::vector<char> on_side(plan.chunks.size(), 0);
-  bool two = false;
-  if (h->nstreams > 1 && h->side && plan.chunks.size() > 1) {
-    int cus = 256;
-    (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device);
+  on_side.assign(units.size(), 0);
+  two = false;
+  if (h->nstreams > 1 && h->side && units.size() > 1) {
     int low = 0;
-    for (size_t ci = 0; ci < plan.chunks.size(); ++ci) {
-      const Chunk& c = plan.chunks[ci];
-      const bool tile = !ns_f32 && c.S % 256 == 0;
-      const int64_t t = tile ? c.S / 256 : c.S / 128;
-      const int64_t tiles = t * (t + 1) / 2 * c.count, slots = int64_t(tile ? cus : 2 * cus);
-      const double occ = double(tiles) / double(((tiles + slots - 1) / slots) * slots);
-      if (occ < 0.9) on_side[ci] = (low++ % 2 == 0);
-      two = two || on_side[ci];
+    for (size_t ui = 0; ui < units.size(); ++ui) {
+      if (units[ui].idle) on_side[ui] = (low++ % 2 == 0);
+      two = two || on_side[ui];
     }
   }
-  // each slot sized for the chunks that run on its stream
+  // each slot sized for the units that run on its stream
   size_t main_bytes = 0, side_bytes = 0;
-  for (size_t ci = 0; ci < plan.chunks.size(); ++ci)
-    (on_side[ci] ? side_bytes : main_bytes) = std::max(on_side[ci] ? side_bytes : main_bytes,
-                                                       plan.chunks[ci].bytes);
-  const size_t slot = align256(main_bytes);
+  for (size_t ui = 0; ui < units.size(); ++ui)
+    (on_side[ui] ? side_bytes : main_bytes) = std::max(on_side[ui] ? side_bytes : main_bytes, units[ui].bytes);
+  slot = align256(main_bytes);
   if (two && h->ws_limit && slot + side_bytes > h->ws_limit) {
     two = false;
     std::fill(on_side.begin(), on_side.end(), 0);
   }
-  muon_status_t st = ensure_workspace(h, two ? slot + side_bytes : plan.ws_bytes);
+  if (!two && main_bytes < side_bytes) main_bytes = side_bytes;
+  need = two ? slot + side_bytes : main_bytes;
+  const bool any_group = std::any_of(units.begin(), units.end(), [](const Unit& u) { return u.members.size() > 1; });
+  if (!(any_group && h->ws_limit && need > h->ws_limit)) break;
+  }
+  muon_status_t st = ensure_workspace(h, need);
   if (st != MUON_OK) return st;
   if (h->log) {
-    std::fprintf(stderr, "muon: %zu matrices in %zu chunks, %s NS, %s, workspace %zu bytes\n",
-                 plan.order.size(), plan.chunks.size(), ns_f32 ? "fp32" : "bf16",
+    std::fprintf(stderr, "muon: %zu matrices in %zu chunks (%zu units), %s NS, %s, workspace %zu bytes\n",
+                 plan.order.size(), plan.chunks.size(), units.size(), ns_f32 ? "fp32" : "bf16",
                  two ? "two streams" : "one stream", h->ws_bytes);
-    for (size_t ci = 0; ci < plan.chunks.size(); ++ci) {
-      const Chunk& c = plan.chunks[ci];
-      std::fprintf(stderr,
-                   "muon:   chunk %zu: %lld matrices of %lld x %lld (padded %lld x %lld), K = %zu, "
-                   "coefficient set %d, X^T %s, %s stream, %zu workspace bytes\n",
-                   ci, (long long)c.count, (long long)c.s, (long long)c.l, (long long)c.S, (long long)c.L,
-                   tables[size_t(c.cset)].size() / 3, int(c.cset), c.keeps_xt ? "kept" : "not kept",
-                   on_side[ci] ? "second" : "caller's", c.bytes);
-    }
+    for (size_t ui = 0; ui < units.size(); ++ui)
+      for (size_t mi = 0; mi < units[ui].members.size(); ++mi) {
+        const size_t ci = units[ui].members[mi];
+        const Chunk& c = plan.chunks[ci];
+        std::fprintf(stderr,
+                     "muon:   chunk %zu: %lld matrices of %lld x %lld (padded %lld x %lld), K = %zu, "
+                     "coefficient set %d, X^T %s, %s stream, %zu workspace bytes%s\n",
+                     ci, (long long)c.count, (long long)c.s, (long long)c.l, (long long)c.S, (long long)c.L,
+                     tables[size_t(c.cset)].size() / 3, int(c.cset), c.keeps_xt ? "kept" : "not kept",
+                     on_side[ui] ? "second" : "caller's", c.bytes,
+                     units[ui].members.size() > 1 ? (mi == 0 ? ", grouped launches (first of the group)"
+                                                            : ", grouped launches") : "");
+      }
   }
   if ((st = begin_call(h, stream)) != MUON_OK) return st;
   // From here every exit records call_done, so that later calls wait for
@@ -930,29 +1016,32 @@ muon_status_t execute(muon_handle_t h, const std::vector<Item>& items, const Pla
       if (e != hipSuccess) return device_fail(h, "fork", e);
     }
     hipError_t launch_err = hipSuccess;
-    for (size_t ci = 0; ci < plan.chunks.size() && launch_err == hipSuccess; ++ci) {
-      const Chunk& c = plan.chunks[ci];
-      const bool odd = on_side[ci] != 0;
-      char* ws = static_cast<char*>(h->ws) + (odd ? slot : 0);
+    for (size_t ui = 0; ui < units.size() && launch_err == hipSuccess; ++ui) {
+      const Unit& u = units[ui];
+      const bool odd = on_side[ui] != 0;
+      char* const base = static_cast<char*>(h->ws) + (odd ? slot : 0);
       const hipStream_t cs = odd ? h->side : s;
-      ChunkGeom g{};
-      g.s = int32_t(c.s); g.l = int32_t(c.l); g.S = int32_t(c.S); g.L = int32_t(c.L);
-      g.nmat = int32_t(c.count);
-      g.ns_f32 = ns_f32 ? 1 : 0;
-      g.grad_dtype = c.gdt == MUON_BF16 ? muon::DT_BF16 : muon::DT_F32;
-      g.param_dtype = c.pdt == MUON_BF16 ? muon::DT_BF16 : muon::DT_F32;
-      ChunkBuffers b{};
-      b.X[0] = ws + c.off_X[0]; b.X[1] = ws + c.off_X[1];
-      b.XT[0] = c.keeps_xt ? ws + c.off_XT[0] : nullptr;
-      b.XT[1] = c.keeps_xt ? ws + c.off_XT[1] : nullptr;
-      b.A = ws + c.off_A; b.B = ws + c.off_B;
-      b.partials = reinterpret_cast<double*>(ws + c.off_part);
-      b.rscale = reinterpret_cast<double*>(ws + c.off_r);
-      b.xscale = reinterpret_cast<float*>(b.rscale + c.count);
-      b.sync = muon::chunk_is_small(c.s, c.l, ns_f32) ? reinterpret_cast<unsigned*>(ws + c.off_sync) : nullptr;
-      const std::vector<float>& ct = tables[size_t(c.cset)];
-      launch_err = muon::run_chunk(g, d_desc + c.first, b, sc, ct.data(), int(ct.size() / 3), cs,
-                                   h->profiling ? &h->timer : nullptr);
+      muon::GroupMember gm[muon::kGroupMax];
+      for (size_t mi = 0; mi < u.members.size(); ++mi) {
+        const Chunk& c = plan.chunks[u.members[mi]];
+        char* const ws = base + u.off[mi];
+        ChunkBuffers b{};
+        b.X[0] = ws + c.off_X[0]; b.X[1] = ws + c.off_X[1];
+        b.XT[0] = c.keeps_xt ? ws + c.off_XT[0] : nullptr;
+        b.XT[1] = c.keeps_xt ? ws + c.off_XT[1] : nullptr;
+        b.A = ws + c.off_A; b.B = ws + c.off_B;
+        b.partials = reinterpret_cast<double*>(ws + c.off_part);
+        b.rscale = reinterpret_cast<double*>(ws + c.off_r);
+        b.xscale = reinterpret_cast<float*>(b.rscale + c.count);
+        b.sync = muon::chunk_is_small(c.s, c.l, ns_f32) ? reinterpret_cast<unsigned*>(ws + c.off_sync) : nullptr;
+        gm[mi] = muon::GroupMember{geom_of(c), d_desc + c.first, b, tables[size_t(c.cset)].data()};
+      }
+      muon::LaunchTimer* const tmr = h->profiling ? &h->timer : nullptr;
+      const int K = steps_of(plan.chunks[u.members[0]]);
+      if (u.members.size() == 1)
+        launch_err = muon::run_chunk(gm[0].geom, gm[0].desc, gm[0].wb, sc, gm[0].coeffs, K, cs, tmr);
+      else
+        launch_err = muon::run_group(gm, int(u.members.size()), sc, K, cs, tmr);
     }
     if (two) {  // joined even after a failed launch, so later calls stay ordered
       hipError_t e = hipEventRecord(h->join, h->side);
@@ -1203,6 +1292,12 @@ muon_status_t muon_set_streams(muon_handle_t h, int streams) {
     return MUON_ERR_DEVICE;
   }
   h->nstreams = streams;
+  return MUON_OK;
+}
+
+muon_status_t muon_set_grouping(muon_handle_t h, int enable) {
+  if (!h || (enable != 0 && enable != 1)) return MUON_ERR_INVALID_ARGUMENT;
+  h->grouping = enable;
   return MUON_OK;
 }
 

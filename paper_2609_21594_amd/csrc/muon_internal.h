@@ -132,6 +132,24 @@ inline bool chunk_is_small(int64_t s, int64_t l, bool ns_f32) {
   return ns_f32 || s <= 64 || l <= 512;
 }
 
+// A group: chunks whose products of each Newton-Schulz step run as one
+// launch per product (the 256 x 256 kernel over all their tiles).  Each
+// member has its own workspace; they share the step count, the NS precision
+// (bf16) and the parameter dtype.
+struct GroupMember {
+  ChunkGeom geom;
+  const MatDesc* desc;
+  ChunkBuffers wb;
+  const float* coeffs;  // host, K x 3
+};
+constexpr int kGroupMax = 8;
+// A chunk can join a group: bf16 NS on the 256 x 256 kernels (padded
+// extents multiples of 256, rows within its offsets), at least one step,
+// not a fused small-matrix chunk.
+bool group_eligible(const ChunkGeom& g, int K);
+hipError_t run_group(const GroupMember* members, int n, const StepScalars& sc, int K, hipStream_t stream,
+                     LaunchTimer* timer);
+
 // ---------------------------------------------------------------------------
 // AdamW for the parameters Muon does not take (1-D and scalar ones; Sec. 6.4
 // delegates them to AdamW through a chained optimizer).

@@ -1530,6 +1530,39 @@ void k_gemm_tile(GemmArgs ga) {
   }
 }
 
+// One launch over the tiles of several chunks (a group): the product of
+// the same Newton-Schulz step for every chunk, each with its own arguments.
+// Tiles are numbered chunk by chunk (start[c] is chunk c's first), and the
+// rounds run as in k_gemm_tile, so a tile of one chunk and a tile of the
+// next can share a round.  Each tile's arithmetic is that of k_gemm_tile.
+constexpr int kMaxGroup = 8;
+struct GroupArgs {
+  GemmArgs ga[kMaxGroup];
+  int32_t start[kMaxGroup + 1];
+  int32_t n;
+};
+static_assert(sizeof(GroupArgs) <= 4096, "kernel argument size");
+
+template <int EPI, class Cfg>
+__global__ __launch_bounds__(64 * Cfg::NW) __attribute__((amdgpu_waves_per_eu(Cfg::WPE, Cfg::WPE)))
+void k_gemm_group(GroupArgs gr) {
+  constexpr int STAGED_C = Cfg::BM * Cfg::BN * 2, STAGED_T = Cfg::BN * (Cfg::BM * 2 + 8);
+  constexpr int STAGED = STAGED_C > STAGED_T ? STAGED_C : STAGED_T;
+  __shared__ __attribute__((aligned(1024))) char smem[Cfg::LDS > STAGED ? Cfg::LDS : STAGED];
+  const int G = static_cast<int>(gridDim.x), b = static_cast<int>(blockIdx.x);
+  const int total = gr.start[gr.n];
+  for (int r = 0;; ++r) {
+    const int logical = (G % 8 == 0) ? r * G + (b & 7) * (G / 8) + (b >> 3) : r * G + b;
+    if (logical >= total) break;
+    int c = 0;
+    while (c + 1 < gr.n && logical >= gr.start[c + 1]) ++c;
+    const GemmArgs& ga = gr.ga[c];
+    int mat, bm, bn;
+    tile_from_logical(ga, logical - gr.start[c], mat, bm, bn);
+    gemm_tile_body<EPI, Cfg>(ga, smem, mat, bm, bn);
+  }
+}
+
 // Update from X0 when K = 0: O is X0 in the caller's layout (the direct
 // buffer), one thread per element of the u-domain; grid = (ceil(rows*cols /
 // 256), matrices).
@@ -1604,6 +1637,51 @@ hipError_t launch_tile(int epi, GemmArgs ga, int nmat, hipStream_t st) {
       else if (!o) hipLaunchKernelGGL((k_gemm_tile<EPI_FINAL_W_F32, Cfg>), grid, block, 0, st, ga);
       else if (!f32) hipLaunchKernelGGL((k_gemm_tile<EPI_FINAL_O_BF16, Cfg>), grid, block, 0, st, ga);
       else hipLaunchKernelGGL((k_gemm_tile<EPI_FINAL_O_F32, Cfg>), grid, block, 0, st, ga);
+      break;
+    }
+  }
+  return hipGetLastError();
+}
+
+// The products of one step for a group of chunks on the 256 x 256 kernel:
+// each chunk's arguments prepared as launch_tile prepares them, one
+// persistent launch over all their tiles.  The chunks share the product, the
+// final kind and the parameter dtype.
+template <class Cfg>
+hipError_t launch_group(int epi, const GemmArgs* gas, const int* nmats, int n, hipStream_t st) {
+  if (n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
+  GroupArgs gr{};
+  gr.n = n;
+  gr.start[0] = 0;
+  for (int c = 0; c < n; ++c) {
+    GemmArgs ga = gas[c];
+    ga.tiles_m = ga.tiles_m * kTile / Cfg::BM;
+    ga.tiles_n = ga.tiles_n * kTile / Cfg::BN;
+    ga.tiles_per_mat = ga.syrk ? ga.tiles_m * (ga.tiles_m + 1) / 2 : ga.tiles_m * ga.tiles_n;
+    ga.k_slabs = ga.k_slabs * 128 / Cfg::SLAB;
+    ga.total_tiles = ga.tiles_per_mat * nmats[c];
+    if (epi == EPI_POLY && ga.beta != 0.f) {
+      ga.e_loop = 1;
+      ga.alpha = ga.alpha / ga.beta;
+    }
+    if (c > 0 && (ga.final_kind != gr.ga[0].final_kind || ga.param_dtype != gr.ga[0].param_dtype))
+      return hipErrorInvalidValue;
+    gr.ga[c] = ga;
+    gr.start[c + 1] = gr.start[c] + ga.total_tiles;
+  }
+  const int total = gr.start[n];
+  const int slots = device_cu_count() * (160 * 1024 / Cfg::LDS);
+  const dim3 grid(static_cast<unsigned>(min(total, slots))), block(64 * Cfg::NW);
+  switch (epi) {
+    case EPI_GRAM: hipLaunchKernelGGL((k_gemm_group<EPI_GRAM, Cfg>), grid, block, 0, st, gr); break;
+    case EPI_POLY: hipLaunchKernelGGL((k_gemm_group<EPI_POLY, Cfg>), grid, block, 0, st, gr); break;
+    case EPI_UPDATE: hipLaunchKernelGGL((k_gemm_group<EPI_UPDATE, Cfg>), grid, block, 0, st, gr); break;
+    default: {
+      const bool o = gr.ga[0].final_kind != 0, f32 = gr.ga[0].param_dtype == DT_F32;
+      if (!o && !f32) hipLaunchKernelGGL((k_gemm_group<EPI_FINAL_W_BF16, Cfg>), grid, block, 0, st, gr);
+      else if (!o) hipLaunchKernelGGL((k_gemm_group<EPI_FINAL_W_F32, Cfg>), grid, block, 0, st, gr);
+      else if (!f32) hipLaunchKernelGGL((k_gemm_group<EPI_FINAL_O_BF16, Cfg>), grid, block, 0, st, gr);
+      else hipLaunchKernelGGL((k_gemm_group<EPI_FINAL_O_F32, Cfg>), grid, block, 0, st, gr);
       break;
     }
   }
@@ -2119,15 +2197,13 @@ hipError_t run_small(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBuff
 }
 
 template <typename GT, typename XT>
-hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBuffers& wb,
+hipError_t run_prologue_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBuffers& wb,
                        const StepScalars& sc, const float* coeffs, int K, hipStream_t st,
                        LaunchTimer* timer) {
-  if (wb.sync) return run_small<GT, XT>(cg, d_desc, wb, sc, coeffs, K, st, timer);
   const int nmat = cg.nmat;
   const double nm = nmat;
   const int64_t numel = static_cast<int64_t>(cg.s) * cg.l;
   const double ne = double(numel);
-  const double s = cg.s, l = cg.l;
   const int nparts = static_cast<int>(norm_tiles(cg.S, cg.L));
   const double gsz = sizeof(GT), xsz = sizeof(XT);
   const double psz = cg.param_dtype == DT_BF16 ? 2.0 : 4.0;
@@ -2179,7 +2255,26 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
     tm.done(0, 0, nm * ne * (xsz + (sc.final_kind == 0 ? 2.0 * psz : psz)));
     return hipSuccess;
   }
+  return hipSuccess;
+}
 
+// The three products of Newton-Schulz step k of a chunk (after the
+// prologue): their launch arguments and work accounting.  `cur` selects the
+// iterate the step reads.
+struct StepProducts {
+  GemmArgs gram, poly, upd;
+  bool last;              // upd is the last step's product (parameter update or O)
+  double f[3], x[3], b[3];  // dense flops, executed flops, bytes of gram, poly, upd
+};
+
+template <typename XT>
+StepProducts step_products(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBuffers& wb,
+                           const StepScalars& sc, const float* coeffs, int K, int k, int cur) {
+  const bool qtr = !chunk_keeps_xt(cg.S, cg.L, sizeof(XT) == 4, K);
+  const double nm = cg.nmat;
+  const double s = cg.s, l = cg.l;
+  const double xsz = sizeof(XT);
+  const double psz = cg.param_dtype == DT_BF16 ? 2.0 : 4.0;
   const int es = static_cast<int>(sizeof(XT));
   const int64_t matX = static_cast<int64_t>(cg.S) * cg.L * es;
   const int64_t matA = static_cast<int64_t>(cg.S) * cg.S * es;
@@ -2197,81 +2292,99 @@ hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBu
   const double gram_frac = upper_frac(tile_sym && tile_rows_fit(cg.S, cg.L, es));
   const double poly_frac = upper_frac(tile_sym && tile_rows_fit(cg.S, cg.S, es));
   const double Sp = cg.S, Lp = cg.L;
+  StepProducts r{};
+  const float a = coeffs[3 * k], b = coeffs[3 * k + 1], c = coeffs[3 * k + 2];
+  const char* X = static_cast<const char*>(wb.X[cur]);
+  const char* XTc = static_cast<const char*>(wb.XT[cur]);
+  // A = X X^T: M = N = S, K = L.
+  GemmArgs& g = r.gram;
+  g.P = X; g.p_mat = matX; g.ldp = cg.L * es;
+  g.Q = X; g.q_mat = matX; g.ldq = cg.L * es;
+  g.k_slabs = cg.L * es / 128;
+  g.tiles_m = ts; g.tiles_n = ts; g.syrk = 1; g.tiles_per_mat = ts * (ts + 1) / 2;
+  g.C = static_cast<char*>(wb.A); g.c_mat = matA; g.ldc = cg.S * es;
+  g.xscale = k == 0 ? wb.xscale : nullptr;  // A0 = r^2 X~ X~^T
+  // Under qtr every consumer of A and B runs on the 256 x 256 kernel and
+  // reads them as upper-triangle tiles (mode 1): no mirrored tile is
+  // written.  Otherwise the lower triangle is written as the mirror.
+  if (!qtr) { g.CT = g.C; g.ct_mat = matA; g.ldct = g.ldc; }
+  r.f[0] = nm * 2 * s * s * l; r.x[0] = nm * 2 * Sp * Sp * Lp * gram_frac; r.b[0] = nm * (s * l + s * s) * xsz;
+  // B = b A + c A A^T: M = N = K = S.
+  GemmArgs& pp = r.poly;
+  pp = g;
+  pp.xscale = nullptr;
+  pp.P = static_cast<const char*>(wb.A); pp.p_mat = matA; pp.ldp = cg.S * es;
+  pp.Q = pp.P; pp.q_mat = matA; pp.ldq = pp.ldp;
+  pp.k_slabs = cg.S * es / 128;
+  pp.E = pp.P; pp.e_mat = matA; pp.lde = pp.ldp;
+  pp.ET = pp.P; pp.et_mat = matA; pp.ldet = pp.ldp;  // A is symmetric
+  pp.C = static_cast<char*>(wb.B); pp.CT = qtr ? nullptr : pp.C;
+  pp.p_mode = pp.q_mode = qtr ? 1 : 0;
+  pp.alpha = b; pp.beta = c;
+  r.f[1] = nm * 2 * s * s * s; r.x[1] = nm * 2 * Sp * Sp * Sp * poly_frac; r.b[1] = nm * 2 * s * s * xsz;
+  // X' = a X + B X: M = S, N = L, K = S.  The second operand is X^T (N x K,
+  // K contiguous) on the 128 x 128 kernel, X itself (K x N) under qtr.
+  GemmArgs& u = r.upd;
+  u.P = static_cast<const char*>(wb.B); u.p_mat = matA; u.ldp = cg.S * es;
+  if (qtr) {
+    u.Q = X; u.q_mat = matX; u.ldq = cg.L * es;
+    u.p_mode = 1;  // B: upper-triangle tiles
+    u.q_mode = 2;  // X: K x N
+  } else {
+    u.Q = XTc; u.q_mat = matX; u.ldq = cg.S * es;
+  }
+  u.k_slabs = cg.S * es / 128;
+  u.tiles_m = ts; u.tiles_n = tl; u.syrk = 0; u.tiles_per_mat = ts * tl;
+  u.E = X; u.e_mat = matX; u.lde = cg.L * es;
+  u.alpha = a;
+  u.s = cg.s; u.l = cg.l;
+  u.xscale = k == 0 ? wb.xscale : nullptr;  // X1 = r (a X~ + B0 X~)
+  r.f[2] = nm * 2 * s * s * l; r.x[2] = nm * 2 * Sp * Sp * Lp;
+  r.last = k + 1 == K;
+  if (!r.last) {
+    u.C = static_cast<char*>(wb.X[cur ^ 1]); u.c_mat = matX; u.ldc = cg.L * es;
+    if (!qtr) { u.CT = static_cast<char*>(wb.XT[cur ^ 1]); u.ct_mat = matX; u.ldct = cg.S * es; }
+    // reads B, X (twice under qtr, else X^T and X); writes X' (and X'^T)
+    r.b[2] = nm * (s * s + (qtr ? 3 : 4) * s * l) * xsz;
+  } else {
+    u.desc = d_desc; u.final_kind = sc.final_kind; u.param_dtype = cg.param_dtype;
+    // reads B, X^T, X (and W); writes W or out
+    r.b[2] = nm * ((s * s + 2 * s * l) * xsz + s * l * (sc.final_kind == 0 ? 2 * psz : psz));
+  }
+  return r;
+}
+
+template <typename GT, typename XT>
+hipError_t run_chunk_t(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBuffers& wb,
+                       const StepScalars& sc, const float* coeffs, int K, hipStream_t st,
+                       LaunchTimer* timer) {
+  if (wb.sync) return run_small<GT, XT>(cg, d_desc, wb, sc, coeffs, K, st, timer);
+  hipError_t e = run_prologue_t<GT, XT>(cg, d_desc, wb, sc, coeffs, K, st, timer);
+  if (e != hipSuccess || K == 0) return e;
+  const bool qtr = !chunk_keeps_xt(cg.S, cg.L, sizeof(XT) == 4, K);
+  const int nmat = cg.nmat;
   int cur = 0;
   for (int k = 0; k < K; ++k) {
-    const float a = coeffs[3 * k], b = coeffs[3 * k + 1], c = coeffs[3 * k + 2];
-    const char* X = static_cast<const char*>(wb.X[cur]);
-    const char* XTc = static_cast<const char*>(wb.XT[cur]);
-    // A = X X^T: M = N = S, K = L.
-    GemmArgs g{};
-    g.P = X; g.p_mat = matX; g.ldp = cg.L * es;
-    g.Q = X; g.q_mat = matX; g.ldq = cg.L * es;
-    g.k_slabs = cg.L * es / 128;
-    g.tiles_m = ts; g.tiles_n = ts; g.syrk = 1; g.tiles_per_mat = ts * (ts + 1) / 2;
-    g.C = static_cast<char*>(wb.A); g.c_mat = matA; g.ldc = cg.S * es;
-    g.xscale = k == 0 ? wb.xscale : nullptr;  // A0 = r^2 X~ X~^T
-    // Under qtr every consumer of A and B runs on the 256 x 256 kernel and
-    // reads them as upper-triangle tiles (mode 1): no mirrored tile is
-    // written.  Otherwise the lower triangle is written as the mirror.
-    if (!qtr) { g.CT = g.C; g.ct_mat = matA; g.ldct = g.ldc; }
+    const StepProducts sp = step_products<XT>(cg, d_desc, wb, sc, coeffs, K, k, cur);
     {
       Timed tm(timer, KK_GRAM, st);
-      if ((e = launch_gemm<XT>(EPI_GRAM, g, nmat, st)) != hipSuccess) return e;
-      tm.done(nm * 2 * s * s * l, nm * 2 * Sp * Sp * Lp * gram_frac, nm * (s * l + s * s) * xsz);
+      if ((e = launch_gemm<XT>(EPI_GRAM, sp.gram, nmat, st)) != hipSuccess) return e;
+      tm.done(sp.f[0], sp.x[0], sp.b[0]);
     }
-    // B = b A + c A A^T: M = N = K = S.
-    GemmArgs p = g;
-    p.xscale = nullptr;
-    p.P = static_cast<const char*>(wb.A); p.p_mat = matA; p.ldp = cg.S * es;
-    p.Q = p.P; p.q_mat = matA; p.ldq = p.ldp;
-    p.k_slabs = cg.S * es / 128;
-    p.E = p.P; p.e_mat = matA; p.lde = p.ldp;
-    p.ET = p.P; p.et_mat = matA; p.ldet = p.ldp;  // A is symmetric
-    p.C = static_cast<char*>(wb.B); p.CT = qtr ? nullptr : p.C;
-    p.p_mode = p.q_mode = qtr ? 1 : 0;
-    p.alpha = b; p.beta = c;
     {
       Timed tm(timer, KK_POLY, st);
-      if ((e = launch_gemm<XT>(EPI_POLY, p, nmat, st)) != hipSuccess) return e;
-      tm.done(nm * 2 * s * s * s, nm * 2 * Sp * Sp * Sp * poly_frac, nm * 2 * s * s * xsz);
+      if ((e = launch_gemm<XT>(EPI_POLY, sp.poly, nmat, st)) != hipSuccess) return e;
+      tm.done(sp.f[1], sp.x[1], sp.b[1]);
     }
-    // X' = a X + B X: M = S, N = L, K = S.  The second operand is X^T (N x K,
-    // K contiguous) on the 128 x 128 kernel, X itself (K x N) under qtr.
-    GemmArgs u{};
-    u.P = static_cast<const char*>(wb.B); u.p_mat = matA; u.ldp = cg.S * es;
-    if (qtr) {
-      u.Q = X; u.q_mat = matX; u.ldq = cg.L * es;
-      u.p_mode = 1;  // B: upper-triangle tiles
-      u.q_mode = 2;  // X: K x N
-    } else {
-      u.Q = XTc; u.q_mat = matX; u.ldq = cg.S * es;
-    }
-    u.k_slabs = cg.S * es / 128;
-    u.tiles_m = ts; u.tiles_n = tl; u.syrk = 0; u.tiles_per_mat = ts * tl;
-    u.E = X; u.e_mat = matX; u.lde = cg.L * es;
-    u.alpha = a;
-    u.s = cg.s; u.l = cg.l;
-    u.xscale = k == 0 ? wb.xscale : nullptr;  // X1 = r (a X~ + B0 X~)
-    const double uf = nm * 2 * s * s * l, ufx = nm * 2 * Sp * Sp * Lp;
-    if (k + 1 < K) {
-      u.C = static_cast<char*>(wb.X[cur ^ 1]); u.c_mat = matX; u.ldc = cg.L * es;
-      if (!qtr) { u.CT = static_cast<char*>(wb.XT[cur ^ 1]); u.ct_mat = matX; u.ldct = cg.S * es; }
-      Timed tm(timer, KK_UPDATE, st);
-      if ((e = qtr ? launch_tile<CfgSquare>(EPI_UPDATE, u, nmat, st) : launch_gemm<XT>(EPI_UPDATE, u, nmat, st)) !=
+    {
+      const int epi = sp.last ? EPI_FINAL : EPI_UPDATE;
+      Timed tm(timer, sp.last ? KK_FINAL : KK_UPDATE, st);
+      if ((e = qtr ? launch_tile<CfgSquare>(epi, sp.upd, nmat, st) : launch_gemm<XT>(epi, sp.upd, nmat, st)) !=
           hipSuccess)
         return e;
-      // reads B, X (twice under qtr, else X^T and X); writes X' (and X'^T)
-      tm.done(uf, ufx, nm * (s * s + (qtr ? 3 : 4) * s * l) * xsz);
-      cur ^= 1;
-    } else {
-      u.desc = d_desc; u.final_kind = sc.final_kind; u.param_dtype = cg.param_dtype;
-      Timed tm(timer, KK_FINAL, st);
-      if ((e = qtr ? launch_tile<CfgSquare>(EPI_FINAL, u, nmat, st) : launch_gemm<XT>(EPI_FINAL, u, nmat, st)) !=
-          hipSuccess)
-        return e;
-      // reads B, X^T, X (and W); writes W or out
-      tm.done(uf, ufx, nm * ((s * s + 2 * s * l) * xsz + s * l * (sc.final_kind == 0 ? 2 * psz : psz)));
+      tm.done(sp.f[2], sp.x[2], sp.b[2]);
     }
+    cur ^= 1;
   }
   return hipSuccess;
 }
@@ -2288,6 +2401,48 @@ hipError_t run_chunk(const ChunkGeom& cg, const MatDesc* d_desc, const ChunkBuff
   }
   return gbf ? run_chunk_t<uint16_t, uint16_t>(cg, d_desc, wb, sc, coeffs, K, st, timer)
              : run_chunk_t<float, uint16_t>(cg, d_desc, wb, sc, coeffs, K, st, timer);
+}
+
+bool group_eligible(const ChunkGeom& cg, int K) {
+  return !cg.ns_f32 && K > 0 && cg.S % 256 == 0 && cg.L % 256 == 0 && tile_rows_fit(cg.S, cg.L, 2) &&
+         !chunk_is_small(cg.s, cg.l, false);
+}
+
+hipError_t run_group(const GroupMember* m, int n, const StepScalars& sc, int K, hipStream_t st,
+                     LaunchTimer* timer) {
+  if (n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
+  for (int c = 0; c < n; ++c)
+    if (!group_eligible(m[c].geom, K) || m[c].geom.param_dtype != m[0].geom.param_dtype) return hipErrorInvalidValue;
+  hipError_t e;
+  for (int c = 0; c < n; ++c) {
+    const bool gbf = m[c].geom.grad_dtype == DT_BF16;
+    e = gbf ? run_prologue_t<uint16_t, uint16_t>(m[c].geom, m[c].desc, m[c].wb, sc, m[c].coeffs, K, st, timer)
+            : run_prologue_t<float, uint16_t>(m[c].geom, m[c].desc, m[c].wb, sc, m[c].coeffs, K, st, timer);
+    if (e != hipSuccess) return e;
+  }
+  int cur = 0;
+  for (int k = 0; k < K; ++k) {
+    GemmArgs ga[3][kMaxGroup];
+    int nm[kMaxGroup];
+    double f[3] = {0, 0, 0}, x[3] = {0, 0, 0}, b[3] = {0, 0, 0};
+    bool last = false;
+    for (int c = 0; c < n; ++c) {
+      const StepProducts sp = step_products<uint16_t>(m[c].geom, m[c].desc, m[c].wb, sc, m[c].coeffs, K, k, cur);
+      ga[0][c] = sp.gram; ga[1][c] = sp.poly; ga[2][c] = sp.upd;
+      nm[c] = m[c].geom.nmat;
+      for (int q = 0; q < 3; ++q) { f[q] += sp.f[q]; x[q] += sp.x[q]; b[q] += sp.b[q]; }
+      last = sp.last;
+    }
+    const int kinds[3] = {KK_GRAM, KK_POLY, last ? KK_FINAL : KK_UPDATE};
+    const int epis[3] = {EPI_GRAM, EPI_POLY, last ? EPI_FINAL : EPI_UPDATE};
+    for (int q = 0; q < 3; ++q) {
+      Timed tm(timer, kinds[q], st);
+      if ((e = launch_group<CfgSquare>(epis[q], ga[q], nm, n, st)) != hipSuccess) return e;
+      tm.done(f[q], x[q], b[q]);
+    }
+    cur ^= 1;
+  }
+  return hipSuccess;
 }
 
 // ---------------------------------------------------------------------------
