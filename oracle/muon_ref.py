@@ -132,6 +132,11 @@ class MuonHParams:
     # 0: multiply by 0.2*sqrt(max(m, n)) (Sec. 2.3); 1: no rescale;
     # 2: sqrt(max(1, m/n)) (the original Muon rule; see rms_scale).
     scale_mode: int = 0
+    # Post-processing after the update (Sec. 6.2 lists it among the
+    # pluggable stages, QK-clip being the example): the updated matrix is
+    # multiplied by this factor, which the caller derives (for QK-clip, per
+    # attention head from its logits).  1: none.
+    post_scale: float = 1.0
 
     def coefficient_table(self) -> List[Tuple[float, float, float]]:
         return coefficient_table(self.ns_steps, self.ns_coeffs)
@@ -222,10 +227,12 @@ def rms_scale(rows: int, cols: int, scale_mode: int = 0) -> float:
 
 
 def apply_update(W: np.ndarray, O: np.ndarray, lr: float, weight_decay: float,
-                 scale: float) -> np.ndarray:
-    """Decoupled weight decay and update: W' = (1 - lr*wd) W - lr*scale*O."""
+                 scale: float, post_scale: float = 1.0) -> np.ndarray:
+    """Decoupled weight decay and update, W' = (1 - lr*wd) W - lr*scale*O,
+    then the post-processing stage (Sec. 6.2): W' multiplied by post_scale."""
     W = np.asarray(W, dtype=np.float64)
-    return (1.0 - lr * weight_decay) * W - lr * scale * np.asarray(O, dtype=np.float64)
+    W_new = (1.0 - lr * weight_decay) * W - lr * scale * np.asarray(O, dtype=np.float64)
+    return W_new if post_scale == 1.0 else post_scale * W_new
 
 
 @dataclass
@@ -243,7 +250,7 @@ def muon_step_matrix(W, g, buf, hp: MuonHParams) -> StepResult:
     buf_new, u = momentum_update(g, buf, hp.beta, hp.nesterov)
     O = orthogonalize(u, hp.ns_steps, hp.ns_coeffs, hp.eps)
     scale = rms_scale(W.shape[0], W.shape[1], hp.scale_mode)
-    return StepResult(apply_update(W, O, hp.lr, hp.weight_decay, scale), buf_new, O)
+    return StepResult(apply_update(W, O, hp.lr, hp.weight_decay, scale, hp.post_scale), buf_new, O)
 
 
 def muon_step(params: Sequence[np.ndarray], grads: Sequence[np.ndarray],

@@ -82,8 +82,16 @@ def _scale_min_side(rows, cols, scale_mode=0):
     return 0.2 * float(np.sqrt(min(rows, cols))) if scale_mode == 0 else 1.0
 
 
-def _apply_decay_after(W, O, lr, weight_decay, scale):
-    return (1.0 - lr * weight_decay) * (np.asarray(W, float) - lr * scale * np.asarray(O, float))
+def _apply_decay_after(W, O, lr, weight_decay, scale, post_scale=1.0):
+    return post_scale * (1.0 - lr * weight_decay) * (np.asarray(W, float) - lr * scale * np.asarray(O, float))
+
+
+def _apply_post_scale_update_only(W, O, lr, weight_decay, scale, post_scale=1.0):
+    return (1.0 - lr * weight_decay) * np.asarray(W, float) - post_scale * lr * scale * np.asarray(O, float)
+
+
+def _apply_post_scale_decay_only(W, O, lr, weight_decay, scale, post_scale=1.0):
+    return post_scale * (1.0 - lr * weight_decay) * np.asarray(W, float) - lr * scale * np.asarray(O, float)
 
 
 def _round_bf16_via_f32(x):
@@ -106,6 +114,8 @@ def _run_all_pins():
         ("diag", pins.test_ns_diagonal_reduces_to_scalars, {}),
         ("apply_scale", pins.test_apply_scale_uses_long_side, {"shape": (6, 9)}),
         ("zero_update", pins.test_apply_zero_update_is_pure_decay, {}),
+        ("post_scale_hand", pins.test_post_scale_hand_example, {}),
+        ("post_scale_decay", pins.test_post_scale_applies_to_the_decayed_weight, {}),
         ("legacy_orthogonal", pins.test_legacy_values_on_orthogonal_input, {"n": 128}),
         ("legacy_vector", pins.test_legacy_value_on_vectors, {"shape": (1, 37)}),
         ("legacy_rank_one", pins.test_legacy_value_on_rank_one, {}),
@@ -134,6 +144,8 @@ MUTANTS = {
     "nesterov_old_buf": ("momentum_update", _momentum_bad_nesterov),
     "scale_min_side": ("rms_scale", _scale_min_side),
     "decay_after_update": ("apply_update", _apply_decay_after),
+    "post_scale_update_only": ("apply_update", _apply_post_scale_update_only),
+    "post_scale_decay_only": ("apply_update", _apply_post_scale_decay_only),
     "bf16_double_round": ("round_to_bf16", _round_bf16_via_f32),
     # one digit off in each coefficient of the default table
     "legacy_a_typo": ("LEGACY_QUINTIC", (3.4454, -4.7750, 2.0315)),

@@ -358,6 +358,31 @@ def test_whole_step_hand_example():
         np.testing.assert_allclose(r.W_new.ravel(), v(key), rtol=0, atol=1e-14)
 
 
+def test_post_scale_hand_example():
+    # the post-processing stage multiplies the updated matrix: the hand-worked
+    # 1x2 step (tests/golden/hand_step_1x2.txt) with a factor of 0.25, which
+    # is exact in binary, gives a quarter of the worked W' (both terms
+    # scaled: the decay of W and the update)
+    fx = _read_fixture("hand_step_1x2.txt")
+    v = lambda k: np.array(fx[k][0], dtype=float)
+    W, g, buf = v("W")[None, :], v("g")[None, :], v("buf")[None, :]
+    for wd, key in ((0.0, "W_new_wd0"), (0.5, "W_new_wd0.5")):
+        hp = ref.MuonHParams(lr=float(fx["lr"][0][0]), beta=float(fx["beta"][0][0]),
+                             weight_decay=wd, eps=float(fx["eps"][0][0]), ns_steps=1,
+                             ns_coeffs=[tuple(v("coeffs"))], post_scale=0.25)
+        r = ref.muon_step_matrix(W, g, buf, hp)
+        np.testing.assert_allclose(r.W_new.ravel(), 0.25 * v(key), rtol=0, atol=1e-14)
+        np.testing.assert_array_equal(r.buf_new.ravel(), v("buf_new"))   # the momentum is not scaled
+
+
+def test_post_scale_applies_to_the_decayed_weight():
+    # zero gradient and momentum: O = 0 and W' = post_scale (1 - lr wd) W;
+    # W = [1, 2], lr = 0.5, wd = 0.5, post_scale = 0.5: (1 - 0.25) 0.5 = 0.375
+    hp = ref.MuonHParams(lr=0.5, weight_decay=0.5, post_scale=0.5)
+    r = ref.muon_step_matrix(np.array([[1.0, 2.0]]), np.zeros((1, 2)), np.zeros((1, 2)), hp)
+    np.testing.assert_array_equal(r.W_new, [[0.375, 0.75]])
+
+
 def test_apply_zero_update_is_pure_decay():
     rng = np.random.default_rng(10)
     W = rng.standard_normal((6, 9))
