@@ -65,7 +65,7 @@
 extern "C" {
 #endif
 
-#define MUON_HIP_ABI_VERSION 2
+#define MUON_HIP_ABI_VERSION 3
 
 typedef struct muon_handle* muon_handle_t;
 
@@ -117,7 +117,13 @@ typedef struct {
                               of blocks * block_stride), else >= the span of a plane */
   int32_t momentum_dense;  /* 0: momentum has param's view; 1: momentum is a
                               dense batch x rows x cols array */
-  int32_t reserved;        /* must be 0 */
+  float post_scale;        /* post-processing stage (Sec. 6.2 names QK-clip as
+                              one): the updated matrix is multiplied by this
+                              factor, W' = post_scale * ((1 - lr*wd) W -
+                              lr*scale*O), e.g. a per-head query/key factor
+                              the caller derives from its attention logits
+                              (one entry per head through row-block views).
+                              0: none (1); otherwise finite and > 0 */
   /* Per-parameter configuration (Sec. 6.2: step count, coefficients and
    * scaling are per-parameter stages).  Entries whose tables hold the same
    * values are batched together; different tables never share a batch. */

@@ -35,7 +35,7 @@ class MuonParam(ctypes.Structure):
                 ("param_dtype", ctypes.c_int), ("grad_dtype", ctypes.c_int),
                 ("row_block", ctypes.c_int64), ("block_stride", ctypes.c_int64),
                 ("plane_stride", ctypes.c_int64), ("momentum_dense", ctypes.c_int32),
-                ("reserved", ctypes.c_int32), ("ns_coeffs", ctypes.POINTER(ctypes.c_float)),
+                ("post_scale", ctypes.c_float), ("ns_coeffs", ctypes.POINTER(ctypes.c_float)),
                 ("ns_steps", ctypes.c_int32), ("scale_mode", ctypes.c_int32)]
 
 
@@ -214,19 +214,22 @@ def _view(x):
     return t, E, rows, N, ld, rb, bs, ps
 
 
-def params_array(params, grads, moms, entry_coeffs=None, entry_scale_modes=None):
+def params_array(params, grads, moms, entry_coeffs=None, entry_scale_modes=None, entry_post_scales=None):
     """(MuonParam[], keepalive) for lists of logical matrices (see _view).
     grad takes the param's view; momentum takes it too, or is a dense
     [M, N] / [E, M, N] tensor.  entry_coeffs[i] (a K x 3 table) and
     entry_scale_modes[i] override the call's for entry i; None keeps the
-    call's.  Keep the second item alive during the call."""
+    call's.  entry_post_scales[i] multiplies entry i's updated matrix (the
+    post-processing stage, e.g. a QK-clip factor); None: none.  Keep the
+    second item alive during the call."""
     import torch
     if not (len(params) == len(grads) == len(moms)):
         raise ValueError("params, grads and momenta must have equal length")
     n = len(params)
     entry_coeffs = entry_coeffs or [None] * n
     entry_scale_modes = entry_scale_modes or [None] * n
-    if len(entry_coeffs) != n or len(entry_scale_modes) != n:
+    entry_post_scales = entry_post_scales or [None] * n
+    if len(entry_coeffs) != n or len(entry_scale_modes) != n or len(entry_post_scales) != n:
         raise ValueError("per-entry options need one item per entry")
     arr = (MuonParam * max(1, n))()
     keep = []
@@ -250,8 +253,9 @@ def params_array(params, grads, moms, entry_coeffs=None, entry_scale_modes=None)
             ctab = (ctypes.c_float * max(1, len(flat)))(*flat)
             keep.append(ctab)
         smode = 0 if entry_scale_modes[i] is None else 1 + int(entry_scale_modes[i])
+        post = 0.0 if entry_post_scales[i] is None else float(entry_post_scales[i])
         arr[i] = MuonParam(vw[0].data_ptr(), vg[0].data_ptr(), vm[0].data_ptr(), rows, cols, batch,
-                           ld, _dtype_code(vw[0]), _dtype_code(vg[0]), rb, bs, ps, mdense, 0,
+                           ld, _dtype_code(vw[0]), _dtype_code(vg[0]), rb, bs, ps, mdense, post,
                            ctypes.cast(ctab, ctypes.POINTER(ctypes.c_float)) if ctab else None,
                            csteps, smode)
     return arr, keep
@@ -343,11 +347,12 @@ class Muon:
         return int(self.lib.muon_workspace_bytes(self.h))
 
     def step(self, params, grads, moms, stream=None, entry_coeffs=None, entry_scale_modes=None,
-             **hp_kw):
+             entry_post_scales=None, **hp_kw):
         """In place: momentum and params updated, grads read (muon_step).
-        entry_coeffs / entry_scale_modes: optional per-entry overrides."""
+        entry_coeffs / entry_scale_modes / entry_post_scales: optional
+        per-entry overrides (see params_array)."""
         _check_device(list(params) + list(grads) + list(moms), self.device)
-        arr, keep_e = params_array(params, grads, moms, entry_coeffs, entry_scale_modes)
+        arr, keep_e = params_array(params, grads, moms, entry_coeffs, entry_scale_modes, entry_post_scales)
         hp, keep = make_hparams(**hp_kw)
         self._check(self.lib.muon_step(self.h, arr, len(params), ctypes.byref(hp),
                                        ctypes.c_void_p(_stream_ptr(stream))))

@@ -159,6 +159,7 @@ struct Item {
   int64_t ld, rb, bs, ld_b, bs_b;
   int32_t cset;            // coefficient table (index into the call's table list)
   int32_t scale_mode;      // 0: 0.2 sqrt(max(m, n)); 1: none; 2: sqrt(max(1, m/n))
+  double post_scale;       // factor applied to the updated matrix (1: none)
 };
 
 // The distinct coefficient tables of a call: [0] is the call's own table,
@@ -361,8 +362,12 @@ muon_status_t validate_step(const muon_param_t* params, int64_t n, const muon_hp
       msg.set("entry %lld: negative stride", (long long)i);
       return MUON_ERR_INVALID_ARGUMENT;
     }
-    if ((p.momentum_dense != 0 && p.momentum_dense != 1) || p.reserved != 0) {
-      msg.set("entry %lld: momentum_dense must be 0 or 1 and reserved 0", (long long)i);
+    if (p.momentum_dense != 0 && p.momentum_dense != 1) {
+      msg.set("entry %lld: momentum_dense must be 0 or 1", (long long)i);
+      return MUON_ERR_INVALID_ARGUMENT;
+    }
+    if (p.post_scale != 0.f && !(std::isfinite(p.post_scale) && p.post_scale > 0.f)) {
+      msg.set("entry %lld: post_scale must be 0 (none) or finite and > 0", (long long)i);
       return MUON_ERR_INVALID_ARGUMENT;
     }
     const int64_t ld = p.ld ? p.ld : p.cols;
@@ -446,6 +451,7 @@ muon_status_t validate_step(const muon_param_t* params, int64_t n, const muon_hp
         it.bs_b = mdense ? rb * p.cols : bs;
         it.cset = cset;
         it.scale_mode = smode;
+        it.post_scale = p.post_scale != 0.f ? double(p.post_scale) : 1.0;
         // row blocks that follow each other at the row stride are no blocks
         if (it.bs == rb * it.ld && it.bs_b == rb * it.ld_b) {
           it.rb = p.rows;
@@ -500,6 +506,7 @@ Item orth_item(const void* in, void* out, int64_t rows, int64_t cols, int dtype,
   set_dense(it);
   it.cset = 0;
   it.scale_mode = 1;
+  it.post_scale = 1.0;
   return it;
 }
 
@@ -859,8 +866,9 @@ MatDesc make_desc(const Item& it, double lr, double wd) {
   double scale = 1.0;
   if (it.scale_mode == 0) scale = 0.2 * std::sqrt(double(std::max(it.rows, it.cols)));
   else if (it.scale_mode == 2) scale = std::sqrt(std::max(1.0, double(it.rows) / double(it.cols)));
-  d.upd_scale = float(lr * scale);
-  d.decay = float(1.0 - lr * wd);
+  // the post-processing factor multiplies both terms of the update
+  d.upd_scale = float(it.post_scale * lr * scale);
+  d.decay = float(it.post_scale * (1.0 - lr * wd));
   return d;
 }
 

@@ -39,7 +39,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.muon_abi_version() == 2
+    assert lib.muon_abi_version() == 3
     for code, name in B.STATUS.items():
         assert lib.muon_status_string(code).decode() == name
 
@@ -101,7 +101,9 @@ def test_validation_accepts_good_request(lib):
     (lambda e: setattr(e, "row_block", -1), 1),
     (lambda e: (setattr(e, "row_block", 4), setattr(e, "block_stride", 3 * 16)), 1),  # blocks overlap
     (lambda e: setattr(e, "momentum_dense", 2), 1),
-    (lambda e: setattr(e, "reserved", 1), 1),
+    (lambda e: setattr(e, "post_scale", -0.5), 1),
+    (lambda e: setattr(e, "post_scale", float("nan")), 1),
+    (lambda e: setattr(e, "post_scale", float("inf")), 1),
     (lambda e: setattr(e, "scale_mode", 4), 1),
     (lambda e: setattr(e, "scale_mode", -1), 1),
     (lambda e: setattr(e, "momentum", e.momentum + 2), 1),   # misaligned fp32
@@ -114,6 +116,13 @@ def test_validation_rejects_bad_entry(lib, mutate, expect):
     st, msg = B.validate_step(es, hp())
     assert st == expect, msg
     assert msg
+
+
+def test_validation_accepts_post_scales(lib):
+    es = entries([(64, 32), (16, 16)])
+    es[0].post_scale = 0.0      # none
+    es[1].post_scale = 0.7
+    assert B.validate_step(es, hp())[0] == 0
 
 
 def test_validation_rejects_cross_entry_overlap(lib):

@@ -97,3 +97,45 @@ def test_original_muon_scale_on_the_call(muon):
         err, rho = w_gate(to_host(Wd[i]), r.W_new, W0, "bf16")
         print(f"scale mode 2 {s}: err {err:.3e} (rho {rho:.1e})", flush=True)
         assert err <= tol_for("bf16", s) + rho, (s, err, rho)
+
+
+@pytest.mark.parametrize("hd,d", [(64, 256), (256, 1024)])
+def test_post_scale_per_head_qk_clip(muon, hd, d):
+    # A QK-clip-style post-processing stage (Sec. 6.2): each head's query and
+    # key slices of a fused [H, 3, hd, d] QKV weight are separate entries
+    # (zero-copy views) with their own factor; values take none.  64 x 256
+    # runs on the fused small-matrix launch, 256 x 1024 on the tile kernels.
+    import torch
+    H = 4
+    shape = (H, 3, hd, d)
+    Wf = synth.draw(shape, 0.02, "bf16", rng(90, hd, 0))
+    gf = synth.draw(shape, 1e-3, "bf16", rng(90, hd, 1))
+    mf = synth.draw(shape, 1e-3, "f32", rng(90, hd, 2))
+    eta = [0.5, 0.8, 1.0, 0.65]                      # per-head clip factors
+    post = [[np.sqrt(e), np.sqrt(e), None] for e in eta]
+    hp = ref.MuonHParams(lr=0.02, beta=0.95, weight_decay=0.01)
+    results = {}
+    for use in (True, False):
+        Wd, gd, md = to_dev(Wf, "bf16"), to_dev(gf, "bf16"), to_dev(mf, "f32")
+        P = [Wd[h, j] for h in range(H) for j in range(3)]
+        G = [gd[h, j] for h in range(H) for j in range(3)]
+        M = [md[h, j] for h in range(H) for j in range(3)]
+        scales = [post[h][j] for h in range(H) for j in range(3)] if use else None
+        muon.step(P, G, M, lr=hp.lr, beta=hp.beta, weight_decay=hp.weight_decay, entry_post_scales=scales)
+        torch.cuda.synchronize()
+        results[use] = (to_host(Wd), to_bits(Wd), to_host(md))
+    W0 = decode(Wf, "bf16")
+    for h in range(H):
+        for j in range(3):
+            r = ref.muon_step_matrix(W0[h, j], decode(gf[h, j], "bf16"), np.asarray(mf[h, j], np.float64),
+                                     ref.MuonHParams(lr=hp.lr, beta=hp.beta, weight_decay=hp.weight_decay,
+                                                     post_scale=post[h][j] or 1.0))
+            err, rho = w_gate(results[True][0][h, j], r.W_new, W0[h, j], "bf16")
+            # the gate is relative to this entry's change, which the factor makes large
+            print(f"post scale {post[h][j]} head {h} slice {j} ({hd}x{d}): W err {err:.3e} (rho {rho:.1e})", flush=True)
+            assert err <= tol_for("bf16", (hd, d)) + rho, (h, j, err, rho)
+            assert rel(results[True][2][h, j], r.buf_new) <= MOMENTUM_TOL
+            if post[h][j] is None:   # untouched entries: the bits of the plain call
+                assert np.array_equal(results[True][1][h, j], results[False][1][h, j]), (h, j)
+    # the momentum does not depend on the stage
+    assert np.array_equal(results[True][2], results[False][2])
