@@ -1002,13 +1002,18 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   // The polynomial adds alpha = b/c times A and scales by beta = c at the
   // end; with c = 0 the launch keeps the epilogue path (e_loop = 0).
   constexpr bool EUPD = QTR;
+  constexpr int EPS = (BN / WN) / 64;           // P slabs holding a wave's columns of A
+  static_assert(EPS == 1 || EPS == 2, "A term: one or two slabs per wave");
+  constexpr int EJ = BJ / EPS;                  // 32-column blocks per such slab
   const bool epoly = EPI == EPI_POLY && ga.e_loop != 0;
   int e_ks0 = -1, e_ks1 = -1;
   if (EUPD) {
     e_ks0 = bm * (BM / 64) + 2 * wm;
     e_ks1 = e_ks0 + 1;
   } else if (epoly) {
-    e_ks0 = bn * (BN / 64) + wn;
+    // the wave's BN / WN columns are EPS slabs of 64 k
+    e_ks0 = bn * (BN / 64) + wn * EPS;
+    if (EPS > 1) e_ks1 = e_ks0 + 1;
   }
   int eo[BJ][2];
   {
@@ -1022,27 +1027,30 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
                       ((2 * (wn * (BN / WN) + 32 * j) + 32 * (G & 1) + 8 * (L & 3)) ^ ((L >> 2) << 6));
         else       // P slab: row r holds chunk c at c ^ ((r >> 1) % 8)
           eo[j][gp] = (wm * (BM / WM) + 4 * (G >> 1) + (L >> 2)) * SLAB +
-                      (((4 * j + 2 * (G & 1) + ((L >> 1) & 1)) ^ (4 * gp + 2 * (G >> 1) + (L >> 3))) << 4) +
+                      (((4 * (j % EJ) + 2 * (G & 1) + ((L >> 1) & 1)) ^ (4 * gp + 2 * (G >> 1) + (L >> 3))) << 4) +
                       8 * (L & 1);
       }
   }
-  auto add_e = [&](const char* sp, auto i0c, auto nic) __attribute__((always_inline)) {
+  // Rows [i0, i0 + ni) and 32-column blocks [j0, j0 + nj) of the wave's
+  // accumulators take the term from the slab at sp.
+  auto add_e = [&](const char* sp, auto i0c, auto nic, auto j0c, auto njc) __attribute__((always_inline)) {
     constexpr int i0 = decltype(i0c)::value, ni = decltype(nic)::value;
+    constexpr int j0 = decltype(j0c)::value, nj = decltype(njc)::value;
     static_for<ni>([&](auto II) {
       constexpr int i = i0 + decltype(II)::value;
-      uint2 ev[BJ][4];
-      static_for<BJ>([&](auto J) {
+      uint2 ev[nj][4];
+      static_for<nj>([&](auto J) {
         static_for<4>([&](auto Gc) {
-          constexpr int j = decltype(J)::value, g = decltype(Gc)::value;
-          ev[j][g] = EUPD ? tr_read_b64(sp + eo[j][0] + (32 * (i & 1) + 8 * g) * 512)
-                          : tr_read_b64(sp + eo[j][g & 1] + (32 * i + 8 * g) * SLAB);
+          constexpr int jj = decltype(J)::value, j = j0 + jj, g = decltype(Gc)::value;
+          ev[jj][g] = EUPD ? tr_read_b64(sp + eo[j][0] + (32 * (i & 1) + 8 * g) * 512)
+                           : tr_read_b64(sp + eo[j][g & 1] + (32 * i + 8 * g) * SLAB);
         });
       });
-      static_for<BJ>([&](auto J) {
+      static_for<nj>([&](auto J) {
         static_for<4>([&](auto Gc) {
-          constexpr int j = decltype(J)::value, g = decltype(Gc)::value;
+          constexpr int jj = decltype(J)::value, j = j0 + jj, g = decltype(Gc)::value;
           float e[4];
-          unpack_bf16x4(ev[j][g], e);
+          unpack_bf16x4(ev[jj][g], e);
           f32x16_t& c = acc[i][j];
           c[4 * g + 0] = fmaf(ga.alpha, e[0], c[4 * g + 0]);
           c[4 * g + 1] = fmaf(ga.alpha, e[1], c[4 * g + 1]);
@@ -1124,10 +1132,13 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
       if (ks == e_ks0 || ks == e_ks1) {  // wave-uniform; at most twice a tile
         __builtin_amdgcn_sched_barrier(0);
         if constexpr (EUPD) {
-          if (ks == e_ks0) add_e(sp, I_<0>{}, I_<2>{});
-          else add_e(sp, I_<2>{}, I_<2>{});
+          if (ks == e_ks0) add_e(sp, I_<0>{}, I_<2>{}, I_<0>{}, I_<BJ>{});
+          else add_e(sp, I_<2>{}, I_<2>{}, I_<0>{}, I_<BJ>{});
+        } else if constexpr (EPS == 1) {
+          add_e(sp, I_<0>{}, I_<BI>{}, I_<0>{}, I_<BJ>{});
         } else {
-          add_e(sp, I_<0>{}, I_<BI>{});
+          if (ks == e_ks0) add_e(sp, I_<0>{}, I_<BI>{}, I_<0>{}, I_<EJ>{});
+          else add_e(sp, I_<0>{}, I_<BI>{}, I_<EJ>{}, I_<EJ>{});
         }
       }
     }
@@ -1165,11 +1176,11 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   };
   using T_ = std::true_type;
   using F_ = std::false_type;
-  static_assert(NLP + NLQ == 8, "slab 0 wait below counts 8 load instructions per slab");
   issue(0);
   if (EARLY && nk > 1) {
     issue(1);
-    asm volatile("s_waitcnt vmcnt(8)" ::: "memory");  // slab 0 has landed, slab 1 may not
+    // slab 0 has landed, slab 1 (NLP + NLQ loads) may not
+    asm volatile("s_waitcnt vmcnt(%0)" :: "n"(NLP + NLQ) : "memory");
   } else {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   }
@@ -1309,28 +1320,30 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
   // (every wave finished its operand-slab reads before the last slab's
   // barrier, so the staging area, which overlaps the slabs, is free)
   if (stage_w) {
-    static_assert(BM * BN * 2 / 1024 == 16 * NW, "W tile: 16 load instructions per wave");
+    constexpr int KW = BM * BN * 2 / 1024 / NW;   // load instructions per wave
+    static_assert(KW * NW * 1024 == BM * BN * 2, "W tile: whole instructions per wave");
     const char* wb = static_cast<const char*>(md->W) + (static_cast<int64_t>(wr0) * md->ld + wc0) * 2;
     const uint32_t ldw = static_cast<uint32_t>(md->ld) * 2;
     const uint32_t lds0 = lds_offset(smem);
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      const int row = 2 * (wave * 16 + k) + lane / 32;
+    for (int k = 0; k < KW; ++k) {
+      const int row = 2 * (wave * KW + k) + lane / 32;
       const int c = (lane % 32) ^ (((row & 3) << 2) | ((row >> 2) & 3));
-      load_lds16(wb, static_cast<uint32_t>(row) * ldw + static_cast<uint32_t>(c * 16), lds0 + (wave * 16 + k) * 1024);
+      load_lds16(wb, static_cast<uint32_t>(row) * ldw + static_cast<uint32_t>(c * 16), lds0 + (wave * KW + k) * 1024);
     }
   }
   if (e_epi && stage_c) {
     // a wave instruction fills 2 staged rows (1 KB); lane l: row 2k + l/32,
     // position l % 32, which holds chunk (l % 32) ^ 4*(row % 4)
-    static_assert(BM * BN * 2 / 1024 == 16 * NW, "E tile: 16 load instructions per wave");
+    constexpr int KE = BM * BN * 2 / 1024 / NW;   // load instructions per wave
+    static_assert(KE * NW * 1024 == BM * BN * 2, "E tile: whole instructions per wave");
     const char* eb = E + static_cast<int64_t>(bm) * BM * ga.lde + bn * BN * 2;
     const uint32_t lds0 = lds_offset(smem);
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      const int row = 2 * (wave * 16 + k) + lane / 32;
+    for (int k = 0; k < KE; ++k) {
+      const int row = 2 * (wave * KE + k) + lane / 32;
       const int c = (lane % 32) ^ ((row & 3) << 2);
-      load_lds16(eb, static_cast<uint32_t>(row * ga.lde + c * 16), lds0 + (wave * 16 + k) * 1024);
+      load_lds16(eb, static_cast<uint32_t>(row * ga.lde + c * 16), lds0 + (wave * KE + k) * 1024);
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -1450,7 +1463,8 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
     const int G = lane >> 4, t = lane & 15;
     const int ra = ((t & 3) * 8 + (t >> 2)) * TST;     // column offset of this lane's first address
     const int rrow = t & 3, rcol = 8 * (t >> 2);       // what it receives
-    static_assert(BM * BN * 2 / 1024 == 16 * NW, "copy-out: 16 instructions per wave");
+    constexpr int KC = BM * BN * 2 / 1024 / NW;   // store instructions per wave
+    static_assert(KC * NW * 1024 == BM * BN * 2, "copy-out: whole instructions per wave");
     auto out_row = [&](int it, auto diagc) __attribute__((always_inline)) {
       const int task = it * NW + wave;                 // 4 rows x 128 columns
       const int R = 4 * (task >> 1), C0 = 128 * (task & 1) + 32 * G;
@@ -1473,10 +1487,10 @@ __device__ __forceinline__ void gemm_tile_body(const GemmArgs& ga, char* smem, i
       store_out(reinterpret_cast<u32x4_t*>(C + static_cast<int64_t>(bm * BM + row) * ga.ldc + (bn * BN + c) * 2), v);
     };
     if (diag) {
-      for (int it = 0; it < 16; ++it) out_row(it, std::true_type{});
+      for (int it = 0; it < KC; ++it) out_row(it, std::true_type{});
     } else {
 #pragma unroll
-      for (int it = 0; it < 16; ++it) out_row(it, std::false_type{});
+      for (int it = 0; it < KC; ++it) out_row(it, std::false_type{});
     }
     __syncthreads();  // the next tile's loads overwrite the staging area
   } else if (stage_c) {
