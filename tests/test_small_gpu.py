@@ -48,18 +48,21 @@ def test_small_orthogonalize_matches_oracle(muon, steps):
         assert err <= TOL["f32"], (sh, err)
 
 
-def test_small_shapes_bf16_path_match_oracle(muon):
+@pytest.mark.parametrize("steps", [5, 1, 0])
+def test_small_shapes_bf16_path_match_oracle(muon, steps):
+    # K = 0 writes X0 = r u from the prologue; K = 1 applies r in the last
+    # step's products themselves
     import torch
     shapes = [(s, l) for s in SHORT for l in LONG_BF16] + [(l, s) for s in (7, 128) for l in LONG_BF16]
-    G = [synth.draw(sh, 1.0, "bf16", rng(50, i)) for i, sh in enumerate(shapes)]
+    G = [synth.draw(sh, 1.0, "bf16", rng(50, steps, i)) for i, sh in enumerate(shapes)]
     ins = [to_dev(g, "bf16") for g in G]
     outs = [torch.full_like(t, float("nan")) for t in ins]
-    muon.orthogonalize(ins, outs, ns_precision="bf16")
+    muon.orthogonalize(ins, outs, ns_steps=steps, ns_precision="bf16")
     torch.cuda.synchronize()
     for sh, g, o in zip(shapes, G, outs):
         x = decode(g, "bf16")
-        err, gate = o_gate(to_host(o), ref.orthogonalize(x, 5), "bf16", "bf16", G=x)
-        print(f"small bf16 {sh}: O err {err:.2e} (gate {gate:.2e})", flush=True)
+        err, gate = o_gate(to_host(o), ref.orthogonalize(x, steps), "bf16", "bf16", steps, G=x)
+        print(f"small bf16 K={steps} {sh}: O err {err:.2e} (gate {gate:.2e})", flush=True)
         assert err <= gate, (sh, err, gate)
 
 
