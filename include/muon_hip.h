@@ -21,6 +21,9 @@
  *              1 (mode 1), or sqrt(max(1, rows/cols)) (mode 2, the rule of
  *              the original Muon method that Sec. 2.3 and Sec. 6.2 keep as a
  *              configurable legacy stage)
+ *   post       the updated matrix multiplied by the entry's post_scale
+ *              (a post-processing stage of Sec. 6.2, e.g. QK-clip factors;
+ *              default none)
  *   eps        added to the Frobenius norm, outside the square root
  *   square     matrices (rows == cols) are not transposed
  *   ns_coeffs  NULL selects the constant quintic (3.4445, -4.7750, 2.0315).
