@@ -3,8 +3,8 @@ to 1300 on a side (tall, wide, square, and multiples of 128 and 256 so that
 every kernel path is taken: the fused small-matrix launch, the 128 x 128
 and 256 x 256 tile kernels, grouped launches), random parameter and
 gradient dtypes, both Newton-Schulz precisions, 0 to 5 steps, per-entry
-scale modes and post-processing factors, some entries as column-range views
-of a wider weight.  Every matrix of a call is compared with the oracle at
+coefficient tables, scale modes and post-processing factors, some entries
+as column-range views of a wider weight.  Every matrix of a call is compared with the oracle at
 the gates of its precision."""
 import numpy as np
 import pytest
@@ -14,6 +14,10 @@ from paper_2609_21594_amd import synth
 from tests.gpu_util import MOMENTUM_TOL, decode, o_gate, rel, require_gpu, to_dev, to_host, tol_for, w_gate
 
 pytestmark = pytest.mark.gpu
+
+QUINTIC = (3.4445, -4.7750, 2.0315)
+# per-entry coefficient tables (None: the call's step count with the constant quintic)
+TABLES = [None, None, [(1.5, -0.5, 0.0)] * 3, [(15 / 8, -10 / 8, 3 / 8)] * 2 + [QUINTIC] * 2, []]
 
 
 @pytest.fixture(scope="module")
@@ -60,29 +64,32 @@ def test_random_calls_match_oracle(muon, case):
         post = [None, None, float(r.uniform(0.5, 1.0))][int(r.integers(3))]
         view = bool(r.integers(3) == 0)
         width = cols + (int(r.integers(1, 65)) if view else 0)   # a column range of a wider weight
+        table = TABLES[int(r.integers(len(TABLES)))]
         Wp = synth.draw((rows, width), 0.02, pdt, rng(case, i, 0))
         gp = synth.draw((rows, width), 1e-3, gdt, rng(case, i, 1))
         mp = synth.draw((rows, width), 1e-3, "f32", rng(case, i, 2))
         dW, dg, dm = to_dev(Wp, pdt), to_dev(gp, gdt), to_dev(mp, "f32")
         off = width - cols
         dev.append((dW, dg, dm, dW[:, off:], dg[:, off:], dm[:, off:]))
-        host.append((Wp, gp, mp, off, rows, cols, pdt, gdt, smode, post))
+        host.append((Wp, gp, mp, off, rows, cols, pdt, gdt, smode, post, table))
     muon.step([d[3] for d in dev], [d[4] for d in dev], [d[5] for d in dev],
               lr=hp.lr, beta=hp.beta, weight_decay=hp.weight_decay, ns_steps=steps,
               nesterov=hp.nesterov, ns_precision=prec,
-              entry_scale_modes=[h[8] for h in host], entry_post_scales=[h[9] for h in host])
+              entry_scale_modes=[h[8] for h in host], entry_post_scales=[h[9] for h in host],
+              entry_coeffs=[h[10] for h in host])
     torch.cuda.synchronize()
-    for i, ((dW, dg, dm, *_), (Wp, gp, mp, off, rows, cols, pdt, gdt, smode, post)) in enumerate(zip(dev, host)):
+    for i, ((dW, dg, dm, *_), (Wp, gp, mp, off, rows, cols, pdt, gdt, smode, post, table)) in enumerate(zip(dev, host)):
         W0 = decode(Wp, pdt)
-        hpi = ref.MuonHParams(lr=hp.lr, beta=hp.beta, weight_decay=hp.weight_decay, ns_steps=steps,
-                              nesterov=hp.nesterov, scale_mode=0 if smode is None else smode,
+        k_i = steps if table is None else len(table)
+        hpi = ref.MuonHParams(lr=hp.lr, beta=hp.beta, weight_decay=hp.weight_decay, ns_steps=k_i,
+                              ns_coeffs=table, nesterov=hp.nesterov, scale_mode=0 if smode is None else smode,
                               post_scale=1.0 if post is None else post)
         res = ref.muon_step_matrix(W0[:, off:], decode(gp, gdt)[:, off:], np.asarray(mp[:, off:], np.float64), hpi)
         got = to_host(dW)
         err, rho = w_gate(got[:, off:], res.W_new, W0[:, off:], pdt)
         u = ref.momentum_update(decode(gp, gdt)[:, off:], np.asarray(mp[:, off:], np.float64), hp.beta, hp.nesterov)[1]
-        gate = tol_for(prec, (rows, cols), steps, None, u)
-        print(f"case {case} {prec} K={steps} entry {i}: {rows}x{cols} {pdt}/{gdt} view={off > 0} "
+        gate = tol_for(prec, (rows, cols), k_i, table, u)
+        print(f"case {case} {prec} K={k_i} entry {i}: {rows}x{cols} {pdt}/{gdt} view={off > 0} "
               f"scale={smode} post={post}: W err {err:.2e} (gate {gate:.1e} + {rho:.1e})", flush=True)
         assert err <= gate + rho, (i, rows, cols, err, gate, rho)
         assert rel(to_host(dm)[:, off:], res.buf_new) <= MOMENTUM_TOL, i
